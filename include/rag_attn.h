@@ -1,0 +1,216 @@
+/*
+ * rag_attn.h -- C ABI of the MI355X (gfx950) attention library for the LLM
+ * synthesis step of a configuration-adaptive RAG system (METIS, arXiv
+ * 2412.10543).
+ *
+ * Why attention: synthesis dominates a RAG query's delay (retrieval is over
+ * 100x cheaper, Sec. "RAG systems and configurations"), and the three knobs the
+ * system adapts per query -- num_chunks, synthesis_method (stuff, map_reduce,
+ * map_rerank) and intermediate_length -- decide how many tokens that step
+ * prefills and decodes.  The served models (Sec. "Setup": a 7B model with 32
+ * query / 8 KV heads of size 128, a 70B model with 64 / 8) run on a serving
+ * engine with a paged KV cache, continuous batching and chunked prefill (Sec.
+ * "Joint configuration-scheduling adaptation", Sec. "Implementation").
+ *
+ * Conventions for every call:
+ *   - Tensors are bf16 unless noted and row-major; "device" pointers are HIP
+ *     device memory, "host" pointers host memory.  Every bf16 tensor pointer
+ *     must be 16-byte aligned.
+ *   - The caller owns every buffer, including workspaces.  The library never
+ *     allocates or frees device memory and keeps no pointer after a call
+ *     returns, apart from the work it has enqueued.
+ *   - Calls enqueue on `stream` (NULL = the null stream) and return; they
+ *     never synchronise (except in the debug mode below).
+ *   - Host-visible arguments are validated before anything is enqueued; a
+ *     failing call enqueues nothing and returns a negative rag_status.
+ *     rag_last_error() then gives a message (thread-local).  No C++ exception
+ *     crosses this boundary.
+ *   - The contents of device arrays (cu_seqlens, kv_lens, block tables) are
+ *     caller preconditions, checked only when the environment variable
+ *     RAG_ATTN_CHECK=1 is set (the call then copies them to the host
+ *     synchronously and returns RAG_ERR_INVALID_ARG on a violation).
+ *   - Calls are thread-safe; the only mutable global state is the
+ *     thread-local error message.
+ *
+ * Attention here is softmax(q k^T * softmax_scale) v per query row, with
+ * grouped-query heads (q head h reads kv head h / (num_q_heads / num_kv_heads))
+ * and causal masking aligned bottom-right: a sequence with nq query rows and
+ * nk keys lets query row i (0-based) see keys j <= (nk - nq) + i.  Inputs are
+ * bf16, products and softmax run in fp32, outputs are bf16 (rounded to
+ * nearest even).
+ */
+#ifndef RAG_ATTN_H
+#define RAG_ATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define RAG_ATTN_ABI_VERSION 1
+
+typedef enum {
+  RAG_OK = 0,
+  RAG_ERR_INVALID_ARG = -1, /* null pointer, negative size, bad enum, bad alignment,
+                               violated precondition (debug mode)              */
+  RAG_ERR_UNSUPPORTED = -2, /* valid but not implemented: head_dim not 64/128,
+                               block_size not 16, GQA group over 16 in decode  */
+  RAG_ERR_WORKSPACE = -3,   /* workspace missing or smaller than required     */
+  RAG_ERR_HIP = -4          /* a HIP call failed (launch error, debug copy)   */
+} rag_status;
+
+/* RAG_ATTN_ABI_VERSION of the loaded library. */
+int rag_abi_version(void);
+
+/* Message for the last non-OK status returned on the calling thread ("" if
+ * none).  The pointer stays valid until the next call on that thread. */
+const char *rag_last_error(void);
+
+/*
+ * Packed variable-length attention: the prefill of a batch of prompts
+ * assembled by rag_plan_prompts (one per stuff query, one per map_reduce
+ * mapper or map_rerank chunk, one per reduce call).
+ *
+ *   q      device [Tq, num_q_heads, head_dim]   Tq = cu_seqlens_q[num_seqs]
+ *   k, v   device [Tk, num_kv_heads, head_dim]  Tk = cu_seqlens_k[num_seqs]
+ *   o      device [Tq, num_q_heads, head_dim]   output, written in full
+ *   lse    device fp32 [num_q_heads, Tq] or NULL: natural-log sum of exp of
+ *          the scaled scores of each row (-inf for a row that sees no key)
+ *   cu_seqlens_q, cu_seqlens_k  device int32 [num_seqs + 1], non-decreasing,
+ *          starting at 0.  Sequence s owns q rows [cu_q[s], cu_q[s+1]) and
+ *          k/v rows [cu_k[s], cu_k[s+1]).  Precondition: with causal=1 each
+ *          sequence has nq <= nk (equal for a plain prefill).
+ *   max_seqlen_q  host upper bound of any nq (sizes the grid); max_seqlen_k
+ *          host upper bound of any nk.
+ *   causal 1: bottom-right causal mask; 0: every row sees all nk keys.
+ *
+ * Returns RAG_OK, RAG_ERR_INVALID_ARG (null q/k/v/o/cu pointer, num_seqs < 0,
+ * heads <= 0, num_q_heads % num_kv_heads != 0, causal not 0/1, misaligned
+ * pointer, max_seqlen < 0), RAG_ERR_UNSUPPORTED (head_dim not 64 or 128) or
+ * RAG_ERR_HIP.  num_seqs == 0 or max_seqlen_q == 0 is a no-op.
+ */
+rag_status rag_attn_prefill_varlen(const void *q, const void *k, const void *v,
+                                   void *o, float *lse,
+                                   const int32_t *cu_seqlens_q,
+                                   const int32_t *cu_seqlens_k,
+                                   int32_t num_seqs, int32_t max_seqlen_q,
+                                   int32_t max_seqlen_k, int32_t num_q_heads,
+                                   int32_t num_kv_heads, int32_t head_dim,
+                                   float softmax_scale, int32_t causal,
+                                   hipStream_t stream);
+
+/*
+ * Number of KV splits rag_attn_decode_paged uses for its decode rows when it
+ * is passed num_splits (0 = choose automatically), given the number of decode
+ * rows, kv heads and the block-table width.  Always >= 1.
+ */
+int32_t rag_attn_decode_num_splits(int32_t num_decode_seqs,
+                                   int32_t num_kv_heads,
+                                   int32_t max_blocks_per_seq,
+                                   int32_t block_size, int32_t num_splits);
+
+/*
+ * Bytes of workspace rag_attn_decode_paged needs for the same arguments (0
+ * when the decode rows use a single split).  Layout (library-internal): fp32
+ * partial outputs [num_decode_seqs, num_q_heads, splits, head_dim] followed by
+ * fp32 partial log-sum-exp values [num_decode_seqs, num_q_heads, splits].
+ */
+size_t rag_attn_decode_workspace_size(int32_t num_decode_seqs,
+                                      int32_t num_q_heads, int32_t num_kv_heads,
+                                      int32_t head_dim,
+                                      int32_t max_blocks_per_seq,
+                                      int32_t block_size, int32_t num_splits);
+
+/*
+ * Attention of query rows against a paged KV cache: one decode step of a
+ * batch, optionally mixed in the same launch with chunked-prefill pieces (the
+ * engine's continuous batching with chunked prefill).
+ *
+ *   q        device [Tq, num_q_heads, head_dim]
+ *   k_cache, v_cache  device [num_blocks, num_kv_heads, block_size, head_dim]
+ *   o        device [Tq, num_q_heads, head_dim]; output
+ *   block_tables  device int32 [num_seqs, max_blocks_per_seq]; entry b of row
+ *            s is the physical block holding keys [16b, 16b+16) of sequence
+ *            s.  Entries past ceil(kv_lens[s]/16) are never read.
+ *   kv_lens  device int32 [num_seqs]: keys of sequence s, counting those of
+ *            its own query rows (1 <= kv_len <= max_blocks_per_seq*16).
+ *   cu_seqlens_q  device int32 [num_seqs + 1] or NULL.
+ *            NULL: pure decode; sequence s has the single query row s
+ *            (Tq = num_seqs) and num_decode_seqs is ignored.
+ *            Non-NULL: mixed batch.  Sequences [0, num_decode_seqs) are decode
+ *            rows (cu[s+1] - cu[s] == 1); sequences [num_decode_seqs,
+ *            num_seqs) are chunked-prefill pieces whose nq = cu[s+1] - cu[s]
+ *            query rows (0 <= nq <= max_seqlen_q, nq <= kv_len) are the last
+ *            nq of their kv_len tokens.
+ *   num_blocks  physical blocks in the pool (bounds for debug checks).
+ *   block_size  must be 16.  head_dim 64 or 128.  The decode rows need
+ *            num_q_heads / num_kv_heads <= 16.
+ *   num_splits  0 = automatic; else the number of KV splits per decode row
+ *            (combined with a log-sum-exp merge).
+ *   workspace, workspace_bytes  device scratch of at least
+ *            rag_attn_decode_workspace_size(...) bytes (may be NULL when that
+ *            is 0); 256-byte aligned.  Overlapping calls must not share it.
+ *
+ * Every element of o for the Tq rows is written.  Returns RAG_OK,
+ * RAG_ERR_INVALID_ARG, RAG_ERR_UNSUPPORTED, RAG_ERR_WORKSPACE or RAG_ERR_HIP.
+ */
+rag_status rag_attn_decode_paged(const void *q, const void *k_cache,
+                                 const void *v_cache, void *o,
+                                 const int32_t *block_tables,
+                                 const int32_t *kv_lens,
+                                 const int32_t *cu_seqlens_q, int32_t num_seqs,
+                                 int32_t num_decode_seqs,
+                                 int32_t max_blocks_per_seq,
+                                 int32_t max_seqlen_q, int32_t num_blocks,
+                                 int32_t num_q_heads, int32_t num_kv_heads,
+                                 int32_t head_dim, int32_t block_size,
+                                 float softmax_scale, int32_t num_splits,
+                                 void *workspace, size_t workspace_bytes,
+                                 hipStream_t stream);
+
+/* Synthesis methods (Sec. "RAG systems and configurations"). */
+typedef enum {
+  RAG_STUFF = 0,             /* one prompt: all chunks, then the query       */
+  RAG_MAP_REDUCE_MAP = 1,    /* one prompt per chunk: chunk + query; each
+                                decodes intermediate_length summary tokens   */
+  RAG_MAP_REDUCE_REDUCE = 2, /* one prompt: the summaries, then the query    */
+  RAG_MAP_RERANK = 3         /* one prompt per chunk: chunk + query; each
+                                decodes an answer                            */
+} rag_synthesis;
+
+/*
+ * Host-only prompt planner: the packed-batch descriptor of the LLM calls a
+ * synthesis method issues for a list of queries.
+ *
+ *   query_len, num_chunks  host int32 [num_queries]: tokens of each query and
+ *            chunks retrieved for it.
+ *   chunk_len  tokens per chunk; intermediate_length  summary tokens per
+ *            mapper; answer_len  tokens decoded by answer-producing calls.
+ *   cu_seqlens_out  host int32 [capacity]: receives num_calls + 1 prefix
+ *            offsets of the prompt lengths.
+ *   num_seqs_out  host: number of calls.
+ *   decode_len_out  host int32 [capacity - 1] or NULL: tokens each call
+ *            decodes.
+ * Prompt lengths: stuff n*chunk_len + query_len; map_reduce map and
+ * map_rerank chunk_len + query_len per chunk; map_reduce reduce
+ * n*intermediate_length + query_len.
+ * Returns RAG_ERR_INVALID_ARG for a bad method, a null array, negative sizes
+ * or a 32-bit overflow of the total, RAG_ERR_WORKSPACE when capacity is too
+ * small (num_seqs_out still receives the number of calls).
+ */
+rag_status rag_plan_prompts(rag_synthesis method, int32_t num_queries,
+                            const int32_t *query_len, const int32_t *num_chunks,
+                            int32_t chunk_len, int32_t intermediate_length,
+                            int32_t answer_len, int32_t *cu_seqlens_out,
+                            int32_t capacity, int32_t *num_seqs_out,
+                            int32_t *decode_len_out);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RAG_ATTN_H */

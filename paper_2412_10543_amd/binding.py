@@ -1,0 +1,194 @@
+"""Thin Python binding of librag_attn.so (the C ABI in include/rag_attn.h).
+
+Argument marshalling only: every step of the attention path runs in the HIP
+library.  Tensors are torch tensors on the GPU (torch supplies device memory
+and the current HIP stream); shapes, dtypes and contiguity are checked here
+and everything else is left to the library's own validation.  There is no
+fallback: if the library is missing or was built for another target, loading
+raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import torch
+
+LIBRARY = os.path.join(os.path.dirname(os.path.abspath(__file__)), "librag_attn.so")
+
+RAG_OK = 0
+RAG_ERR_INVALID_ARG = -1
+RAG_ERR_UNSUPPORTED = -2
+RAG_ERR_WORKSPACE = -3
+RAG_ERR_HIP = -4
+
+RAG_STUFF = 0
+RAG_MAP_REDUCE_MAP = 1
+RAG_MAP_REDUCE_REDUCE = 2
+RAG_MAP_RERANK = 3
+METHOD_CODES = {"stuff": RAG_STUFF, "map_reduce_map": RAG_MAP_REDUCE_MAP,
+                "map_reduce_reduce": RAG_MAP_REDUCE_REDUCE, "map_rerank": RAG_MAP_RERANK}
+
+
+class RagError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"rag_attn status {status}: {message}")
+        self.status = status
+
+
+_i32 = ctypes.c_int32
+_i32p = ctypes.POINTER(ctypes.c_int32)
+_vp = ctypes.c_void_p
+_lib = None
+
+
+def exported_symbols():
+    return ["rag_abi_version", "rag_last_error", "rag_attn_prefill_varlen",
+            "rag_attn_decode_num_splits", "rag_attn_decode_workspace_size",
+            "rag_attn_decode_paged", "rag_plan_prompts"]
+
+
+def lib():
+    """Load (once) and return the ctypes handle of librag_attn.so."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIBRARY):
+        raise ImportError(f"{LIBRARY} is not built; run __graft_entry__.build() or "
+                          "python -m paper_2412_10543_amd.build")
+    L = ctypes.CDLL(LIBRARY)
+    L.rag_abi_version.restype = ctypes.c_int
+    L.rag_last_error.restype = ctypes.c_char_p
+    L.rag_attn_prefill_varlen.restype = ctypes.c_int
+    L.rag_attn_prefill_varlen.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _i32, _i32, _i32,
+                                          _i32, _i32, _i32, ctypes.c_float, _i32, _vp]
+    L.rag_attn_decode_num_splits.restype = _i32
+    L.rag_attn_decode_num_splits.argtypes = [_i32, _i32, _i32, _i32, _i32]
+    L.rag_attn_decode_workspace_size.restype = ctypes.c_size_t
+    L.rag_attn_decode_workspace_size.argtypes = [_i32, _i32, _i32, _i32, _i32, _i32, _i32]
+    L.rag_attn_decode_paged.restype = ctypes.c_int
+    L.rag_attn_decode_paged.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _i32, _i32, _i32,
+                                        _i32, _i32, _i32, _i32, _i32, _i32, ctypes.c_float,
+                                        _i32, _vp, ctypes.c_size_t, _vp]
+    L.rag_plan_prompts.restype = ctypes.c_int
+    L.rag_plan_prompts.argtypes = [ctypes.c_int, _i32, _i32p, _i32p, _i32, _i32, _i32, _i32p,
+                                   _i32, _i32p, _i32p]
+    _lib = L
+    return L
+
+
+def _check(status: int):
+    if status != RAG_OK:
+        raise RagError(status, lib().rag_last_error().decode())
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def _need(t, dtype, name, ndim=None):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if ndim is not None and t.dim() != ndim:
+        raise ValueError(f"{name} must have {ndim} dimensions")
+
+
+def rag_abi_version() -> int:
+    return lib().rag_abi_version()
+
+
+def rag_last_error() -> str:
+    return lib().rag_last_error().decode()
+
+
+def rag_attn_prefill_varlen(q, k, v, o, lse, cu_seqlens_q, cu_seqlens_k, max_seqlen_q,
+                            max_seqlen_k, softmax_scale, causal=True, stream=None) -> None:
+    """q, o [Tq, Hq, d]; k, v [Tk, Hkv, d] bf16; lse fp32 [Hq, Tq] or None;
+    cu_seqlens_* int32 [S+1] on the GPU."""
+    for t, n in ((q, "q"), (k, "k"), (v, "v"), (o, "o")):
+        _need(t, torch.bfloat16, n, 3)
+    _need(cu_seqlens_q, torch.int32, "cu_seqlens_q", 1)
+    _need(cu_seqlens_k, torch.int32, "cu_seqlens_k", 1)
+    if lse is not None:
+        _need(lse, torch.float32, "lse", 2)
+    _check(lib().rag_attn_prefill_varlen(
+        _ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), _ptr(cu_seqlens_q), _ptr(cu_seqlens_k),
+        cu_seqlens_q.numel() - 1, int(max_seqlen_q), int(max_seqlen_k), q.shape[1], k.shape[1],
+        q.shape[2], float(softmax_scale), int(bool(causal)), _stream(stream)))
+
+
+def rag_attn_decode_num_splits(num_decode_seqs, num_kv_heads, max_blocks_per_seq,
+                               block_size=16, num_splits=0) -> int:
+    return lib().rag_attn_decode_num_splits(num_decode_seqs, num_kv_heads, max_blocks_per_seq,
+                                            block_size, num_splits)
+
+
+def rag_attn_decode_workspace_size(num_decode_seqs, num_q_heads, num_kv_heads, head_dim,
+                                   max_blocks_per_seq, block_size=16, num_splits=0) -> int:
+    return lib().rag_attn_decode_workspace_size(num_decode_seqs, num_q_heads, num_kv_heads,
+                                                head_dim, max_blocks_per_seq, block_size,
+                                                num_splits)
+
+
+def rag_attn_decode_paged(q, k_cache, v_cache, o, block_tables, kv_lens, softmax_scale,
+                          cu_seqlens_q=None, num_decode_seqs=None, max_seqlen_q=1,
+                          num_splits=0, workspace=None, stream=None) -> None:
+    """q, o [Tq, Hq, d]; caches [num_blocks, Hkv, 16, d] bf16; block_tables
+    int32 [S, max_blocks]; kv_lens int32 [S]; cu_seqlens_q int32 [S+1] or
+    None; workspace a uint8 GPU tensor or None."""
+    for t, n in ((q, "q"), (o, "o")):
+        _need(t, torch.bfloat16, n, 3)
+    for t, n in ((k_cache, "k_cache"), (v_cache, "v_cache")):
+        _need(t, torch.bfloat16, n, 4)
+    _need(block_tables, torch.int32, "block_tables", 2)
+    _need(kv_lens, torch.int32, "kv_lens", 1)
+    if cu_seqlens_q is not None:
+        _need(cu_seqlens_q, torch.int32, "cu_seqlens_q", 1)
+    num_seqs = block_tables.shape[0]
+    if num_decode_seqs is None:
+        num_decode_seqs = num_seqs
+    ws_bytes = 0
+    if workspace is not None:
+        if not workspace.is_cuda or not workspace.is_contiguous():
+            raise ValueError("workspace must be a contiguous GPU tensor")
+        ws_bytes = workspace.numel() * workspace.element_size()
+    _check(lib().rag_attn_decode_paged(
+        _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(o), _ptr(block_tables), _ptr(kv_lens),
+        _ptr(cu_seqlens_q), num_seqs, int(num_decode_seqs), block_tables.shape[1],
+        int(max_seqlen_q), k_cache.shape[0], q.shape[1], k_cache.shape[1], q.shape[2],
+        k_cache.shape[2], float(softmax_scale), int(num_splits), _ptr(workspace), ws_bytes,
+        _stream(stream)))
+
+
+def rag_plan_prompts(method, query_len, num_chunks, chunk_len, intermediate_length=0,
+                     answer_len=0):
+    """Host planner.  Returns (cu_seqlens list, decode_len list)."""
+    code = METHOD_CODES[method] if isinstance(method, str) else int(method)
+    n = len(query_len)
+    ql = (_i32 * max(n, 1))(*query_len)
+    nc = (_i32 * max(n, 1))(*num_chunks)
+    count = _i32(0)
+    L = lib()
+    st = L.rag_plan_prompts(code, n, ql, nc, chunk_len, intermediate_length, answer_len, None, 0,
+                            ctypes.byref(count), None)
+    if st not in (RAG_OK, RAG_ERR_WORKSPACE):
+        _check(st)
+    cap = count.value + 1
+    cu = (_i32 * cap)()
+    dec = (_i32 * max(count.value, 1))()
+    _check(L.rag_plan_prompts(code, n, ql, nc, chunk_len, intermediate_length, answer_len, cu,
+                              cap, ctypes.byref(count), dec))
+    return list(cu), list(dec)[:count.value]

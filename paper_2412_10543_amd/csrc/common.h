@@ -1,0 +1,111 @@
+// Internal definitions shared by the gfx950 attention kernels and their host
+// launchers.  Not part of the public ABI (include/rag_attn.h is).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace rag {
+
+typedef uint16_t bf16_t;  // raw bf16 storage
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+constexpr int kWave = 64;
+constexpr int kNumXcd = 8;        // MI355X: 8 accelerator complex dies
+constexpr float kLog2e = 1.4426950408889634f;
+// Lazy rescaling: the running maximum used as the exponent reference is only
+// moved when a new score exceeds it by more than 2^kRescaleLog2 in the
+// exponentiated domain, so unnormalised weights stay <= 2^8 (fp32 and bf16
+// hold that exactly in range).
+constexpr float kRescaleLog2 = 8.0f;
+
+// ---- MFMA wrappers (gfx950 bf16, fp32 accumulate) --------------------------
+// 32x32x16: A lane l holds A[l%32][8*(l/32) .. +8], B lane l holds
+// B[8*(l/32) .. +8][l%32], C lane l holds C[8*(j/4) + 4*(l/32) + j%4][l%32]
+// for j = 0..15.
+__device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+// 16x16x32: A lane l holds A[l%16][8*(l/16) .. +8], B lane l holds
+// B[8*(l/16) .. +8][l%16], C lane l holds C[4*(l/16) + j][l%16], j = 0..3.
+__device__ __forceinline__ f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) {
+  return __builtin_bit_cast(bf16x8, v);
+}
+__device__ __forceinline__ u32x4 as_u32x4(bf16x8 v) {
+  return __builtin_bit_cast(u32x4, v);
+}
+
+// fp32 -> bf16, round to nearest even (v_cvt_pk_bf16_f32).
+__device__ __forceinline__ bf16x8 to_bf16x8(float a0, float a1, float a2, float a3,
+                                            float a4, float a5, float a6, float a7) {
+  f32x8 f = {a0, a1, a2, a3, a4, a5, a6, a7};
+  return __builtin_convertvector(f, bf16x8);
+}
+__device__ __forceinline__ bf16x4 to_bf16x4(float a0, float a1, float a2, float a3) {
+  f32x4 f = {a0, a1, a2, a3};
+  return __builtin_convertvector(f, bf16x4);
+}
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+__device__ __forceinline__ float wave_xor(float x, int mask) {
+  return __shfl_xor(x, mask, kWave);
+}
+
+__device__ __forceinline__ bool wave_any(bool p) {
+  return __builtin_amdgcn_ballot_w64(p) != 0;
+}
+
+__device__ __forceinline__ u32x4 load16(const void* p) {
+  return *reinterpret_cast<const u32x4*>(p);
+}
+
+// Workgroup index as seen by one XCD: the hardware deals consecutive
+// workgroup ids round-robin to the 8 XCDs, so id n runs on XCD n % 8.  The
+// returned index runs contiguously on each XCD, which keeps workgroups that
+// read the same K/V rows inside one XCD's L2.
+__device__ __forceinline__ void xcd_slot(int n, int& xcd, int& local) {
+  xcd = n % kNumXcd;
+  local = n / kNumXcd;
+}
+
+// Prefill tiling shared by host and device.
+constexpr int kPfBM = 128;          // query rows per workgroup
+constexpr int kPfBN = 64;           // keys per K/V tile
+constexpr int kPfThreads = 256;     // 4 waves x 32 query rows
+
+template <int D>
+struct PfLds {
+  static constexpr int kStrK = D + 8;        // bf16 per K row (16 B pad)
+  static constexpr int kStrV = kPfBN + 8;    // bf16 per transposed-V row
+  static constexpr int kElemsK = kPfBN * kStrK;
+  static constexpr int kElemsV = D * kStrV;
+  static constexpr int kElemsBuf = kElemsK + kElemsV;
+  static constexpr int kBytes = 2 * kElemsBuf * 2;   // two buffers of bf16
+};
+
+// Decode tiling: one wave per (sequence, kv head, split) unit, two 16-token
+// pages per step.
+constexpr int kDecThreads = 256;
+constexpr int kDecWaves = kDecThreads / kWave;
+constexpr int kDecMaxGroup = 16;           // q heads per kv head (MFMA N)
+
+template <int D>
+struct DecLds {
+  static constexpr int kStrV = 32 + 8;       // bf16 per transposed-V row
+  static constexpr int kElemsWave = D * kStrV;
+  static constexpr int kBytes = kDecWaves * kElemsWave * 2;
+};
+
+}  // namespace rag

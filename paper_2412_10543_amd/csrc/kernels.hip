@@ -1,0 +1,285 @@
+// gfx950 kernels of the RAG-synthesis attention path and their launchers:
+//   prefill_varlen_kernel  packed variable-length prefill (dense K/V)
+//   paged_kernel           decode rows against a paged KV cache, optionally
+//                          with chunked-prefill pieces in the same launch
+//   combine_kernel         log-sum-exp merge of split-KV partial results
+#include <algorithm>
+#include <climits>
+
+#include "common.h"
+#include "decode_unit.h"
+#include "launch.h"
+#include "prefill_tile.h"
+
+namespace rag {
+
+// ---------------------------------------------------------------------------
+// Work order of prefill tiles.  A "stream" is one (sequence, kv head) pair;
+// all q heads of its GQA group and all its query tiles read the same K/V.
+// Stream sigma runs on XCD sigma % 8, so every XCD gets the same mix of
+// sequences (and, with 8 kv heads, exactly one kv head of each).  On an XCD
+// the order is: stream, then query tile from the last (most keys) to the
+// first, then the q heads of the group -- the workgroups resident on one XCD
+// at a time share K/V tiles through its L2.
+// ---------------------------------------------------------------------------
+struct TileCoord {
+  int seq, kvh, head, qt;
+  bool valid;
+};
+
+__device__ __forceinline__ TileCoord prefill_coord(int block, int num_streams, int hkv,
+                                                   int group, int n_qt) {
+  int xcd, local;
+  xcd_slot(block, xcd, local);
+  const int g = local % group;
+  const int rest = local / group;
+  const int tile_rank = rest % n_qt;
+  const int r = rest / n_qt;
+  const int stream = xcd + kNumXcd * r;
+  TileCoord t;
+  t.valid = stream < num_streams;
+  t.seq = stream / hkv;
+  t.kvh = stream % hkv;
+  t.head = t.kvh * group + g;
+  t.qt = n_qt - 1 - tile_rank;
+  return t;
+}
+
+int64_t prefill_grid(int num_seqs, int hkv, int group, int max_seqlen_q) {
+  const int64_t streams = (int64_t)num_seqs * hkv;
+  const int64_t per_xcd = (streams + kNumXcd - 1) / kNumXcd;
+  const int64_t n_qt = (max_seqlen_q + kPfBM - 1) / kPfBM;
+  return (int64_t)kNumXcd * per_xcd * n_qt * group;
+}
+
+int64_t paged_prefill_grid(int num_pieces, int hkv, int group, int max_seqlen_q) {
+  return prefill_grid(num_pieces, hkv, group, max_seqlen_q);
+}
+
+int64_t paged_decode_grid(int num_decode, int hkv, int num_splits) {
+  const int64_t units = (int64_t)num_decode * hkv * num_splits;
+  return (units + kDecWaves - 1) / kDecWaves;
+}
+
+template <int D>
+__global__ __launch_bounds__(kPfThreads, 2) void prefill_varlen_kernel(
+    const bf16_t* __restrict__ q, const bf16_t* __restrict__ k,
+    const bf16_t* __restrict__ v, bf16_t* __restrict__ o, float* __restrict__ lse,
+    const int32_t* __restrict__ cu_q, const int32_t* __restrict__ cu_k, int num_seqs,
+    int hq, int hkv, int n_qt, float scale, int causal) {
+  __shared__ __attribute__((aligned(16))) bf16_t lds[PfLds<D>::kBytes / 2];
+  const int group = hq / hkv;
+  const TileCoord tc = prefill_coord(blockIdx.x, num_seqs * hkv, hkv, group, n_qt);
+  if (!tc.valid) return;
+  const int qb = cu_q[tc.seq], nq = cu_q[tc.seq + 1] - qb;
+  const int kb = cu_k[tc.seq], nk = cu_k[tc.seq + 1] - kb;
+  if (tc.qt * kPfBM >= nq) return;
+  const int tq = cu_q[num_seqs];
+  const size_t qs = (size_t)hq * D;
+  DenseKV kv{k + ((size_t)kb * hkv + tc.kvh) * D, v + ((size_t)kb * hkv + tc.kvh) * D,
+             (size_t)hkv * D};
+  prefill_tile<D>(q + ((size_t)qb * hq + tc.head) * D, qs, o + ((size_t)qb * hq + tc.head) * D,
+                  qs, lse ? lse + (size_t)tc.head * tq + qb : nullptr, kv, nq, nk, tc.qt, scale,
+                  causal, lds);
+}
+
+// ---------------------------------------------------------------------------
+// Paged kernel.  Blocks [0, n_pf_blocks) are chunked-prefill tiles (mixed
+// batches only); the rest hold four decode units each, one per wave.  Decode
+// unit u covers split sp = u / (num_decode * hkv) of (sequence, kv head)
+// u % (num_decode * hkv); split sp of a sequence with P pages is the page
+// range [sp * pps, min((sp + 1) * pps, P)).
+// ---------------------------------------------------------------------------
+struct PagedKernelArgs {
+  const bf16_t* q;
+  const bf16_t* kc;
+  const bf16_t* vc;
+  bf16_t* o;
+  const int32_t* tables;
+  const int32_t* kv_lens;
+  const int32_t* cu_q;
+  float* part_o;
+  float* part_lse;
+  int num_seqs, num_decode, max_blocks, hq, hkv, num_splits, pps;
+  int n_pf_blocks, n_qt;
+  float scale;
+};
+
+template <int D, bool kMixed>
+__global__ __launch_bounds__(256, 2) void paged_kernel(PagedKernelArgs a) {
+  constexpr int kLdsBytes =
+      kMixed ? (PfLds<D>::kBytes > DecLds<D>::kBytes ? PfLds<D>::kBytes : DecLds<D>::kBytes)
+             : DecLds<D>::kBytes;
+  __shared__ __attribute__((aligned(16))) bf16_t lds[kLdsBytes / 2];
+  const int group = a.hq / a.hkv;
+  const size_t block_stride = (size_t)a.hkv * 16 * D;
+  int block = blockIdx.x;
+  if constexpr (kMixed) {
+    if (block < a.n_pf_blocks) {
+      const int num_pieces = a.num_seqs - a.num_decode;
+      const TileCoord tc = prefill_coord(block, num_pieces * a.hkv, a.hkv, group, a.n_qt);
+      if (!tc.valid) return;
+      const int s = a.num_decode + tc.seq;
+      const int qb = a.cu_q[s], nq = a.cu_q[s + 1] - qb;
+      if (tc.qt * kPfBM >= nq) return;
+      const int nk = a.kv_lens[s];
+      const size_t qs = (size_t)a.hq * D;
+      PagedKV<D> kv{a.kc + (size_t)tc.kvh * 16 * D, a.vc + (size_t)tc.kvh * 16 * D,
+                    a.tables + (size_t)s * a.max_blocks, block_stride};
+      prefill_tile<D>(a.q + ((size_t)qb * a.hq + tc.head) * D, qs,
+                      a.o + ((size_t)qb * a.hq + tc.head) * D, qs, nullptr, kv, nq, nk, tc.qt,
+                      a.scale, 1, lds);
+      return;
+    }
+    block -= a.n_pf_blocks;
+  }
+  const int wave = threadIdx.x >> 6;
+  const int64_t unit = (int64_t)block * kDecWaves + wave;
+  const int64_t pairs = (int64_t)a.num_decode * a.hkv;
+  if (unit >= pairs * a.num_splits) return;
+  const int sp = (int)(unit / pairs);
+  const int pr = (int)(unit % pairs);
+  const int s = pr / a.hkv, kvh = pr % a.hkv;
+  const int kv_len = a.kv_lens[s];
+  const int n_pages = (kv_len + 15) >> 4;
+  const int n_sp = (n_pages + a.pps - 1) / a.pps;
+  if (sp >= n_sp && sp > 0) return;
+  const int p_begin = sp * a.pps;
+  const int p_end = min(n_pages, p_begin + a.pps);
+  const int row = a.cu_q ? a.cu_q[s] : s;
+  const int h0 = kvh * group;
+  DecodeOut out;
+  if (n_sp <= 1) {
+    out.o = a.o + ((size_t)row * a.hq + h0) * D;
+    out.part_o = nullptr;
+    out.part_lse = nullptr;
+    out.head_stride_part = 0;
+  } else {
+    out.o = nullptr;
+    out.part_o = a.part_o + (((size_t)s * a.hq + h0) * a.num_splits + sp) * D;
+    out.part_lse = a.part_lse + ((size_t)s * a.hq + h0) * a.num_splits + sp;
+    out.head_stride_part = a.num_splits * D;
+  }
+  decode_unit<D>(a.q + ((size_t)row * a.hq + h0) * D, a.kc + (size_t)kvh * 16 * D,
+                 a.vc + (size_t)kvh * 16 * D, block_stride, a.tables + (size_t)s * a.max_blocks,
+                 kv_len, group, p_begin, p_end, a.scale, out,
+                 lds + wave * DecLds<D>::kElemsWave);
+}
+
+// One wave per (decode row, q head): merge that row's split partials in
+// split order.  Rows whose sequence used a single split were written by the
+// paged kernel and are skipped.
+template <int D>
+__global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ part_o,
+                                                      const float* __restrict__ part_lse,
+                                                      bf16_t* __restrict__ o,
+                                                      const int32_t* __restrict__ kv_lens,
+                                                      const int32_t* __restrict__ cu_q,
+                                                      int num_decode, int hq, int num_splits,
+                                                      int pps) {
+  constexpr int kPer = D / 64;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t idx = (int64_t)blockIdx.x * kDecWaves + wave;
+  if (idx >= (int64_t)num_decode * hq) return;
+  const int s = (int)(idx / hq), h = (int)(idx % hq);
+  const int n_pages = (kv_lens[s] + 15) >> 4;
+  const int n_sp = (n_pages + pps - 1) / pps;
+  if (n_sp <= 1) return;
+  const float* pl = part_lse + (size_t)idx * num_splits;
+  const float* po = part_o + (size_t)idx * num_splits * D;
+  float mx = -INFINITY;
+  for (int sp = 0; sp < n_sp; ++sp) mx = fmaxf(mx, pl[sp]);
+  float acc[kPer];
+#pragma unroll
+  for (int e = 0; e < kPer; ++e) acc[e] = 0.f;
+  float den = 0.f;
+  if (mx != -INFINITY) {
+    for (int sp = 0; sp < n_sp; ++sp) {
+      const float w = expf(pl[sp] - mx);
+      den += w;
+#pragma unroll
+      for (int e = 0; e < kPer; ++e) acc[e] += w * po[(size_t)sp * D + lane * kPer + e];
+    }
+  }
+  const float inv = den > 0.f ? 1.f / den : 0.f;
+  const int row = cu_q ? cu_q[s] : s;
+  bf16_t* orow = o + ((size_t)row * hq + h) * D + lane * kPer;
+#pragma unroll
+  for (int e = 0; e < kPer; ++e) {
+    const __bf16 b = (__bf16)(acc[e] * inv);
+    orow[e] = __builtin_bit_cast(bf16_t, b);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// launchers
+// ---------------------------------------------------------------------------
+template <int D>
+static hipError_t launch_prefill_d(const PrefillArgs& a, hipStream_t stream) {
+  const int group = a.hq / a.hkv;
+  const int64_t grid = prefill_grid(a.num_seqs, a.hkv, group, a.max_seqlen_q);
+  if (grid == 0) return hipSuccess;
+  const int n_qt = (a.max_seqlen_q + kPfBM - 1) / kPfBM;
+  hipLaunchKernelGGL(prefill_varlen_kernel<D>, dim3((unsigned)grid), dim3(kPfThreads), 0, stream,
+                     (const bf16_t*)a.q, (const bf16_t*)a.k, (const bf16_t*)a.v, (bf16_t*)a.o,
+                     a.lse, a.cu_q, a.cu_k, a.num_seqs, a.hq, a.hkv, n_qt, a.scale, a.causal);
+  return hipGetLastError();
+}
+
+hipError_t launch_prefill_varlen(const PrefillArgs& a, hipStream_t stream) {
+  return a.d == 64 ? launch_prefill_d<64>(a, stream) : launch_prefill_d<128>(a, stream);
+}
+
+template <int D>
+static hipError_t launch_paged_d(const PagedArgs& a, hipStream_t stream) {
+  const int group = a.hq / a.hkv;
+  PagedKernelArgs k;
+  k.q = (const bf16_t*)a.q;
+  k.kc = (const bf16_t*)a.k_cache;
+  k.vc = (const bf16_t*)a.v_cache;
+  k.o = (bf16_t*)a.o;
+  k.tables = a.block_tables;
+  k.kv_lens = a.kv_lens;
+  k.cu_q = a.cu_q;
+  k.part_o = a.part_o;
+  k.part_lse = a.part_lse;
+  k.num_seqs = a.num_seqs;
+  k.num_decode = a.num_decode;
+  k.max_blocks = a.max_blocks;
+  k.hq = a.hq;
+  k.hkv = a.hkv;
+  k.num_splits = a.num_splits;
+  k.pps = std::max(1, (a.max_blocks + a.num_splits - 1) / a.num_splits);
+  k.scale = a.scale;
+  const bool mixed = a.cu_q != nullptr && a.num_seqs > a.num_decode;
+  k.n_qt = mixed ? (a.max_seqlen_q + kPfBM - 1) / kPfBM : 0;
+  const int64_t pf = mixed ? paged_prefill_grid(a.num_seqs - a.num_decode, a.hkv, group,
+                                                a.max_seqlen_q)
+                           : 0;
+  k.n_pf_blocks = (int)pf;
+  const int64_t dec = paged_decode_grid(a.num_decode, a.hkv, a.num_splits);
+  const int64_t grid = pf + dec;
+  if (grid > 0) {
+    if (pf > 0)
+      hipLaunchKernelGGL((paged_kernel<D, true>), dim3((unsigned)grid), dim3(256), 0, stream, k);
+    else
+      hipLaunchKernelGGL((paged_kernel<D, false>), dim3((unsigned)grid), dim3(256), 0, stream, k);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  if (a.num_splits > 1 && a.num_decode > 0) {
+    const int64_t rows = (int64_t)a.num_decode * a.hq;
+    const int64_t cgrid = (rows + kDecWaves - 1) / kDecWaves;
+    hipLaunchKernelGGL(combine_kernel<D>, dim3((unsigned)cgrid), dim3(256), 0, stream, a.part_o,
+                       a.part_lse, (bf16_t*)a.o, a.kv_lens, a.cu_q, a.num_decode, a.hq,
+                       a.num_splits, k.pps);
+    return hipGetLastError();
+  }
+  return hipSuccess;
+}
+
+hipError_t launch_paged(const PagedArgs& a, hipStream_t stream) {
+  return a.d == 64 ? launch_paged_d<64>(a, stream) : launch_paged_d<128>(a, stream);
+}
+
+}  // namespace rag

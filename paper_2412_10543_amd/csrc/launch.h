@@ -1,0 +1,45 @@
+// Host-side launch descriptors for the gfx950 kernels (internal).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace rag {
+
+struct PrefillArgs {
+  const void* q;
+  const void* k;
+  const void* v;
+  void* o;
+  float* lse;
+  const int32_t* cu_q;
+  const int32_t* cu_k;
+  int num_seqs, max_seqlen_q, hq, hkv, d, causal;
+  float scale;
+};
+
+struct PagedArgs {
+  const void* q;
+  const void* k_cache;
+  const void* v_cache;
+  void* o;
+  const int32_t* block_tables;
+  const int32_t* kv_lens;
+  const int32_t* cu_q;          // null: pure decode
+  int num_seqs, num_decode, max_blocks, max_seqlen_q;
+  int hq, hkv, d, num_splits;
+  float scale;
+  float* part_o;                // workspace (null when num_splits == 1)
+  float* part_lse;
+};
+
+// Launch-grid sizes, exposed so the host can check them before launching.
+int64_t prefill_grid(int num_seqs, int hkv, int group, int max_seqlen_q);
+int64_t paged_prefill_grid(int num_pieces, int hkv, int group, int max_seqlen_q);
+int64_t paged_decode_grid(int num_decode, int hkv, int num_splits);
+
+hipError_t launch_prefill_varlen(const PrefillArgs& a, hipStream_t stream);
+hipError_t launch_paged(const PagedArgs& a, hipStream_t stream);
+
+}  // namespace rag

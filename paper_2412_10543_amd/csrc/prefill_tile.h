@@ -1,0 +1,258 @@
+// Causal (or full) attention of one 128-row query tile of one q head against
+// the keys of its sequence, for gfx950.
+//
+// Method: exact tiled attention with an online softmax (FlashAttention's
+// forward pass; the running-max rescaling of Milakov & Gimelshein), laid out
+// for CDNA4:
+//   * 4 waves, each owning 32 query rows; the wave keeps its Q rows in
+//     registers as the B operand of v_mfma_f32_32x32x16_bf16;
+//   * K/V tiles of 64 keys are staged through LDS, double-buffered, with one
+//     barrier per tile; global loads of tile t+1 are in flight while tile t
+//     is computed;
+//   * scores are computed transposed, S^T = K Q^T, so each lane owns one query
+//     row and its scores sit in the accumulator exactly where the B operand
+//     of the P.V product needs them (O^T = V^T P^T).  K rows are read from
+//     LDS in an order that swaps bits 2 and 3 of the row index, which makes
+//     accumulator element j of a 32-key block hold key 16*(j/8) + 8*half +
+//     j%8; V is written to LDS transposed ([d][key]) with matching order, so
+//     every MFMA operand is one 16-byte LDS read and nothing is shuffled
+//     between the two products;
+//   * softmax statistics in fp32 with exp2 and the scale folded into one
+//     FMA; the reference maximum is moved lazily (only when a score exceeds
+//     it by 2^8), which keeps rescales of the output off the common path;
+//   * masking only on tiles that cross the causal diagonal or the sequence
+//     end; tiles fully above the diagonal are skipped per wave.
+#pragma once
+
+#include "common.h"
+
+namespace rag {
+
+// K/V rows of one (sequence, kv head) stored densely: token j at k + j*stride.
+struct DenseKV {
+  const bf16_t* k;
+  const bf16_t* v;
+  size_t stride;
+  __device__ __forceinline__ const bf16_t* krow(int j) const { return k + (size_t)j * stride; }
+  __device__ __forceinline__ const bf16_t* vrow(int j) const { return v + (size_t)j * stride; }
+};
+
+// K/V rows of one (sequence, kv head) in a paged cache: token j lives in
+// physical block table[j / 16], slot j % 16.  k and v already point at the kv
+// head inside block 0; block_stride is the distance between blocks.
+template <int D>
+struct PagedKV {
+  const bf16_t* k;
+  const bf16_t* v;
+  const int32_t* table;
+  size_t block_stride;
+  __device__ __forceinline__ size_t off(int j) const {
+    return (size_t)table[j >> 4] * block_stride + (size_t)(j & 15) * D;
+  }
+  __device__ __forceinline__ const bf16_t* krow(int j) const { return k + off(j); }
+  __device__ __forceinline__ const bf16_t* vrow(int j) const { return v + off(j); }
+};
+
+// Row index inside a 32-key block whose scores land, after the S^T product,
+// where the P.V product's B operand expects them: bits 2 and 3 swapped.
+__device__ __forceinline__ int swap_bits23(int m) {
+  return (m & ~12) | ((m & 4) << 1) | ((m & 8) >> 1);
+}
+
+template <int D, class KV>
+__device__ __forceinline__ void prefill_tile(
+    const bf16_t* __restrict__ q, size_t q_stride,   // row 0 of this seq, this head
+    bf16_t* __restrict__ o, size_t o_stride,
+    float* __restrict__ lse,                         // lse of row 0 (stride 1) or null
+    const KV& kv, int nq, int nk, int qt, float scale, int causal,
+    bf16_t* __restrict__ lds) {
+  using L = PfLds<D>;
+  constexpr int kCh = D / 8;                  // 16-byte chunks per row
+  constexpr int kRowsPerIt = kPfThreads / kCh;
+  constexpr int kItK = kPfBN / kRowsPerIt;    // K loads per thread per tile
+  constexpr int kVk = kPfBN * kCh / kPfThreads;  // V keys per thread per tile
+  constexpr int kKs = D / 16;                 // MFMA k-steps over d
+  constexpr int kDt = D / 32;                 // 32-row d tiles of O^T
+
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6, lane = tid & 63;
+  const int l32 = lane & 31, half = lane >> 5;
+  const int q0 = qt * kPfBM;
+  const int off = nk - nq;                    // bottom-right causal offset
+  const int r0 = q0 + 32 * wave;
+  const int row = r0 + l32;
+
+  const int wg_last = min(q0 + kPfBM, nq) - 1;
+  const int kend = causal ? min(nk, wg_last + off + 1) : nk;
+  const int w_last = min(r0 + 32, nq) - 1;
+  const int kend_w = (r0 >= nq) ? 0 : (causal ? min(nk, w_last + off + 1) : nk);
+  const int n_tiles = kend > 0 ? (kend + kPfBN - 1) / kPfBN : 0;
+
+  // Q^T fragments (B operand): lane holds q[row][16*ks + 8*half .. +8].
+  bf16x8 qf[kKs];
+#pragma unroll
+  for (int ks = 0; ks < kKs; ++ks) {
+    u32x4 z = {0, 0, 0, 0};
+    qf[ks] = as_bf16x8(row < nq ? load16(q + (size_t)row * q_stride + ks * 16 + half * 8) : z);
+  }
+
+  f32x16 oacc[kDt];
+#pragma unroll
+  for (int dt = 0; dt < kDt; ++dt)
+#pragma unroll
+    for (int j = 0; j < 16; ++j) oacc[dt][j] = 0.f;
+
+  const float c = scale * kLog2e;
+  const float tau = kRescaleLog2 / c;
+  float m_used = -INFINITY;
+  float l = 0.f;
+
+  const int ld_ch = tid % kCh;
+  const int ld_row = tid / kCh;
+  u32x4 kreg[kItK], vreg[kVk];
+
+  auto load_tile = [&](int k0) {
+#pragma unroll
+    for (int it = 0; it < kItK; ++it) {
+      const int j = k0 + it * kRowsPerIt + ld_row;
+      u32x4 z = {0, 0, 0, 0};
+      kreg[it] = j < nk ? load16(kv.krow(j) + ld_ch * 8) : z;
+    }
+#pragma unroll
+    for (int e = 0; e < kVk; ++e) {
+      const int j = k0 + ld_row * kVk + e;
+      u32x4 z = {0, 0, 0, 0};
+      vreg[e] = j < nk ? load16(kv.vrow(j) + ld_ch * 8) : z;
+    }
+  };
+  auto store_tile = [&](int buf) {
+    bf16_t* kl = lds + buf * L::kElemsBuf;
+    bf16_t* vl = kl + L::kElemsK;
+#pragma unroll
+    for (int it = 0; it < kItK; ++it)
+      *reinterpret_cast<u32x4*>(kl + (it * kRowsPerIt + ld_row) * L::kStrK + ld_ch * 8) = kreg[it];
+    // transpose: element e of this thread's kVk key rows -> row d = 8*ld_ch+e
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const uint32_t sel = (e & 1) ? 0x07060302u : 0x05040100u;
+      bf16_t* dst = vl + (ld_ch * 8 + e) * L::kStrV + ld_row * kVk;
+      if constexpr (kVk == 4) {
+        u32x2 w = {__builtin_amdgcn_perm(vreg[1][e >> 1], vreg[0][e >> 1], sel),
+                   __builtin_amdgcn_perm(vreg[3][e >> 1], vreg[2][e >> 1], sel)};
+        *reinterpret_cast<u32x2*>(dst) = w;
+      } else {
+        static_assert(kVk == 2, "unsupported head size");
+        *reinterpret_cast<uint32_t*>(dst) =
+            __builtin_amdgcn_perm(vreg[1][e >> 1], vreg[0][e >> 1], sel);
+      }
+    }
+  };
+
+  if (n_tiles > 0) {
+    load_tile(0);
+    store_tile(0);
+  }
+  __syncthreads();
+
+  const int krow_sw = swap_bits23(l32);
+  for (int t = 0; t < n_tiles; ++t) {
+    const int k0 = t * kPfBN;
+    if (t + 1 < n_tiles) load_tile(k0 + kPfBN);
+    const bf16_t* kl = lds + (t & 1) * L::kElemsBuf;
+    const bf16_t* vl = kl + L::kElemsK;
+
+    if (k0 < kend_w) {
+      // ---- S^T = K Q^T for 64 keys x 32 rows -------------------------------
+      f32x16 s[2];
+#pragma unroll
+      for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+        for (int j = 0; j < 16; ++j) s[mt][j] = 0.f;
+#pragma unroll
+      for (int ks = 0; ks < kKs; ++ks) {
+#pragma unroll
+        for (int mt = 0; mt < 2; ++mt) {
+          const bf16x8 a = *reinterpret_cast<const bf16x8*>(
+              kl + (32 * mt + krow_sw) * L::kStrK + ks * 16 + half * 8);
+          s[mt] = mfma32(a, qf[ks], s[mt]);
+        }
+      }
+      // ---- mask (diagonal / ragged tiles only) -----------------------------
+      const bool need_mask = (k0 + kPfBN > nk) || (causal && k0 + kPfBN - 1 > r0 + off);
+      if (need_mask) {
+        const int lim = causal ? min(nk - 1, row + off) : nk - 1;
+#pragma unroll
+        for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+          for (int j = 0; j < 16; ++j) {
+            const int key = k0 + 32 * mt + 16 * (j >> 3) + 8 * half + (j & 7);
+            if (key > lim) s[mt][j] = -INFINITY;
+          }
+      }
+      // ---- online softmax ----------------------------------------------------
+      float tmax = s[0][0];
+#pragma unroll
+      for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+        for (int j = 0; j < 16; ++j) tmax = fmaxf(tmax, s[mt][j]);
+      tmax = fmaxf(tmax, wave_xor(tmax, 32));
+      if (wave_any(tmax > m_used + tau)) {
+        const float m_new = fmaxf(m_used, tmax);
+        const float alpha = (m_used == -INFINITY) ? 0.f : fast_exp2((m_used - m_new) * c);
+        l *= alpha;
+#pragma unroll
+        for (int dt = 0; dt < kDt; ++dt)
+#pragma unroll
+          for (int j = 0; j < 16; ++j) oacc[dt][j] *= alpha;
+        m_used = m_new;
+      }
+      const float mref = (m_used == -INFINITY) ? 0.f : m_used * c;
+#pragma unroll
+      for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+          const float p = fast_exp2(fmaf(s[mt][j], c, -mref));
+          s[mt][j] = p;
+          l += p;
+        }
+      // ---- O^T += V^T P^T ----------------------------------------------------
+#pragma unroll
+      for (int mt = 0; mt < 2; ++mt) {
+#pragma unroll
+        for (int s2 = 0; s2 < 2; ++s2) {
+          const int b = 8 * s2;
+          const bf16x8 pb = to_bf16x8(s[mt][b], s[mt][b + 1], s[mt][b + 2], s[mt][b + 3],
+                                      s[mt][b + 4], s[mt][b + 5], s[mt][b + 6], s[mt][b + 7]);
+#pragma unroll
+          for (int dt = 0; dt < kDt; ++dt) {
+            const bf16x8 a = *reinterpret_cast<const bf16x8*>(
+                vl + (32 * dt + l32) * L::kStrV + 32 * mt + 16 * s2 + 8 * half);
+            oacc[dt] = mfma32(a, pb, oacc[dt]);
+          }
+        }
+      }
+    }
+    if (t + 1 < n_tiles) store_tile((t + 1) & 1);
+    __syncthreads();
+  }
+
+  // ---- epilogue: normalise, store bf16 rows and the log-sum-exp -------------
+  const float lt = l + wave_xor(l, 32);
+  const float inv = lt > 0.f ? 1.f / lt : 0.f;
+  if (row < nq) {
+    bf16_t* orow = o + (size_t)row * o_stride;
+#pragma unroll
+    for (int dt = 0; dt < kDt; ++dt)
+#pragma unroll
+      for (int g4 = 0; g4 < 4; ++g4) {
+        const int d = 32 * dt + 8 * g4 + 4 * half;
+        const bf16x4 w = to_bf16x4(oacc[dt][4 * g4] * inv, oacc[dt][4 * g4 + 1] * inv,
+                                   oacc[dt][4 * g4 + 2] * inv, oacc[dt][4 * g4 + 3] * inv);
+        *reinterpret_cast<bf16x4*>(orow + d) = w;
+      }
+    if (lse != nullptr && half == 0)
+      lse[row] = lt > 0.f ? m_used * scale + __logf(lt) : -INFINITY;
+  }
+}
+
+}  // namespace rag

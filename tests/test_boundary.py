@@ -1,0 +1,160 @@
+"""The C ABI on the CPU: the library loads, exports every function the header
+declares, rejects bad host arguments with the documented status before
+enqueueing anything, and its prompt planner matches the oracle's.
+
+No call here reaches a kernel launch: every call either fails validation or is
+a documented no-op (num_seqs == 0), so no GPU is needed.
+"""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import plan_prompts as oracle_plan
+from paper_2412_10543_amd import binding
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "rag_attn.h")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(binding.LIBRARY),
+                                reason="librag_attn.so not built")
+
+FAKE = 0x100000  # 16- and 256-byte aligned address; never dereferenced on these paths
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(rag_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_header_declarations_exported():
+    L = binding.lib()
+    names = _declared()
+    assert names == sorted(binding.exported_symbols())
+    for n in names:
+        assert hasattr(L, n), f"{n} not exported"
+
+
+def test_abi_version():
+    assert binding.rag_abi_version() == 1
+
+
+def _prefill(**kw):
+    a = dict(q=FAKE, k=FAKE, v=FAKE, o=FAKE, lse=None, cu_q=FAKE, cu_k=FAKE, num_seqs=1,
+             max_q=16, max_k=16, hq=4, hkv=2, d=64, scale=0.125, causal=1)
+    a.update(kw)
+    return binding.lib().rag_attn_prefill_varlen(
+        a["q"], a["k"], a["v"], a["o"], a["lse"], a["cu_q"], a["cu_k"], a["num_seqs"],
+        a["max_q"], a["max_k"], a["hq"], a["hkv"], a["d"], a["scale"], a["causal"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(q=None), binding.RAG_ERR_INVALID_ARG),
+    (dict(cu_k=None), binding.RAG_ERR_INVALID_ARG),
+    (dict(num_seqs=-1), binding.RAG_ERR_INVALID_ARG),
+    (dict(hq=6, hkv=4), binding.RAG_ERR_INVALID_ARG),
+    (dict(hkv=0), binding.RAG_ERR_INVALID_ARG),
+    (dict(causal=2), binding.RAG_ERR_INVALID_ARG),
+    (dict(scale=0.0), binding.RAG_ERR_INVALID_ARG),
+    (dict(scale=float("nan")), binding.RAG_ERR_INVALID_ARG),
+    (dict(q=FAKE + 8), binding.RAG_ERR_INVALID_ARG),
+    (dict(d=96), binding.RAG_ERR_UNSUPPORTED),
+    (dict(d=256), binding.RAG_ERR_UNSUPPORTED),
+    (dict(num_seqs=0), binding.RAG_OK),
+    (dict(max_q=0), binding.RAG_OK),
+])
+def test_prefill_validation(kw, status):
+    assert _prefill(**kw) == status
+    if status != binding.RAG_OK:
+        assert binding.rag_last_error() != ""
+    else:
+        assert binding.rag_last_error() == ""
+
+
+def _decode(**kw):
+    a = dict(q=FAKE, kc=FAKE, vc=FAKE, o=FAKE, bt=FAKE, kl=FAKE, cu=None, num_seqs=4,
+             num_decode=4, max_blocks=64, max_q=1, num_blocks=300, hq=32, hkv=8, d=128, bs=16,
+             scale=0.088, splits=0, ws=None, ws_bytes=0)
+    a.update(kw)
+    return binding.lib().rag_attn_decode_paged(
+        a["q"], a["kc"], a["vc"], a["o"], a["bt"], a["kl"], a["cu"], a["num_seqs"],
+        a["num_decode"], a["max_blocks"], a["max_q"], a["num_blocks"], a["hq"], a["hkv"],
+        a["d"], a["bs"], a["scale"], a["splits"], a["ws"], a["ws_bytes"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(kc=None), binding.RAG_ERR_INVALID_ARG),
+    (dict(kl=None), binding.RAG_ERR_INVALID_ARG),
+    (dict(num_seqs=-2), binding.RAG_ERR_INVALID_ARG),
+    (dict(splits=-1), binding.RAG_ERR_INVALID_ARG),
+    (dict(hq=12, hkv=8), binding.RAG_ERR_INVALID_ARG),
+    (dict(o=FAKE + 2), binding.RAG_ERR_INVALID_ARG),
+    (dict(d=80), binding.RAG_ERR_UNSUPPORTED),
+    (dict(bs=32), binding.RAG_ERR_UNSUPPORTED),
+    (dict(hq=64, hkv=2), binding.RAG_ERR_UNSUPPORTED),       # group of 32 > 16
+    (dict(cu=FAKE, num_decode=5), binding.RAG_ERR_INVALID_ARG),
+    (dict(max_blocks=0), binding.RAG_ERR_INVALID_ARG),
+    (dict(splits=4), binding.RAG_ERR_WORKSPACE),               # no workspace given
+    (dict(splits=4, ws=FAKE, ws_bytes=1024), binding.RAG_ERR_WORKSPACE),
+    (dict(splits=4, ws=FAKE + 64, ws_bytes=1 << 30), binding.RAG_ERR_INVALID_ARG),
+    (dict(num_seqs=0), binding.RAG_OK),
+])
+def test_decode_validation(kw, status):
+    assert _decode(**kw) == status
+
+
+def test_split_policy():
+    ns = binding.rag_attn_decode_num_splits
+    # one split never needs a workspace
+    assert ns(2560, 8, 40, 16, 1) == 1
+    assert binding.rag_attn_decode_workspace_size(2560, 32, 8, 128, 40, 16, 1) == 0
+    for nd, hkv, mb in [(16, 8, 653), (4, 8, 2260), (320, 8, 40), (256, 8, 2048), (1, 2, 19),
+                        (1, 1, 1), (3, 4, 7)]:
+        n = ns(nd, hkv, mb)
+        assert 1 <= n <= mb
+        pps = -(-mb // n)
+        assert -(-mb // pps) == n, "every split of the longest sequence is non-empty"
+        ws = binding.rag_attn_decode_workspace_size(nd, hkv * 4, hkv, 128, mb)
+        if n == 1:
+            assert ws == 0
+        else:
+            assert ws >= nd * hkv * 4 * n * 129 * 4
+    # requested counts are honoured up to one split per block
+    assert ns(16, 8, 653, 16, 7) == 7
+    assert ns(16, 8, 5, 16, 64) == 5
+
+
+@pytest.mark.parametrize("method", ["stuff", "map_reduce_map", "map_reduce_reduce", "map_rerank"])
+def test_planner_matches_oracle(method):
+    r = np.random.Generator(np.random.PCG64(7))
+    for trial in range(20):
+        nq = int(r.integers(0, 12))
+        ql = [int(x) for x in r.integers(1, 200, size=nq)]
+        nc = [int(x) for x in r.integers(0, 36, size=nq)]
+        C, IL, A = int(r.integers(1, 2048)), int(r.integers(0, 300)), int(r.integers(0, 256))
+        cu, dec = binding.rag_plan_prompts(method, ql, nc, C, IL, A)
+        ocu, odec, _ = oracle_plan(method, ql, nc, C, IL, A)
+        assert cu == ocu and dec == odec
+
+
+def test_planner_errors():
+    L = binding.lib()
+    n = ctypes.c_int32(0)
+    one = (ctypes.c_int32 * 1)(5)
+    assert L.rag_plan_prompts(9, 1, one, one, 512, 0, 0, None, 0, ctypes.byref(n), None) == \
+        binding.RAG_ERR_INVALID_ARG
+    neg = (ctypes.c_int32 * 1)(-1)
+    assert L.rag_plan_prompts(0, 1, one, neg, 512, 0, 0, None, 0, ctypes.byref(n), None) == \
+        binding.RAG_ERR_INVALID_ARG
+    cu = (ctypes.c_int32 * 2)()
+    assert L.rag_plan_prompts(1, 1, one, one, 512, 0, 0, cu, 2, ctypes.byref(n), None) == \
+        binding.RAG_ERR_WORKSPACE  # 5 mapper calls need 6 entries
+    assert n.value == 5
+    big = (ctypes.c_int32 * 1)(2_000_000_000)
+    many = (ctypes.c_int32 * 1)(10)
+    cu2 = (ctypes.c_int32 * 2)()
+    assert L.rag_plan_prompts(0, 1, big, many, 1_000_000_000, 0, 0, cu2, 2, ctypes.byref(n),
+                              None) == binding.RAG_ERR_INVALID_ARG
