@@ -1,0 +1,433 @@
+#!/usr/bin/env python3
+"""Benchmark of the RAG-synthesis attention path on one MI355X.
+
+One step = one pass of the hot path over the 7B-class stuff batch
+(16 queries, 64 query tokens + U{5..20} chunks of 512 tokens each):
+  1. prompt planning (rag_plan_prompts, host),
+  2. packed varlen causal prefill of all 16 prompts (rag_attn_prefill_varlen),
+  3. 128 decode steps of paged attention (rag_attn_decode_paged), kv_len
+     growing by one per step.
+Inputs (Q/K/V, paged KV pools, per-step queries and kv lengths) are resident
+in HBM before the timed region.  Two KV pools alternate between decode steps
+so that a step does not find the previous step's pages in the 256 MB
+Infinity Cache.
+
+Printed: one JSON line with the prefill TFLOP/s (value), the decode KV GB/s,
+roofline objects, extra phases (map_reduce mappers, 70B long stuff, mixed
+decode + chunked prefill) and the oracle's CPU baseline on a bounded sample.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-extra] [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "prefill attn TFLOP/s (% MFMA peak); decode attn KV GB/s (% HBM peak)"
+PEAK_BF16_TFLOPS = 2516.6     # 256 CU x 4096 FLOP/clk x 2.4 GHz, dense
+PEAK_HBM_GBS = 8000.0
+PROFILES = os.path.join(ROOT, "profiles")
+
+
+# ---------------------------------------------------------------------------
+# algorithmic work (what the method must do; no masked or padded work)
+# ---------------------------------------------------------------------------
+def prefill_flops(lens_q, lens_k, hq, d):
+    pairs = 0
+    for nq, nk in zip(lens_q, lens_k):
+        pairs += nq * (nk - nq) + nq * (nq + 1) // 2
+    return 4.0 * d * hq * pairs
+
+
+def prefill_bytes(lens_q, lens_k, hq, hkv, d):
+    return float(sum(2 * nq * hq * d * 2 + 2 * nk * hkv * d * 2
+                     for nq, nk in zip(lens_q, lens_k)))
+
+
+def decode_bytes(kv_lens, hq, hkv, d, q_rows=None):
+    g = hq // hkv
+    rows = q_rows or [1] * len(kv_lens)
+    return float(sum(n * hkv * d * 2 * 2 + 2 * r * g * hkv * d * 2 + 4 * ((n + 15) // 16) + 4
+                     for n, r in zip(kv_lens, rows)))
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2412_10543_amd", "csrc")
+    for name in sorted(os.listdir(csrc)):
+        with open(os.path.join(csrc, name), "rb") as f:
+            h.update(name.encode() + f.read())
+    return h.hexdigest()[:16]
+
+
+def stored_traffic(kernel_key):
+    """HBM traffic per launch from the committed counter summary, if it was
+    taken on the current kernel sources."""
+    path = os.path.join(PROFILES, "traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        t = json.load(f)
+    if t.get("source_hash") != kernel_source_hash():
+        return None
+    k = t.get("kernels", {}).get(kernel_key)
+    return None if k is None else k.get("bytes_per_launch")
+
+
+class Timer:
+    """HIP events on the current stream (the stream every call is enqueued on)."""
+
+    def __init__(self, torch):
+        self.torch = torch
+        self.pairs = {}
+
+    def start(self, name):
+        e = self.torch.cuda.Event(enable_timing=True)
+        e.record()
+        self.pairs.setdefault(name, []).append([e, None])
+
+    def stop(self, name):
+        e = self.torch.cuda.Event(enable_timing=True)
+        e.record()
+        self.pairs[name][-1][1] = e
+
+    def ms(self, name):
+        return [a.elapsed_time(b) for a, b in self.pairs.get(name, [])]
+
+
+# ---------------------------------------------------------------------------
+# workload set-up
+# ---------------------------------------------------------------------------
+def setup_stuff(torch, w, dev, n_pools=2):
+    from paper_2412_10543_amd import binding
+    from paper_2412_10543_amd.workloads import normal_bf16, paged_pool
+    cu, dec = binding.rag_plan_prompts(w.method, w.query_lens, w.num_chunks, w.chunk_len,
+                                       w.intermediate_length, w.answer_len)
+    lens = [b - a for a, b in zip(cu[:-1], cu[1:])]
+    T = cu[-1]
+    st = {"w": w, "lens": lens, "cu": cu, "decode_steps": max(dec) if dec else 0}
+    st["q"] = normal_bf16((T, w.hq, w.d), w.seed, dev)
+    st["k"] = normal_bf16((T, w.hkv, w.d), w.seed + 1, dev)
+    st["v"] = normal_bf16((T, w.hkv, w.d), w.seed + 2, dev)
+    st["o"] = torch.empty_like(st["q"])
+    st["cu_t"] = torch.tensor(cu, dtype=torch.int32, device=dev)
+    nsteps = st["decode_steps"]
+    S = len(lens)
+    if nsteps > 0:
+        full = [n + nsteps for n in lens]
+        st["pools"] = [paged_pool(full, w.hkv, w.d, w.seed + 100 + i, device=dev)
+                       for i in range(n_pools)]
+        st["dq"] = normal_bf16((nsteps, S, w.hq, w.d), w.seed + 7, dev)
+        st["do"] = torch.empty((S, w.hq, w.d), dtype=torch.bfloat16, device=dev)
+        kv = torch.tensor([[n + t + 1 for n in lens] for t in range(nsteps)], dtype=torch.int32,
+                          device=dev)
+        st["kv_steps"] = kv
+        mb = st["pools"][0].block_tables.shape[1]
+        n = binding.rag_attn_decode_workspace_size(S, w.hq, w.hkv, w.d, mb)
+        st["ws"] = torch.empty(max(n, 256), dtype=torch.uint8, device=dev)
+        st["splits"] = binding.rag_attn_decode_num_splits(S, w.hkv, mb)
+    return st
+
+
+def run_stuff_step(st, timer=None, plan=True):
+    from paper_2412_10543_amd import binding
+    w = st["w"]
+    if plan:
+        binding.rag_plan_prompts(w.method, w.query_lens, w.num_chunks, w.chunk_len,
+                                 w.intermediate_length, w.answer_len)
+    L = max(st["lens"])
+    if timer:
+        timer.start("prefill")
+    binding.rag_attn_prefill_varlen(st["q"], st["k"], st["v"], st["o"], None, st["cu_t"],
+                                    st["cu_t"], L, L, w.scale, True)
+    if timer:
+        timer.stop("prefill")
+    pools = st.get("pools", [])
+    for t in range(st["decode_steps"]):
+        pool = pools[t % len(pools)]
+        if timer:
+            timer.start("decode")
+        binding.rag_attn_decode_paged(st["dq"][t], pool.k_cache, pool.v_cache, st["do"],
+                                      pool.block_tables, st["kv_steps"][t], w.scale,
+                                      workspace=st["ws"])
+        if timer:
+            timer.stop("decode")
+
+
+def stuff_work(st):
+    w = st["w"]
+    lens = st["lens"]
+    fl = prefill_flops(lens, lens, w.hq, w.d)
+    pb = prefill_bytes(lens, lens, w.hq, w.hkv, w.d)
+    db = [decode_bytes([n + t + 1 for n in lens], w.hq, w.hkv, w.d)
+          for t in range(st["decode_steps"])]
+    return fl, pb, db
+
+
+def roofline(bound, achieved, peak, unit, traffic=None, kernel=None):
+    r = {"bound": bound, "achieved": round(achieved, 2), "peak": peak, "unit": unit,
+         "frac": round(achieved / peak, 4), "traffic": traffic}
+    if kernel:
+        r["kernel"] = kernel
+    return r
+
+
+def median(x):
+    s = sorted(x)
+    return s[len(s) // 2] if s else float("nan")
+
+
+# ---------------------------------------------------------------------------
+# extra phases (other workloads; measured, not part of the step)
+# ---------------------------------------------------------------------------
+def bench_phase_stuff(torch, w, dev, reps):
+    st = setup_stuff(torch, w, dev)
+    fl, pb, db = stuff_work(st)
+    run_stuff_step(st, None, plan=False)
+    torch.cuda.synchronize()
+    timer = Timer(torch)
+    for _ in range(reps):
+        run_stuff_step(st, timer, plan=False)
+    torch.cuda.synchronize()
+    pf_ms = median(timer.ms("prefill"))
+    dec_ms = timer.ms("decode")
+    out = {"tokens": st["cu"][-1], "seqs": len(st["lens"]), "hq": w.hq, "hkv": w.hkv, "d": w.d,
+           "prefill_ms": round(pf_ms, 4), "prefill_tflops": round(fl / pf_ms / 1e9, 1),
+           "prefill_frac_mfma": round(fl / pf_ms / 1e9 / PEAK_BF16_TFLOPS, 4),
+           "prefill_hbm_gbs": round(pb / pf_ms / 1e6, 1)}
+    if dec_ms:
+        per = st["decode_steps"]
+        tot = sum(dec_ms) / reps
+        gbs = sum(db) / tot / 1e6
+        out.update({"decode_steps": per, "decode_us_per_step": round(tot / per * 1e3, 2),
+                    "decode_gbs": round(gbs, 1), "decode_frac_hbm": round(gbs / PEAK_HBM_GBS, 4),
+                    "decode_splits": st["splits"]})
+    del st
+    torch.cuda.empty_cache()
+    return out
+
+
+def bench_phase_mixed(torch, dev, reps):
+    from paper_2412_10543_amd import binding
+    from paper_2412_10543_amd.workloads import mixed, normal_bf16, paged_pool
+    w = mixed()
+    kv = w.decode_kv_lens + [p + w.piece_len for p in w.piece_prior]
+    q_lens = [1] * len(w.decode_kv_lens) + [w.piece_len] * len(w.piece_prior)
+    cu = [0]
+    for n in q_lens:
+        cu.append(cu[-1] + n)
+    pools = [paged_pool(kv, w.hkv, w.d, w.seed + i, device=dev) for i in range(2)]
+    q = normal_bf16((cu[-1], w.hq, w.d), w.seed + 9, dev)
+    o = torch.empty_like(q)
+    nd = len(w.decode_kv_lens)
+    mb = pools[0].block_tables.shape[1]
+    n = binding.rag_attn_decode_workspace_size(nd, w.hq, w.hkv, w.d, mb)
+    ws = torch.empty(max(n, 256), dtype=torch.uint8, device=dev)
+    cu_t = torch.tensor(cu, dtype=torch.int32, device=dev)
+    kv_t = torch.tensor(kv, dtype=torch.int32, device=dev)
+
+    def call(pool):
+        binding.rag_attn_decode_paged(q, pool.k_cache, pool.v_cache, o, pool.block_tables, kv_t,
+                                      w.scale, cu_seqlens_q=cu_t, num_decode_seqs=nd,
+                                      max_seqlen_q=w.piece_len, workspace=ws)
+    call(pools[0])
+    torch.cuda.synchronize()
+    timer = Timer(torch)
+    for r in range(reps):
+        timer.start("mixed")
+        call(pools[r % 2])
+        timer.stop("mixed")
+    torch.cuda.synchronize()
+    ms = median(timer.ms("mixed"))
+    dbytes = decode_bytes(w.decode_kv_lens, w.hq, w.hkv, w.d)
+    pl_q = [w.piece_len] * len(w.piece_prior)
+    pl_k = [p + w.piece_len for p in w.piece_prior]
+    pfl = prefill_flops(pl_q, pl_k, w.hq, w.d)
+    pbytes = decode_bytes(pl_k, w.hq, w.hkv, w.d, q_rows=pl_q)
+    t_hbm = (dbytes + pbytes) / (PEAK_HBM_GBS * 1e6)
+    t_mfma = pfl / (PEAK_BF16_TFLOPS * 1e9)
+    out = {"decode_seqs": nd, "pieces": len(w.piece_prior), "piece_len": w.piece_len,
+           "ms": round(ms, 4), "kv_gbs": round((dbytes + pbytes) / ms / 1e6, 1),
+           "piece_tflops": round(pfl / ms / 1e9, 1),
+           "roofline_ms_overlapped": round(max(t_hbm, t_mfma), 4),
+           "roofline_ms_serial": round(t_hbm + t_mfma, 4),
+           "frac_of_overlapped_roofline": round(max(t_hbm, t_mfma) / ms, 4),
+           "splits": binding.rag_attn_decode_num_splits(nd, w.hkv, mb)}
+    del pools, q, o
+    torch.cuda.empty_cache()
+    return out
+
+
+# ---------------------------------------------------------------------------
+# CPU baseline: the oracle on a bounded sample of the same workload
+# ---------------------------------------------------------------------------
+def cpu_baseline(torch, st, budget_s=12.0):
+    import numpy as np
+
+    import oracle
+    from paper_2412_10543_amd.workloads import bf16_bits
+    w = st["w"]
+    orc = oracle.default()
+    lens, cu = st["lens"], st["cu"]
+    s = int(np.argmax(lens))           # the longest prompt
+    L = lens[s]
+    k = bf16_bits(st["k"][cu[s]:cu[s + 1]])
+    v = bf16_bits(st["v"][cu[s]:cu[s + 1]])
+    qs = st["q"][cu[s]:cu[s + 1]]
+    rng = np.random.Generator(np.random.PCG64(0))
+    flops, secs, nrows = 0.0, 0.0, 0
+    while secs < budget_s * 0.5 and nrows < L * w.hq:
+        rows = np.sort(rng.integers(0, L, size=64)).astype(np.int32)
+        heads = rng.integers(0, w.hq, size=64).astype(np.int32)
+        qr = bf16_bits(qs[torch.as_tensor(rows, device=qs.device).long(),
+                          torch.as_tensor(heads, device=qs.device).long()])
+        t0 = time.perf_counter()
+        orc.seq_rows(qr, k, v, L, rows, heads, w.hq, w.scale, True)
+        secs += time.perf_counter() - t0
+        flops += float(sum(4 * w.d * (r + 1) for r in rows))
+        nrows += len(rows)
+    out = {"value": round(flops / secs / 1e12, 6), "unit": "TFLOP/s",
+           "cores": len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else
+           os.cpu_count(), "kind": "oracle",
+           "sample": f"prefill: {nrows} (row, head) pairs of the longest stuff prompt "
+                     f"(L={L}), {secs:.1f}s"}
+    # decode: one step for as many sequences as fit in the budget
+    pool = st["pools"][0]
+    steps_kv = [n + 1 for n in lens]
+    tables = pool.block_tables.cpu().numpy()
+    dbytes, dsecs, nseq = 0.0, 0.0, 0
+    for si in np.argsort(lens)[::-1]:
+        if dsecs >= budget_s * 0.5:
+            break
+        nb = (steps_kv[si] + 15) // 16
+        blocks = torch.as_tensor(tables[si, :nb], device=pool.k_cache.device).long()
+        kc = bf16_bits(pool.k_cache[blocks])
+        vc = bf16_bits(pool.v_cache[blocks])
+        qd = bf16_bits(st["dq"][0][si:si + 1])
+        table = np.arange(nb, dtype=np.int32)[None, :]
+        t0 = time.perf_counter()
+        orc.paged(qd, kc, vc, table, [steps_kv[si]], w.scale, want_lse=False)
+        dsecs += time.perf_counter() - t0
+        dbytes += decode_bytes([steps_kv[si]], w.hq, w.hkv, w.d)
+        nseq += 1
+    out["decode"] = {"value": round(dbytes / dsecs / 1e9, 4), "unit": "GB/s",
+                     "sample": f"decode step 0 of {nseq} sequences, {dsecs:.1f}s"}
+    out["omp_threads"] = os.environ.get("OMP_NUM_THREADS", "default")
+    return out
+
+
+# ---------------------------------------------------------------------------
+def copy_calibration(torch, gib=1.0):
+    """A plain device copy of known size, for scaling the HBM traffic counters."""
+    n = int(gib * (1 << 30))
+    src = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes": n, "launches": 3}))
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawTextHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--no-extra", action="store_true", help="skip the other workloads")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--extra-reps", type=int, default=5)
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a 1 GiB device copy (counter calibration)")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path "
+              "(sequences shard across GPUs with no exchange; see DESIGN.md). "
+              "Run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    if args.copy_calibration:
+        copy_calibration(torch)
+        return
+    from paper_2412_10543_amd import binding
+    from paper_2412_10543_amd.workloads import long70b, mapred7b, stuff7b
+    binding.lib()
+    dev = torch.device("cuda:0")
+
+    w = stuff7b()
+    st = setup_stuff(torch, w, dev)
+    fl, pb, db = stuff_work(st)
+    for _ in range(args.warmup):
+        run_stuff_step(st)
+    torch.cuda.synchronize()
+
+    timer = Timer(torch)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        run_stuff_step(st, timer)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+
+    pf_ms = timer.ms("prefill")
+    dec_ms = timer.ms("decode")
+    pf_avg = sum(pf_ms) / len(pf_ms)
+    dec_total = sum(dec_ms) / args.steps                   # ms of decode per step
+    nsteps = st["decode_steps"]
+    dec_avg = dec_total / nsteps                           # ms per decode launch
+    tflops = fl / pf_avg / 1e9
+    dec_gbs = sum(db) / dec_total / 1e6
+    dec_bytes_avg = sum(db) / nsteps
+
+    rl_pf = roofline("mfma", tflops, PEAK_BF16_TFLOPS, "TFLOP/s",
+                     traffic=stored_traffic("prefill_varlen_kernel"),
+                     kernel="prefill_varlen_kernel<128>")
+    rl_dec = roofline("hbm", dec_gbs, PEAK_HBM_GBS, "GB/s",
+                      traffic=stored_traffic("paged_kernel"),
+                      kernel="rag_attn_decode_paged (paged_kernel<128> + combine_kernel<128>)")
+    dominant = rl_dec if dec_total > pf_avg else rl_pf
+
+    res = {
+        "metric": METRIC, "value": round(tflops, 2), "unit": "TFLOP/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(wall / args.steps * 1e3, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic: seeded N(0,1) fp32 rounded to bf16; RAG prompt shapes",
+        "config": {"workload": "stuff7b", "queries": 16, "query_tokens": 64, "chunk_len": 512,
+                   "num_chunks": w.num_chunks, "tokens": st["cu"][-1], "hq": w.hq,
+                   "hkv": w.hkv, "d": w.d, "decode_steps": nsteps, "block_size": 16,
+                   "decode_splits": st["splits"]},
+        "prefill": {"ms": round(pf_avg, 4), "tflops": round(tflops, 2),
+                    "frac_mfma": round(tflops / PEAK_BF16_TFLOPS, 4),
+                    "algorithmic_flops": fl, "algorithmic_bytes": pb},
+        "decode": {"value": round(dec_gbs, 1), "unit": "GB/s",
+                   "frac_hbm": round(dec_gbs / PEAK_HBM_GBS, 4),
+                   "us_per_step": round(dec_avg * 1e3, 3),
+                   "algorithmic_bytes_per_launch": round(dec_bytes_avg)},
+        "roofline": dominant,
+        "rooflines": {"prefill": rl_pf, "decode": rl_dec},
+    }
+    if not args.no_extra:
+        phases = {}
+        for fn in (mapred7b, long70b):
+            phases[fn.__name__] = bench_phase_stuff(torch, fn(), dev, args.extra_reps)
+        phases["mixed"] = bench_phase_mixed(torch, dev, args.extra_reps)
+        res["phases"] = phases
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(torch, st)
+    print(json.dumps(res))
+
+
+if __name__ == "__main__":
+    main()
