@@ -16,6 +16,7 @@ typedef float f32x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kWave = 64;
 constexpr int kNumXcd = 8;        // MI355X: 8 accelerator complex dies
@@ -71,6 +72,21 @@ __device__ __forceinline__ u32x4 load16(const void* p) {
   return *reinterpret_cast<const u32x4*>(p);
 }
 
+// gfx950 transposing LDS read (ds_read_b64_tr_b16).  Within each group of 16
+// lanes, lane i supplies the address of 4 consecutive bf16 values (row i of a
+// 16 x 4 tile M) and receives M[i/4 + 4k][i%4] for k = 0..3.  Reading a
+// row-major [key][d] tile this way yields the column (fixed d, four keys) that
+// an MFMA A operand of V^T needs, with no transpose on the way into LDS.
+__device__ __forceinline__ i16x4 lds_read_tr4(const bf16_t* p) {
+  typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p));
+}
+__device__ __forceinline__ bf16x8 join_bf16x8(i16x4 lo, i16x4 hi) {
+  typedef short i16x8 __attribute__((ext_vector_type(8)));
+  i16x8 v = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+  return __builtin_bit_cast(bf16x8, v);
+}
+
 // Workgroup index as seen by one XCD: the hardware deals consecutive
 // workgroup ids round-robin to the 8 XCDs, so id n runs on XCD n % 8.  The
 // returned index runs contiguously on each XCD, which keeps workgroups that
@@ -85,12 +101,16 @@ constexpr int kPfBM = 128;          // query rows per workgroup
 constexpr int kPfBN = 64;           // keys per K/V tile
 constexpr int kPfThreads = 256;     // 4 waves x 32 query rows
 
+// K and V tiles are both row-major [key][d] in LDS.  K rows are padded by
+// 16 B (consecutive rows land 4 banks apart: the 16-byte A-operand reads of 8
+// lanes hit distinct banks); V rows by 32 B (the transposing reads of 16
+// lanes cover 4 rows x 32 B, which then map to distinct banks).
 template <int D>
 struct PfLds {
-  static constexpr int kStrK = D + 8;        // bf16 per K row (16 B pad)
-  static constexpr int kStrV = kPfBN + 8;    // bf16 per transposed-V row
+  static constexpr int kStrK = D + 8;
+  static constexpr int kStrV = D + 16;
   static constexpr int kElemsK = kPfBN * kStrK;
-  static constexpr int kElemsV = D * kStrV;
+  static constexpr int kElemsV = kPfBN * kStrV;
   static constexpr int kElemsBuf = kElemsK + kElemsV;
   static constexpr int kBytes = 2 * kElemsBuf * 2;   // two buffers of bf16
 };
@@ -101,10 +121,11 @@ constexpr int kDecThreads = 256;
 constexpr int kDecWaves = kDecThreads / kWave;
 constexpr int kDecMaxGroup = 16;           // q heads per kv head (MFMA N)
 
+// Per wave: the V rows of the two pages of one step, row-major [32][D + 16].
 template <int D>
 struct DecLds {
-  static constexpr int kStrV = 32 + 8;       // bf16 per transposed-V row
-  static constexpr int kElemsWave = D * kStrV;
+  static constexpr int kStrV = D + 16;
+  static constexpr int kElemsWave = 32 * kStrV;
   static constexpr int kBytes = kDecWaves * kElemsWave * 2;
 };
 

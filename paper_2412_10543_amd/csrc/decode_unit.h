@@ -10,7 +10,8 @@
 //     instruction read 64 contiguous bytes of that key's row;
 //   * both products run on v_mfma_f32_16x16x32_bf16 with the G query heads as
 //     the N dimension (padded to 16): S^T = K Q^T straight from registers,
-//     then O^T = V^T P^T with V transposed through a per-wave LDS tile;
+//     then O^T = V^T P^T with the V rows staged row-major in a per-wave LDS
+//     slice and read back as V^T fragments by the transposing LDS read;
 //   * two pages (32 keys) per step; the next step's pages are loaded while
 //     the current step computes.
 #pragma once
@@ -67,7 +68,7 @@ __device__ __forceinline__ void decode_unit(
 
   // Register staging for one step (two pages):
   //   ka/kb: K rows as the MFMA A operand (key l16, d chunk 4*ks + gq)
-  //   va/vb: V rows for the transpose (keys 4*gq + t, d chunk l16)
+  //   va/vb: V rows (keys 4*gq + t, d chunk l16) for the LDS slice
   u32x4 ka[kKs], kb[kKs], va[4], vb[4];
   auto load_step = [&](int p) {
     const bool has_b = p + 1 < p_end;
@@ -85,7 +86,7 @@ __device__ __forceinline__ void decode_unit(
         vb[t] = load16(vc + bb + (size_t)(4 * gq + t) * D + l16 * 8);
       }
     } else {
-      // D == 64: 8 chunks per row; lane (chunk l16 % 8, keys 8*(gq) + 4*(l16/8) ..)
+      // D == 64: 8 chunks per row; lanes l16 and l16 + 8 load the same chunk
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
         va[t] = load16(vc + ba + (size_t)(4 * gq + t) * D + (l16 & 7) * 8);
@@ -93,6 +94,9 @@ __device__ __forceinline__ void decode_unit(
       }
     }
   };
+
+  // transposing-read source: row 4*gq + l16/4, d 4*(l16%4) of a 16-d tile
+  const int tr_off = (4 * gq + (l16 >> 2)) * L::kStrV + 4 * (l16 & 3);
 
   if (p_begin < p_end) load_step(p_begin);
   for (int p = p_begin; p < p_end; p += 2) {
@@ -146,37 +150,24 @@ __device__ __forceinline__ void decode_unit(
     }
     const bf16x8 pfrag = to_bf16x8(pa[0], pa[1], pa[2], pa[3], pbv[0], pbv[1], pbv[2], pbv[3]);
 
-    // ---- V^T into LDS: row d, position 8*gq + t holds key 4*gq + t of page A
-    // (t < 4) or of page B (t >= 4), matching the P fragment's slot order ----
-    if constexpr (D == 128) {
+    // ---- V rows of both pages into this wave's LDS slice, row-major:
+    // rows 0..15 page A, rows 16..31 page B ------------------------------------
+    if (D == 128 || l16 < 8) {
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const uint32_t sel = (e & 1) ? 0x07060302u : 0x05040100u;
-        u32x4 w = {__builtin_amdgcn_perm(wa[1][e >> 1], wa[0][e >> 1], sel),
-                   __builtin_amdgcn_perm(wa[3][e >> 1], wa[2][e >> 1], sel),
-                   __builtin_amdgcn_perm(wb[1][e >> 1], wb[0][e >> 1], sel),
-                   __builtin_amdgcn_perm(wb[3][e >> 1], wb[2][e >> 1], sel)};
-        *reinterpret_cast<u32x4*>(vt + (l16 * 8 + e) * L::kStrV + 8 * gq) = w;
-      }
-    } else {
-      // D == 64: lanes l16 >= 8 duplicate lanes l16 - 8 (same chunk, same keys)
-      if (l16 < 8) {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const uint32_t sel = (e & 1) ? 0x07060302u : 0x05040100u;
-          u32x4 w = {__builtin_amdgcn_perm(wa[1][e >> 1], wa[0][e >> 1], sel),
-                     __builtin_amdgcn_perm(wa[3][e >> 1], wa[2][e >> 1], sel),
-                     __builtin_amdgcn_perm(wb[1][e >> 1], wb[0][e >> 1], sel),
-                     __builtin_amdgcn_perm(wb[3][e >> 1], wb[2][e >> 1], sel)};
-          *reinterpret_cast<u32x4*>(vt + (l16 * 8 + e) * L::kStrV + 8 * gq) = w;
-        }
+      for (int t = 0; t < 4; ++t) {
+        *reinterpret_cast<u32x4*>(vt + (4 * gq + t) * L::kStrV + l16 * 8) = wa[t];
+        *reinterpret_cast<u32x4*>(vt + (16 + 4 * gq + t) * L::kStrV + l16 * 8) = wb[t];
       }
     }
     wave_lds_sync();
     // ---- O^T += V^T P^T ------------------------------------------------------
+    // A operand of d-tile dt: slot 8*gq + t holds key 4*gq + t of page A
+    // (t < 4) or page B (t >= 4) at d = 16*dt + l16 -- two transposing reads
+    // whose 16-lane groups each cover 4 rows x 16 d of one page.
 #pragma unroll
     for (int dt = 0; dt < kDt; ++dt) {
-      const bf16x8 a = *reinterpret_cast<const bf16x8*>(vt + (16 * dt + l16) * L::kStrV + 8 * gq);
+      const bf16x8 a = join_bf16x8(lds_read_tr4(vt + tr_off + 16 * dt),
+                                   lds_read_tr4(vt + 16 * L::kStrV + tr_off + 16 * dt));
       oacc[dt] = mfma16(a, pfrag, oacc[dt]);
     }
     wave_lds_sync();

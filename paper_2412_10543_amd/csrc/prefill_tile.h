@@ -6,17 +6,15 @@
 // for CDNA4:
 //   * 4 waves, each owning 32 query rows; the wave keeps its Q rows in
 //     registers as the B operand of v_mfma_f32_32x32x16_bf16;
-//   * K/V tiles of 64 keys are staged through LDS, double-buffered, with one
-//     barrier per tile; global loads of tile t+1 are in flight while tile t
-//     is computed;
+//   * K/V tiles of 64 keys are staged through LDS row-major ([key][d]),
+//     double-buffered, with one barrier per tile; the global loads of tile
+//     t+1 are in flight while tile t is computed;
 //   * scores are computed transposed, S^T = K Q^T, so each lane owns one query
-//     row and its scores sit in the accumulator exactly where the B operand
-//     of the P.V product needs them (O^T = V^T P^T).  K rows are read from
-//     LDS in an order that swaps bits 2 and 3 of the row index, which makes
-//     accumulator element j of a 32-key block hold key 16*(j/8) + 8*half +
-//     j%8; V is written to LDS transposed ([d][key]) with matching order, so
-//     every MFMA operand is one 16-byte LDS read and nothing is shuffled
-//     between the two products;
+//     row and its scores already sit where the B operand of O^T = V^T P^T
+//     needs them; the matching V^T A operand comes straight from the
+//     row-major V tile through the transposing LDS read (ds_read_b64_tr_b16),
+//     so no data is shuffled between the two products and nothing is
+//     transposed on the way into LDS;
 //   * softmax statistics in fp32 with exp2 and the scale folded into one
 //     FMA; the reference maximum is moved lazily (only when a score exceeds
 //     it by 2^8), which keeps rescales of the output off the common path;
@@ -53,12 +51,6 @@ struct PagedKV {
   __device__ __forceinline__ const bf16_t* vrow(int j) const { return v + off(j); }
 };
 
-// Row index inside a 32-key block whose scores land, after the S^T product,
-// where the P.V product's B operand expects them: bits 2 and 3 swapped.
-__device__ __forceinline__ int swap_bits23(int m) {
-  return (m & ~12) | ((m & 4) << 1) | ((m & 8) >> 1);
-}
-
 template <int D, class KV>
 __device__ __forceinline__ void prefill_tile(
     const bf16_t* __restrict__ q, size_t q_stride,   // row 0 of this seq, this head
@@ -69,8 +61,7 @@ __device__ __forceinline__ void prefill_tile(
   using L = PfLds<D>;
   constexpr int kCh = D / 8;                  // 16-byte chunks per row
   constexpr int kRowsPerIt = kPfThreads / kCh;
-  constexpr int kItK = kPfBN / kRowsPerIt;    // K loads per thread per tile
-  constexpr int kVk = kPfBN * kCh / kPfThreads;  // V keys per thread per tile
+  constexpr int kIt = kPfBN / kRowsPerIt;     // K (and V) loads per thread per tile
   constexpr int kKs = D / 16;                 // MFMA k-steps over d
   constexpr int kDt = D / 32;                 // 32-row d tiles of O^T
 
@@ -107,44 +98,27 @@ __device__ __forceinline__ void prefill_tile(
   float m_used = -INFINITY;
   float l = 0.f;
 
+  // ---- staging: K and V rows copied as 16-byte chunks ----------------------
   const int ld_ch = tid % kCh;
   const int ld_row = tid / kCh;
-  u32x4 kreg[kItK], vreg[kVk];
-
+  u32x4 kreg[kIt], vreg[kIt];
   auto load_tile = [&](int k0) {
 #pragma unroll
-    for (int it = 0; it < kItK; ++it) {
+    for (int it = 0; it < kIt; ++it) {
       const int j = k0 + it * kRowsPerIt + ld_row;
       u32x4 z = {0, 0, 0, 0};
       kreg[it] = j < nk ? load16(kv.krow(j) + ld_ch * 8) : z;
-    }
-#pragma unroll
-    for (int e = 0; e < kVk; ++e) {
-      const int j = k0 + ld_row * kVk + e;
-      u32x4 z = {0, 0, 0, 0};
-      vreg[e] = j < nk ? load16(kv.vrow(j) + ld_ch * 8) : z;
+      vreg[it] = j < nk ? load16(kv.vrow(j) + ld_ch * 8) : z;
     }
   };
   auto store_tile = [&](int buf) {
     bf16_t* kl = lds + buf * L::kElemsBuf;
     bf16_t* vl = kl + L::kElemsK;
 #pragma unroll
-    for (int it = 0; it < kItK; ++it)
-      *reinterpret_cast<u32x4*>(kl + (it * kRowsPerIt + ld_row) * L::kStrK + ld_ch * 8) = kreg[it];
-    // transpose: element e of this thread's kVk key rows -> row d = 8*ld_ch+e
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const uint32_t sel = (e & 1) ? 0x07060302u : 0x05040100u;
-      bf16_t* dst = vl + (ld_ch * 8 + e) * L::kStrV + ld_row * kVk;
-      if constexpr (kVk == 4) {
-        u32x2 w = {__builtin_amdgcn_perm(vreg[1][e >> 1], vreg[0][e >> 1], sel),
-                   __builtin_amdgcn_perm(vreg[3][e >> 1], vreg[2][e >> 1], sel)};
-        *reinterpret_cast<u32x2*>(dst) = w;
-      } else {
-        static_assert(kVk == 2, "unsupported head size");
-        *reinterpret_cast<uint32_t*>(dst) =
-            __builtin_amdgcn_perm(vreg[1][e >> 1], vreg[0][e >> 1], sel);
-      }
+    for (int it = 0; it < kIt; ++it) {
+      const int r = it * kRowsPerIt + ld_row;
+      *reinterpret_cast<u32x4*>(kl + r * L::kStrK + ld_ch * 8) = kreg[it];
+      *reinterpret_cast<u32x4*>(vl + r * L::kStrV + ld_ch * 8) = vreg[it];
     }
   };
 
@@ -154,7 +128,13 @@ __device__ __forceinline__ void prefill_tile(
   }
   __syncthreads();
 
-  const int krow_sw = swap_bits23(l32);
+  // Transposing-read source address inside the V tile (see lds_read_tr4):
+  // lane (group g = lane/16, r = lane%16) points at key 4*half + r/4 and
+  // d = 16*(g%2) + 4*(r%4) of a 16-key slice; the group's result gives lane
+  // l the values V[slice + 4*half + k][l%32], k = 0..3.
+  const int g16 = lane >> 4, r16 = lane & 15;
+  const int tr_off = (4 * half + (r16 >> 2)) * L::kStrV + 16 * (g16 & 1) + 4 * (r16 & 3);
+
   for (int t = 0; t < n_tiles; ++t) {
     const int k0 = t * kPfBN;
     if (t + 1 < n_tiles) load_tile(k0 + kPfBN);
@@ -163,6 +143,8 @@ __device__ __forceinline__ void prefill_tile(
 
     if (k0 < kend_w) {
       // ---- S^T = K Q^T for 64 keys x 32 rows -------------------------------
+      // accumulator element j of m-tile mt holds key 32*mt + 8*(j/4) +
+      // 4*half + j%4 of this lane's query row.
       f32x16 s[2];
 #pragma unroll
       for (int mt = 0; mt < 2; ++mt)
@@ -173,7 +155,7 @@ __device__ __forceinline__ void prefill_tile(
 #pragma unroll
         for (int mt = 0; mt < 2; ++mt) {
           const bf16x8 a = *reinterpret_cast<const bf16x8*>(
-              kl + (32 * mt + krow_sw) * L::kStrK + ks * 16 + half * 8);
+              kl + (32 * mt + l32) * L::kStrK + ks * 16 + half * 8);
           s[mt] = mfma32(a, qf[ks], s[mt]);
         }
       }
@@ -185,7 +167,7 @@ __device__ __forceinline__ void prefill_tile(
         for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
           for (int j = 0; j < 16; ++j) {
-            const int key = k0 + 32 * mt + 16 * (j >> 3) + 8 * half + (j & 7);
+            const int key = k0 + 32 * mt + 8 * (j >> 2) + 4 * half + (j & 3);
             if (key > lim) s[mt][j] = -INFINITY;
           }
       }
@@ -216,6 +198,10 @@ __device__ __forceinline__ void prefill_tile(
           l += p;
         }
       // ---- O^T += V^T P^T ----------------------------------------------------
+      // k-step (mt, s2) covers keys 32*mt + 16*s2 + [0, 16); B-operand slot
+      // 8*half + t is accumulator element 8*s2 + t, i.e. key
+      // 32*mt + 16*s2 + 8*(t/4) + 4*half + t%4, which the two transposing
+      // reads (slices +0 and +8) deliver in the same order.
 #pragma unroll
       for (int mt = 0; mt < 2; ++mt) {
 #pragma unroll
@@ -223,10 +209,11 @@ __device__ __forceinline__ void prefill_tile(
           const int b = 8 * s2;
           const bf16x8 pb = to_bf16x8(s[mt][b], s[mt][b + 1], s[mt][b + 2], s[mt][b + 3],
                                       s[mt][b + 4], s[mt][b + 5], s[mt][b + 6], s[mt][b + 7]);
+          const bf16_t* vs = vl + (32 * mt + 16 * s2) * L::kStrV + tr_off;
 #pragma unroll
           for (int dt = 0; dt < kDt; ++dt) {
-            const bf16x8 a = *reinterpret_cast<const bf16x8*>(
-                vl + (32 * dt + l32) * L::kStrV + 32 * mt + 16 * s2 + 8 * half);
+            const bf16x8 a = join_bf16x8(lds_read_tr4(vs + 32 * dt),
+                                         lds_read_tr4(vs + 8 * L::kStrV + 32 * dt));
             oacc[dt] = mfma32(a, pb, oacc[dt]);
           }
         }
@@ -251,7 +238,7 @@ __device__ __forceinline__ void prefill_tile(
         *reinterpret_cast<bf16x4*>(orow + d) = w;
       }
     if (lse != nullptr && half == 0)
-      lse[row] = lt > 0.f ? m_used * scale + __logf(lt) : -INFINITY;
+      lse[row] = lt > 0.f ? m_used * scale + logf(lt) : -INFINITY;
   }
 }
 
