@@ -132,7 +132,7 @@ def setup_stuff(torch, w, dev, n_pools=2):
         st["kv_steps"] = kv
         mb = st["pools"][0].block_tables.shape[1]
         n = binding.rag_attn_decode_workspace_size(S, w.hq, w.hkv, w.d, mb)
-        st["ws"] = torch.empty(max(n, 256), dtype=torch.uint8, device=dev)
+        st["ws"] = torch.zeros(max(n, 256), dtype=torch.uint8, device=dev)
         st["splits"] = binding.rag_attn_decode_num_splits(S, w.hkv, mb)
     return st
 
@@ -230,7 +230,7 @@ def bench_phase_mixed(torch, dev, reps):
     nd = len(w.decode_kv_lens)
     mb = pools[0].block_tables.shape[1]
     n = binding.rag_attn_decode_workspace_size(nd, w.hq, w.hkv, w.d, mb)
-    ws = torch.empty(max(n, 256), dtype=torch.uint8, device=dev)
+    ws = torch.zeros(max(n, 256), dtype=torch.uint8, device=dev)
     cu_t = torch.tensor(cu, dtype=torch.int32, device=dev)
     kv_t = torch.tensor(kv, dtype=torch.int32, device=dev)
 
@@ -395,7 +395,7 @@ def main():
                      kernel="prefill_varlen_kernel<128>")
     rl_dec = roofline("hbm", dec_gbs, PEAK_HBM_GBS, "GB/s",
                       traffic=stored_traffic("paged_kernel"),
-                      kernel="rag_attn_decode_paged (paged_kernel<128> + combine_kernel<128>)")
+                      kernel="paged_kernel<128,false> (rag_attn_decode_paged)")
     dominant = rl_dec if dec_total > pf_avg else rl_pf
 
     res = {

@@ -115,9 +115,10 @@ int32_t rag_attn_decode_num_splits(int32_t num_decode_seqs,
 
 /*
  * Bytes of workspace rag_attn_decode_paged needs for the same arguments (0
- * when the decode rows use a single split).  Layout (library-internal): fp32
- * partial outputs [num_decode_seqs, num_q_heads, splits, head_dim] followed by
- * fp32 partial log-sum-exp values [num_decode_seqs, num_q_heads, splits].
+ * when the decode rows use a single split).  Layout (library-internal): int32
+ * arrival counters [num_decode_seqs, num_kv_heads], fp32 partial outputs
+ * [num_decode_seqs, num_q_heads, splits, head_dim] and fp32 partial
+ * log-sum-exp values [num_decode_seqs, num_q_heads, splits].
  */
 size_t rag_attn_decode_workspace_size(int32_t num_decode_seqs,
                                       int32_t num_q_heads, int32_t num_kv_heads,
@@ -150,10 +151,15 @@ size_t rag_attn_decode_workspace_size(int32_t num_decode_seqs,
  *   block_size  must be 16.  head_dim 64 or 128.  The decode rows need
  *            num_q_heads / num_kv_heads <= 16.
  *   num_splits  0 = automatic; else the number of KV splits per decode row
- *            (combined with a log-sum-exp merge).
+ *            (clamped to [1, min(64, max_blocks_per_seq)]).
+ *            Splits are merged (log-sum-exp) inside the same kernel by the
+ *            last split of each row to finish.
  *   workspace, workspace_bytes  device scratch of at least
  *            rag_attn_decode_workspace_size(...) bytes (may be NULL when that
- *            is 0); 256-byte aligned.  Overlapping calls must not share it.
+ *            is 0); 256-byte aligned.  It must be zero-filled before its first
+ *            use; every completed call leaves it zero-filled again (the split
+ *            merge counts arrivals in it), so one zeroed buffer serves any
+ *            sequence of calls.  Overlapping calls must not share it.
  *
  * Every element of o for the Tq rows is written.  Returns RAG_OK,
  * RAG_ERR_INVALID_ARG, RAG_ERR_UNSUPPORTED, RAG_ERR_WORKSPACE or RAG_ERR_HIP.

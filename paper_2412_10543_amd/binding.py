@@ -148,7 +148,8 @@ def rag_attn_decode_paged(q, k_cache, v_cache, o, block_tables, kv_lens, softmax
                           num_splits=0, workspace=None, stream=None) -> None:
     """q, o [Tq, Hq, d]; caches [num_blocks, Hkv, 16, d] bf16; block_tables
     int32 [S, max_blocks]; kv_lens int32 [S]; cu_seqlens_q int32 [S+1] or
-    None; workspace a uint8 GPU tensor or None."""
+    None; workspace a zero-initialised GPU tensor (torch.zeros, uint8) of
+    rag_attn_decode_workspace_size bytes, or None when that size is 0."""
     for t, n in ((q, "q"), (o, "o")):
         _need(t, torch.bfloat16, n, 3)
     for t, n in ((k_cache, "k_cache"), (v_cache, "v_cache")):

@@ -66,9 +66,15 @@ rag_status check_cu(const std::vector<int32_t>& cu, const char* name, int32_t ma
 
 constexpr int32_t kBlock = 16;
 constexpr int32_t kMaxGroupDecode = 16;
-constexpr int32_t kTargetUnits = 4096;   // wave-units that fill 256 CUs several times over
-constexpr int32_t kMaxPagesPerUnit = 64;
-constexpr int32_t kMinPagesPerUnit = 8;
+// Decode units are workgroups of four waves.  Each unit pays a fixed cost
+// (first page latency, merge of its split), so auto splits aim at about one
+// unit per CU, cap a unit at 512 pages (load balance across sequences of very
+// different length) and keep at least 16 pages per unit (two steps per
+// wave).  The in-kernel merge handles at most 64 splits.
+constexpr int32_t kTargetUnits = 256;
+constexpr int32_t kMaxPagesPerUnit = 512;
+constexpr int32_t kMinPagesPerUnit = 16;
+constexpr int32_t kMaxSplits = 64;
 
 int32_t auto_splits(int32_t num_decode, int32_t hkv, int32_t max_blocks) {
   const int64_t base = std::max<int64_t>(1, (int64_t)num_decode * hkv);
@@ -81,22 +87,28 @@ int32_t auto_splits(int32_t num_decode, int32_t hkv, int32_t max_blocks) {
 
 int32_t resolve_splits(int32_t num_decode, int32_t hkv, int32_t max_blocks, int32_t requested) {
   int32_t n = requested > 0 ? requested : auto_splits(num_decode, hkv, max_blocks);
-  n = std::max(1, std::min(n, std::max(1, max_blocks)));
+  n = std::max(1, std::min({n, std::max(1, max_blocks), kMaxSplits}));
   // No split may be empty for the longest sequence: shrink to ceil(P / pps).
   const int32_t pps = (max_blocks + n - 1) / n;
   return std::max(1, (max_blocks + pps - 1) / pps);
 }
 
-size_t workspace_layout(int32_t num_decode, int32_t hq, int32_t d, int32_t splits,
-                        size_t* lse_offset) {
-  if (splits <= 1 || num_decode <= 0) {
-    if (lse_offset) *lse_offset = 0;
-    return 0;
-  }
+// Workspace: [arrival counters int32, one per (decode row, kv head)]
+// [partial outputs fp32] [partial log-sum-exp fp32], each 256-byte aligned.
+struct WsLayout {
+  size_t o_off, lse_off, bytes;
+};
+
+WsLayout workspace_layout(int32_t num_decode, int32_t hq, int32_t hkv, int32_t d,
+                          int32_t splits) {
+  WsLayout w{0, 0, 0};
+  if (splits <= 1 || num_decode <= 0) return w;
+  auto up = [](size_t x) { return (x + 255) & ~(size_t)255; };
   const size_t rows = (size_t)num_decode * hq * splits;
-  const size_t o_bytes = (rows * d * sizeof(float) + 255) & ~(size_t)255;
-  if (lse_offset) *lse_offset = o_bytes;
-  return o_bytes + ((rows * sizeof(float) + 255) & ~(size_t)255);
+  w.o_off = up((size_t)num_decode * hkv * sizeof(int32_t));
+  w.lse_off = w.o_off + up(rows * d * sizeof(float));
+  w.bytes = w.lse_off + up(rows * sizeof(float));
+  return w;
 }
 
 }  // namespace
@@ -170,7 +182,7 @@ size_t rag_attn_decode_workspace_size(int32_t num_decode_seqs, int32_t num_q_hea
     return 0;
   const int32_t n = rag_attn_decode_num_splits(num_decode_seqs, num_kv_heads,
                                                max_blocks_per_seq, block_size, num_splits);
-  return workspace_layout(num_decode_seqs, num_q_heads, head_dim, n, nullptr);
+  return workspace_layout(num_decode_seqs, num_q_heads, num_kv_heads, head_dim, n).bytes;
 }
 
 rag_status rag_attn_decode_paged(const void* q, const void* k_cache, const void* v_cache,
@@ -210,8 +222,8 @@ rag_status rag_attn_decode_paged(const void* q, const void* k_cache, const void*
   const int32_t splits =
       num_decode > 0 ? resolve_splits(num_decode, num_kv_heads, max_blocks_per_seq, num_splits)
                      : 1;
-  size_t lse_off = 0;
-  const size_t need = workspace_layout(num_decode, num_q_heads, head_dim, splits, &lse_off);
+  const WsLayout ws = workspace_layout(num_decode, num_q_heads, num_kv_heads, head_dim, splits);
+  const size_t need = ws.bytes;
   if (need > 0 && (workspace == nullptr || workspace_bytes < need))
     return fail(RAG_ERR_WORKSPACE, "decode: workspace of %zu bytes needed, %zu given", need,
                 workspace == nullptr ? (size_t)0 : workspace_bytes);
@@ -272,9 +284,10 @@ rag_status rag_attn_decode_paged(const void* q, const void* k_cache, const void*
   a.d = head_dim;
   a.num_splits = splits;
   a.scale = softmax_scale;
-  a.part_o = need > 0 ? static_cast<float*>(workspace) : nullptr;
-  a.part_lse =
-      need > 0 ? reinterpret_cast<float*>(static_cast<char*>(workspace) + lse_off) : nullptr;
+  char* wsb = static_cast<char*>(workspace);
+  a.arrivals = need > 0 ? reinterpret_cast<int*>(wsb) : nullptr;
+  a.part_o = need > 0 ? reinterpret_cast<float*>(wsb + ws.o_off) : nullptr;
+  a.part_lse = need > 0 ? reinterpret_cast<float*>(wsb + ws.lse_off) : nullptr;
   const hipError_t e = rag::launch_paged(a, stream);
   if (e != hipSuccess) return fail(RAG_ERR_HIP, "decode launch: %s", hipGetErrorString(e));
   return ok();

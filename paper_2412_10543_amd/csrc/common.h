@@ -68,6 +68,24 @@ __device__ __forceinline__ bool wave_any(bool p) {
   return __builtin_amdgcn_ballot_w64(p) != 0;
 }
 
+// Device-coherent 4-byte store / load (global_store/load ... sc1): written
+// through to, or read from, the point where all XCDs agree, with no L2
+// write-back or invalidate of the whole cache.  Used only for the split-KV
+// partial results that another XCD may merge.
+__device__ __forceinline__ void store_coherent(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float load_coherent(const float* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// Waits until every memory access this wave issued has completed (the
+// coherent stores above have reached the coherence point).
+__device__ __forceinline__ void wait_all_memory() {
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_s_waitcnt(0);
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
 __device__ __forceinline__ u32x4 load16(const void* p) {
   return *reinterpret_cast<const u32x4*>(p);
 }
@@ -121,11 +139,15 @@ constexpr int kDecThreads = 256;
 constexpr int kDecWaves = kDecThreads / kWave;
 constexpr int kDecMaxGroup = 16;           // q heads per kv head (MFMA N)
 
-// Per wave: the V rows of the two pages of one step, row-major [32][D + 16].
-template <int D>
+// Per wave: the V rows of the NP pages of one step, row-major [16*NP][D + 16].
+#ifndef RAG_DEC_PAGES
+#define RAG_DEC_PAGES 2
+#endif
+constexpr int kDecPages = RAG_DEC_PAGES;   // pages per decode step
+template <int D, int NP = kDecPages>
 struct DecLds {
   static constexpr int kStrV = D + 16;
-  static constexpr int kElemsWave = 32 * kStrV;
+  static constexpr int kElemsWave = 16 * NP * kStrV;
   static constexpr int kBytes = kDecWaves * kElemsWave * 2;
 };
 

@@ -1,19 +1,23 @@
-// One decode unit on gfx950: a single wave attends the query rows of all q
-// heads of one GQA group (one decode token of one sequence) to a contiguous
-// range of pages of that sequence's paged KV cache.
+// One decode unit on gfx950: a workgroup of four waves attends the query row
+// of every q head of one GQA group (one decode token of one sequence) to a
+// contiguous range of pages of that sequence's paged KV cache.
 //
 // Method: paged KV (PagedAttention) read through the block table, split-KV
 // with a log-sum-exp merge of the partial results (Flash-Decoding), online
 // softmax in fp32.  Layout choices for CDNA4:
-//   * every K/V byte of the range is read once, for all G heads of the
-//     group, with 16-byte loads; for each key the four lane groups of a load
-//     instruction read 64 contiguous bytes of that key's row;
+//   * every K/V byte of the range is read once, for all G heads of the group,
+//     with 16-byte loads; the four waves take interleaved steps of NP pages,
+//     so at any time they stream neighbouring pages;
 //   * both products run on v_mfma_f32_16x16x32_bf16 with the G query heads as
 //     the N dimension (padded to 16): S^T = K Q^T straight from registers,
 //     then O^T = V^T P^T with the V rows staged row-major in a per-wave LDS
 //     slice and read back as V^T fragments by the transposing LDS read;
-//   * two pages (32 keys) per step; the next step's pages are loaded while
-//     the current step computes.
+//   * one register set per step is refilled as soon as it has been consumed,
+//     so the next step's pages are in flight while the current one computes;
+//   * the four waves' states are merged through LDS; a unit that covers only
+//     part of its sequence (a split) writes a normalised partial output and
+//     its log-sum-exp, and the last split of the sequence to finish merges
+//     all of them in the same kernel.
 #pragma once
 
 #include "common.h"
@@ -28,23 +32,27 @@ __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// Where a unit's result goes.  h0 is the first q head of the group.
 struct DecodeOut {
-  bf16_t* o;          // final output of head 0 of the group (null when split)
-  float* part_o;      // partial output of head 0 (null when not split)
-  float* part_lse;    // partial log-sum-exp of head 0
-  int head_stride_part;  // floats between consecutive heads in part_o (lse: / D)
+  bf16_t* o;            // final output row of head h0
+  float* part_o;        // partials of head h0: [head][split][D] (n_sp > 1)
+  float* part_lse;      // [head][split]
+  int* arrival;         // arrival counter of this (sequence, kv head)
+  int sp, n_sp, num_splits;
 };
 
-template <int D>
-__device__ __forceinline__ void decode_unit(
-    const bf16_t* __restrict__ q,          // query row of head 0 of the group
-    const bf16_t* __restrict__ kc,         // k cache at (block 0, kv head)
-    const bf16_t* __restrict__ vc,
-    size_t block_stride,                   // elements between blocks
-    const int32_t* __restrict__ table,     // block table row of the sequence
-    int kv_len, int group, int p_begin, int p_end, float scale,
-    const DecodeOut& out, bf16_t* __restrict__ vt /* per-wave LDS tile */) {
-  using L = DecLds<D>;
+// Per wave: attend the wave's steps of the page range.  Leaves, per lane
+// (head l16, lane group gq), the unnormalised O^T accumulators, the head's
+// sum of weights l (already reduced over the lane groups) and the reference
+// maximum m_used (raw score units).
+template <int D, int NP>
+__device__ __forceinline__ void decode_wave(
+    const bf16_t* __restrict__ q, const bf16_t* __restrict__ kc, const bf16_t* __restrict__ vc,
+    size_t block_stride, const int32_t* __restrict__ table, int kv_len, int group,
+    int p_first, int p_end, int p_stride, float scale, bf16_t* __restrict__ vt,
+    f32x4 (&oacc)[D / 16], float& m_used, float& l) {
+  static_assert(NP % 2 == 0, "pages are consumed in pairs (32 keys per MFMA)");
+  using L = DecLds<D, NP>;
   constexpr int kKs = D / 32;   // k-steps over d for S^T
   constexpr int kDt = D / 16;   // 16-row d tiles of O^T
   const int lane = threadIdx.x & 63;
@@ -57,79 +65,91 @@ __device__ __forceinline__ void decode_unit(
     u32x4 z = {0, 0, 0, 0};
     qf[ks] = as_bf16x8(l16 < group ? load16(q + (size_t)l16 * D + ks * 32 + gq * 8) : z);
   }
-  f32x4 oacc[kDt];
 #pragma unroll
   for (int dt = 0; dt < kDt; ++dt) oacc[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   const float c = scale * kLog2e;
   const float tau = kRescaleLog2 / c;
-  float m_used = -INFINITY;
-  float l = 0.f;
+  m_used = -INFINITY;
+  l = 0.f;
 
-  // Register staging for one step (two pages):
-  //   ka/kb: K rows as the MFMA A operand (key l16, d chunk 4*ks + gq)
-  //   va/vb: V rows (keys 4*gq + t, d chunk l16) for the LDS slice
-  u32x4 ka[kKs], kb[kKs], va[4], vb[4];
-  auto load_step = [&](int p) {
-    const bool has_b = p + 1 < p_end;
-    const size_t ba = (size_t)table[p] * block_stride;
-    const size_t bb = has_b ? (size_t)table[p + 1] * block_stride : ba;
+  //   kr[j]: K rows of page j as the MFMA A operand (key l16, d chunk 4*ks+gq)
+  //   vr[j]: V rows of page j (keys 4*gq + t, d chunk l16) for the LDS slice
+  u32x4 kr[NP][kKs], vr[NP][4];
+  constexpr int kVch = D / 8;                  // 16-byte chunks per V row
+  // Block ids of the wave's next 64 / NP steps, one per lane (lane NP*k + j
+  // holds page j of step k), fetched with one vector load so that issuing a
+  // step's loads never waits on a scalar block-table read.
+  constexpr int kStepsPerFetch = kWave / NP;
+  int ids = 0, ids_base = p_first;
+  auto fetch_ids = [&](int p_from) {
+    const int pg = p_from + (lane / NP) * p_stride + lane % NP;
+    ids = pg < p_end ? table[pg] : 0;
+    ids_base = p_from;
+  };
+  auto issue_loads = [&](int p0) {
+    const int k = (p0 - ids_base) / p_stride;
 #pragma unroll
-    for (int ks = 0; ks < kKs; ++ks) {
-      ka[ks] = load16(kc + ba + (size_t)l16 * D + ks * 32 + gq * 8);
-      kb[ks] = load16(kc + bb + (size_t)l16 * D + ks * 32 + gq * 8);
-    }
-    if constexpr (D == 128) {
+    for (int j = 0; j < NP; ++j) {
+      const int id = __builtin_amdgcn_readlane(ids, k * NP + (p0 + j < p_end ? j : 0));
+      const size_t base = (size_t)id * block_stride;
 #pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        va[t] = load16(vc + ba + (size_t)(4 * gq + t) * D + l16 * 8);
-        vb[t] = load16(vc + bb + (size_t)(4 * gq + t) * D + l16 * 8);
-      }
-    } else {
-      // D == 64: 8 chunks per row; lanes l16 and l16 + 8 load the same chunk
+      for (int ks = 0; ks < kKs; ++ks)
+        kr[j][ks] = load16(kc + base + (size_t)l16 * D + ks * 32 + gq * 8);
 #pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        va[t] = load16(vc + ba + (size_t)(4 * gq + t) * D + (l16 & 7) * 8);
-        vb[t] = load16(vc + bb + (size_t)(4 * gq + t) * D + (l16 & 7) * 8);
-      }
+      for (int t = 0; t < 4; ++t)
+        vr[j][t] = load16(vc + base + (size_t)(4 * gq + t) * D + (l16 % kVch) * 8);
     }
   };
 
   // transposing-read source: row 4*gq + l16/4, d 4*(l16%4) of a 16-d tile
   const int tr_off = (4 * gq + (l16 >> 2)) * L::kStrV + 4 * (l16 & 3);
 
-  if (p_begin < p_end) load_step(p_begin);
-  for (int p = p_begin; p < p_end; p += 2) {
-    const bool has_b = p + 1 < p_end;
+  if (p_first < p_end) {
+    fetch_ids(p_first);
+    issue_loads(p_first);
+  }
+  for (int p0 = p_first; p0 < p_end; p0 += p_stride) {
+    // ---- V rows into this wave's LDS slice (row 16*j + key of page j).  Rows
+    // of keys past kv_len (tail slots) or of pages past the range are zeroed
+    // so that whatever the pool holds there cannot reach the output. ---------
+#pragma unroll
+    for (int j = 0; j < NP; ++j) {
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const int key = 16 * (p0 + j) + 4 * gq + t;
+        const bool valid = p0 + j < p_end && key < kv_len;
+        u32x4 z = {0, 0, 0, 0};
+        if (l16 < kVch)
+          *reinterpret_cast<u32x4*>(vt + (16 * j + 4 * gq + t) * L::kStrV + l16 * 8) =
+              valid ? vr[j][t] : z;
+      }
+    }
     // ---- S^T = K Q^T: 16 keys x 16 heads per page --------------------------
-    f32x4 sa = {0.f, 0.f, 0.f, 0.f}, sb = {0.f, 0.f, 0.f, 0.f};
+    f32x4 sc[NP];
 #pragma unroll
-    for (int ks = 0; ks < kKs; ++ks) {
-      sa = mfma16(as_bf16x8(ka[ks]), qf[ks], sa);
-      sb = mfma16(as_bf16x8(kb[ks]), qf[ks], sb);
-    }
-    // V rows of keys past kv_len (tail slots) or of a missing second page are
-    // zeroed so that whatever the pool holds there cannot reach the output.
-    const int key_a = 16 * p + 4 * gq;       // this lane's first score key, page A
-    const int key_b = key_a + 16;
-    u32x4 z = {0, 0, 0, 0};
-    u32x4 wa[4], wb[4];
+    for (int j = 0; j < NP; ++j) {
+      sc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      wa[t] = (key_a + t < kv_len) ? va[t] : z;
-      wb[t] = (has_b && key_b + t < kv_len) ? vb[t] : z;
+      for (int ks = 0; ks < kKs; ++ks) sc[j] = mfma16(as_bf16x8(kr[j][ks]), qf[ks], sc[j]);
     }
-    // Prefetch the next step (registers ka/kb/va/vb are free again).
-    if (p + 2 < p_end) load_step(p + 2);
+    // ---- next step's loads go out now ---------------------------------------
+    if (p0 + p_stride < p_end) {
+      if ((p0 + p_stride - ids_base) / p_stride == kStepsPerFetch) fetch_ids(p0 + p_stride);
+      issue_loads(p0 + p_stride);
+    }
 
     // ---- mask and online softmax ---------------------------------------------
+    float tmax = -INFINITY;
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      if (key_a + t >= kv_len) sa[t] = -INFINITY;
-      if (!has_b || key_b + t >= kv_len) sb[t] = -INFINITY;
+    for (int j = 0; j < NP; ++j) {
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const int key = 16 * (p0 + j) + 4 * gq + t;
+        if (p0 + j >= p_end || key >= kv_len) sc[j][t] = -INFINITY;
+        tmax = fmaxf(tmax, sc[j][t]);
+      }
     }
-    float tmax = fmaxf(fmaxf(fmaxf(sa[0], sa[1]), fmaxf(sa[2], sa[3])),
-                       fmaxf(fmaxf(sb[0], sb[1]), fmaxf(sb[2], sb[3])));
     tmax = fmaxf(tmax, wave_xor(tmax, 16));
     tmax = fmaxf(tmax, wave_xor(tmax, 32));
     if (wave_any(tmax > m_used + tau)) {
@@ -141,61 +161,183 @@ __device__ __forceinline__ void decode_unit(
       m_used = m_new;
     }
     const float mref = (m_used == -INFINITY) ? 0.f : m_used * c;
-    float pa[4], pbv[4];
+    bf16x8 pfrag[NP / 2];
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      pa[t] = fast_exp2(fmaf(sa[t], c, -mref));
-      pbv[t] = fast_exp2(fmaf(sb[t], c, -mref));
-      l += pa[t] + pbv[t];
-    }
-    const bf16x8 pfrag = to_bf16x8(pa[0], pa[1], pa[2], pa[3], pbv[0], pbv[1], pbv[2], pbv[3]);
-
-    // ---- V rows of both pages into this wave's LDS slice, row-major:
-    // rows 0..15 page A, rows 16..31 page B ------------------------------------
-    if (D == 128 || l16 < 8) {
+    for (int pp = 0; pp < NP / 2; ++pp) {
+      float pv[8];
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
-        *reinterpret_cast<u32x4*>(vt + (4 * gq + t) * L::kStrV + l16 * 8) = wa[t];
-        *reinterpret_cast<u32x4*>(vt + (16 + 4 * gq + t) * L::kStrV + l16 * 8) = wb[t];
+        pv[t] = fast_exp2(fmaf(sc[2 * pp][t], c, -mref));
+        pv[4 + t] = fast_exp2(fmaf(sc[2 * pp + 1][t], c, -mref));
+        l += pv[t] + pv[4 + t];
       }
+      pfrag[pp] = to_bf16x8(pv[0], pv[1], pv[2], pv[3], pv[4], pv[5], pv[6], pv[7]);
     }
+
     wave_lds_sync();
     // ---- O^T += V^T P^T ------------------------------------------------------
-    // A operand of d-tile dt: slot 8*gq + t holds key 4*gq + t of page A
-    // (t < 4) or page B (t >= 4) at d = 16*dt + l16 -- two transposing reads
-    // whose 16-lane groups each cover 4 rows x 16 d of one page.
+    // Pair pp (pages 2pp, 2pp+1): A operand slot 8*gq + t holds key 4*gq + t
+    // of page 2pp (t < 4) or page 2pp+1 (t >= 4) at d = 16*dt + l16 -- two
+    // transposing reads whose 16-lane groups each cover 4 rows x 16 d.
 #pragma unroll
-    for (int dt = 0; dt < kDt; ++dt) {
-      const bf16x8 a = join_bf16x8(lds_read_tr4(vt + tr_off + 16 * dt),
-                                   lds_read_tr4(vt + 16 * L::kStrV + tr_off + 16 * dt));
-      oacc[dt] = mfma16(a, pfrag, oacc[dt]);
+    for (int pp = 0; pp < NP / 2; ++pp) {
+      const bf16_t* v0 = vt + 32 * pp * L::kStrV + tr_off;
+#pragma unroll
+      for (int dt = 0; dt < kDt; ++dt) {
+        const bf16x8 a = join_bf16x8(lds_read_tr4(v0 + 16 * dt),
+                                     lds_read_tr4(v0 + 16 * L::kStrV + 16 * dt));
+        oacc[dt] = mfma16(a, pfrag[pp], oacc[dt]);
+      }
     }
     wave_lds_sync();
   }
-
-  // ---- combine the four lane groups' sums and write ---------------------------
   l += wave_xor(l, 16);
   l += wave_xor(l, 32);
-  const float inv = l > 0.f ? 1.f / l : 0.f;
-  if (l16 < group) {
-    if (out.o != nullptr) {
-      bf16_t* orow = out.o + (size_t)l16 * D;
+}
+
+// Merge of the n_sp split partials of the q heads assigned to this wave (h =
+// wave, wave + 4, ...), in split order.  Lane sp holds split sp's weight; the
+// partial rows are read with device-coherent loads, 16 splits at a time, each
+// lane owning D/64 consecutive output values.
+template <int D>
+__device__ __forceinline__ void merge_splits(const DecodeOut& out, int group) {
+  constexpr int kPer = D / 64;                 // 2 (D = 128) or 1 (D = 64)
+  constexpr int kBatch = 16;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  for (int h = wave; h < group; h += kDecWaves) {
+    const float* pl = out.part_lse + (size_t)h * out.num_splits;
+    const float* po = out.part_o + (size_t)h * out.num_splits * D + lane * kPer;
+    const float lse = lane < out.n_sp ? load_coherent(pl + lane) : -INFINITY;
+    float mx = lse;
 #pragma unroll
-      for (int dt = 0; dt < kDt; ++dt) {
-        const bf16x4 w = to_bf16x4(oacc[dt][0] * inv, oacc[dt][1] * inv,
-                                   oacc[dt][2] * inv, oacc[dt][3] * inv);
-        *reinterpret_cast<bf16x4*>(orow + 16 * dt + 4 * gq) = w;
+    for (int m = 32; m >= 1; m >>= 1) mx = fmaxf(mx, wave_xor(mx, m));
+    const float w = (lse == -INFINITY) ? 0.f : fast_exp2((lse - mx) * kLog2e);
+    float den = w;
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) den += wave_xor(den, m);
+    float acc[kPer];
+#pragma unroll
+    for (int e = 0; e < kPer; ++e) acc[e] = 0.f;
+    for (int s0 = 0; s0 < out.n_sp; s0 += kBatch) {
+      float x[kBatch][kPer];
+#pragma unroll
+      for (int b = 0; b < kBatch; ++b) {
+        const int sp = s0 + b < out.n_sp ? s0 + b : s0;
+#pragma unroll
+        for (int e = 0; e < kPer; ++e) x[b][e] = load_coherent(po + (size_t)sp * D + e);
       }
-    } else {
-      float* prow = out.part_o + (size_t)l16 * out.head_stride_part;
 #pragma unroll
-      for (int dt = 0; dt < kDt; ++dt)
-        *reinterpret_cast<f32x4*>(prow + 16 * dt + 4 * gq) = oacc[dt] * inv;
-      if (gq == 0)
-        out.part_lse[(size_t)l16 * (out.head_stride_part / D)] =
-            l > 0.f ? m_used * scale + __logf(l) : -INFINITY;
+      for (int b = 0; b < kBatch; ++b) {
+        const float wb = __shfl(w, s0 + b < out.n_sp ? s0 + b : 0, kWave);
+        if (s0 + b < out.n_sp) {
+#pragma unroll
+          for (int e = 0; e < kPer; ++e) acc[e] += wb * x[b][e];
+        }
+      }
+    }
+    const float inv = den > 0.f ? 1.f / den : 0.f;
+#pragma unroll
+    for (int e = 0; e < kPer; ++e) {
+      const __bf16 b = (__bf16)(acc[e] * inv);
+      out.o[(size_t)h * D + lane * kPer + e] = __builtin_bit_cast(bf16_t, b);
     }
   }
+}
+
+// Bytes of LDS the merge of four waves needs (it reuses the V slices).
+template <int D>
+constexpr int dec_merge_bytes() {
+  return (kDecWaves * 16 * D + 2 * kDecWaves * 16 + 1) * 4;
+}
+
+// The whole unit: the workgroup's four waves cover the page range
+// [p_begin, p_end) in interleaved steps of NP pages, merge through LDS and
+// write either the final rows (n_sp == 1) or this split's partial rows; the
+// last split of the row to arrive then merges all partials.
+template <int D, int NP>
+__device__ __forceinline__ void decode_unit(
+    const bf16_t* __restrict__ q, const bf16_t* __restrict__ kc, const bf16_t* __restrict__ vc,
+    size_t block_stride, const int32_t* __restrict__ table, int kv_len, int group,
+    int p_begin, int p_end, float scale, const DecodeOut& out, bf16_t* __restrict__ lds) {
+  using L = DecLds<D, NP>;
+  static_assert(dec_merge_bytes<D>() <= L::kBytes, "merge area must fit in the V slices");
+  constexpr int kDt = D / 16;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int l16 = lane & 15, gq = lane >> 4;
+
+  f32x4 oacc[kDt];
+  float m_used, l;
+  decode_wave<D, NP>(q, kc, vc, block_stride, table, kv_len, group, p_begin + wave * NP, p_end,
+                     kDecWaves * NP, scale, lds + wave * L::kElemsWave, oacc, m_used, l);
+
+  // ---- merge the four waves through LDS (reusing the V slices) -------------
+  // floats: O [wave][16 heads][D], then m [wave][16], then l [wave][16]
+  float* mo = reinterpret_cast<float*>(lds);
+  float* mm = mo + kDecWaves * 16 * D;
+  float* ml = mm + kDecWaves * 16;
+  __syncthreads();
+  if (l16 < group) {
+#pragma unroll
+    for (int dt = 0; dt < kDt; ++dt)
+      *reinterpret_cast<f32x4*>(mo + (wave * 16 + l16) * D + 16 * dt + 4 * gq) = oacc[dt];
+    if (gq == 0) {
+      mm[wave * 16 + l16] = m_used;
+      ml[wave * 16 + l16] = l;
+    }
+  }
+  __syncthreads();
+  const float c = scale * kLog2e;
+  constexpr int kPer = D / 64;
+  for (int h = wave; h < group; h += kDecWaves) {
+    float m = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < kDecWaves; ++w) m = fmaxf(m, mm[w * 16 + h]);
+    float den = 0.f, acc[kPer];
+#pragma unroll
+    for (int e = 0; e < kPer; ++e) acc[e] = 0.f;
+#pragma unroll
+    for (int w = 0; w < kDecWaves; ++w) {
+      const float mw = mm[w * 16 + h];
+      const float f = (mw == -INFINITY) ? 0.f : fast_exp2((mw - m) * c);
+      den += f * ml[w * 16 + h];
+#pragma unroll
+      for (int e = 0; e < kPer; ++e) acc[e] += f * mo[(w * 16 + h) * D + lane * kPer + e];
+    }
+    const float inv = den > 0.f ? 1.f / den : 0.f;
+    if (out.n_sp <= 1) {
+#pragma unroll
+      for (int e = 0; e < kPer; ++e) {
+        const __bf16 b = (__bf16)(acc[e] * inv);
+        out.o[(size_t)h * D + lane * kPer + e] = __builtin_bit_cast(bf16_t, b);
+      }
+    } else {
+      // Partials may be merged by a workgroup on another XCD: coherent stores.
+      float* prow = out.part_o + ((size_t)h * out.num_splits + out.sp) * D + lane * kPer;
+#pragma unroll
+      for (int e = 0; e < kPer; ++e) store_coherent(prow + e, acc[e] * inv);
+      if (lane == 0)
+        store_coherent(out.part_lse + (size_t)h * out.num_splits + out.sp,
+                       den > 0.f ? m * scale + __logf(den) : -INFINITY);
+    }
+  }
+  if (out.n_sp <= 1) return;
+
+  // ---- arrival: the last split of this (sequence, kv head) merges ----------
+  // Every partial has gone out with device-coherent stores; once they have
+  // completed, one arrival is counted with a device-scope atomic.  The
+  // workgroup that sees the final count reads all partials with
+  // device-coherent loads and resets the counter, so the workspace is all-zero
+  // between calls.
+  wait_all_memory();
+  __syncthreads();
+  int* flag = reinterpret_cast<int*>(ml + kDecWaves * 16);
+  if (threadIdx.x == 0)
+    *flag = __hip_atomic_fetch_add(out.arrival, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  __syncthreads();
+  if (*flag != out.n_sp - 1) return;
+  merge_splits<D>(out, group);
+  if (threadIdx.x == 0)
+    __hip_atomic_store(out.arrival, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 }  // namespace rag

@@ -2,7 +2,8 @@
 //   prefill_varlen_kernel  packed variable-length prefill (dense K/V)
 //   paged_kernel           decode rows against a paged KV cache, optionally
 //                          with chunked-prefill pieces in the same launch
-//   combine_kernel         log-sum-exp merge of split-KV partial results
+//                          (split-KV partials are merged inside it by the
+//                          last split of each sequence to finish)
 #include <algorithm>
 #include <climits>
 
@@ -57,8 +58,7 @@ int64_t paged_prefill_grid(int num_pieces, int hkv, int group, int max_seqlen_q)
 }
 
 int64_t paged_decode_grid(int num_decode, int hkv, int num_splits) {
-  const int64_t units = (int64_t)num_decode * hkv * num_splits;
-  return (units + kDecWaves - 1) / kDecWaves;
+  return (int64_t)num_decode * hkv * num_splits;
 }
 
 template <int D>
@@ -85,10 +85,10 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_varlen_kernel(
 
 // ---------------------------------------------------------------------------
 // Paged kernel.  Blocks [0, n_pf_blocks) are chunked-prefill tiles (mixed
-// batches only); the rest hold four decode units each, one per wave.  Decode
-// unit u covers split sp = u / (num_decode * hkv) of (sequence, kv head)
-// u % (num_decode * hkv); split sp of a sequence with P pages is the page
-// range [sp * pps, min((sp + 1) * pps, P)).
+// batches only); each remaining block is one decode unit: split
+// sp = u / (num_decode * hkv) of (sequence, kv head) u % (num_decode * hkv),
+// where split sp of a sequence with P pages is the page range
+// [sp * pps, min((sp + 1) * pps, P)).
 // ---------------------------------------------------------------------------
 struct PagedKernelArgs {
   const bf16_t* q;
@@ -100,6 +100,7 @@ struct PagedKernelArgs {
   const int32_t* cu_q;
   float* part_o;
   float* part_lse;
+  int* arrivals;              // one counter per (decode sequence, kv head)
   int num_seqs, num_decode, max_blocks, hq, hkv, num_splits, pps;
   int n_pf_blocks, n_qt;
   float scale;
@@ -133,12 +134,10 @@ __global__ __launch_bounds__(256, 2) void paged_kernel(PagedKernelArgs a) {
     }
     block -= a.n_pf_blocks;
   }
-  const int wave = threadIdx.x >> 6;
-  const int64_t unit = (int64_t)block * kDecWaves + wave;
   const int64_t pairs = (int64_t)a.num_decode * a.hkv;
-  if (unit >= pairs * a.num_splits) return;
-  const int sp = (int)(unit / pairs);
-  const int pr = (int)(unit % pairs);
+  if ((int64_t)block >= pairs * a.num_splits) return;
+  const int sp = (int)(block / pairs);
+  const int pr = (int)(block % pairs);
   const int s = pr / a.hkv, kvh = pr % a.hkv;
   const int kv_len = a.kv_lens[s];
   const int n_pages = (kv_len + 15) >> 4;
@@ -149,66 +148,19 @@ __global__ __launch_bounds__(256, 2) void paged_kernel(PagedKernelArgs a) {
   const int row = a.cu_q ? a.cu_q[s] : s;
   const int h0 = kvh * group;
   DecodeOut out;
-  if (n_sp <= 1) {
-    out.o = a.o + ((size_t)row * a.hq + h0) * D;
-    out.part_o = nullptr;
-    out.part_lse = nullptr;
-    out.head_stride_part = 0;
-  } else {
-    out.o = nullptr;
-    out.part_o = a.part_o + (((size_t)s * a.hq + h0) * a.num_splits + sp) * D;
-    out.part_lse = a.part_lse + ((size_t)s * a.hq + h0) * a.num_splits + sp;
-    out.head_stride_part = a.num_splits * D;
-  }
-  decode_unit<D>(a.q + ((size_t)row * a.hq + h0) * D, a.kc + (size_t)kvh * 16 * D,
-                 a.vc + (size_t)kvh * 16 * D, block_stride, a.tables + (size_t)s * a.max_blocks,
-                 kv_len, group, p_begin, p_end, a.scale, out,
-                 lds + wave * DecLds<D>::kElemsWave);
-}
-
-// One wave per (decode row, q head): merge that row's split partials in
-// split order.  Rows whose sequence used a single split were written by the
-// paged kernel and are skipped.
-template <int D>
-__global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ part_o,
-                                                      const float* __restrict__ part_lse,
-                                                      bf16_t* __restrict__ o,
-                                                      const int32_t* __restrict__ kv_lens,
-                                                      const int32_t* __restrict__ cu_q,
-                                                      int num_decode, int hq, int num_splits,
-                                                      int pps) {
-  constexpr int kPer = D / 64;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int64_t idx = (int64_t)blockIdx.x * kDecWaves + wave;
-  if (idx >= (int64_t)num_decode * hq) return;
-  const int s = (int)(idx / hq), h = (int)(idx % hq);
-  const int n_pages = (kv_lens[s] + 15) >> 4;
-  const int n_sp = (n_pages + pps - 1) / pps;
-  if (n_sp <= 1) return;
-  const float* pl = part_lse + (size_t)idx * num_splits;
-  const float* po = part_o + (size_t)idx * num_splits * D;
-  float mx = -INFINITY;
-  for (int sp = 0; sp < n_sp; ++sp) mx = fmaxf(mx, pl[sp]);
-  float acc[kPer];
-#pragma unroll
-  for (int e = 0; e < kPer; ++e) acc[e] = 0.f;
-  float den = 0.f;
-  if (mx != -INFINITY) {
-    for (int sp = 0; sp < n_sp; ++sp) {
-      const float w = expf(pl[sp] - mx);
-      den += w;
-#pragma unroll
-      for (int e = 0; e < kPer; ++e) acc[e] += w * po[(size_t)sp * D + lane * kPer + e];
-    }
-  }
-  const float inv = den > 0.f ? 1.f / den : 0.f;
-  const int row = cu_q ? cu_q[s] : s;
-  bf16_t* orow = o + ((size_t)row * hq + h) * D + lane * kPer;
-#pragma unroll
-  for (int e = 0; e < kPer; ++e) {
-    const __bf16 b = (__bf16)(acc[e] * inv);
-    orow[e] = __builtin_bit_cast(bf16_t, b);
-  }
+  out.o = a.o + ((size_t)row * a.hq + h0) * D;
+  out.part_o = a.part_o ? a.part_o + (size_t)s * a.hq * a.num_splits * D +
+                              (size_t)h0 * a.num_splits * D
+                        : nullptr;
+  out.part_lse = a.part_lse ? a.part_lse + ((size_t)s * a.hq + h0) * a.num_splits : nullptr;
+  out.arrival = a.arrivals ? a.arrivals + (size_t)s * a.hkv + kvh : nullptr;
+  out.sp = sp;
+  out.n_sp = n_sp;
+  out.num_splits = a.num_splits;
+  decode_unit<D, kDecPages>(a.q + ((size_t)row * a.hq + h0) * D, a.kc + (size_t)kvh * 16 * D,
+                            a.vc + (size_t)kvh * 16 * D, block_stride,
+                            a.tables + (size_t)s * a.max_blocks, kv_len, group, p_begin, p_end,
+                            a.scale, out, lds);
 }
 
 // ---------------------------------------------------------------------------
@@ -243,6 +195,7 @@ static hipError_t launch_paged_d(const PagedArgs& a, hipStream_t stream) {
   k.cu_q = a.cu_q;
   k.part_o = a.part_o;
   k.part_lse = a.part_lse;
+  k.arrivals = a.arrivals;
   k.num_seqs = a.num_seqs;
   k.num_decode = a.num_decode;
   k.max_blocks = a.max_blocks;
@@ -266,14 +219,6 @@ static hipError_t launch_paged_d(const PagedArgs& a, hipStream_t stream) {
       hipLaunchKernelGGL((paged_kernel<D, false>), dim3((unsigned)grid), dim3(256), 0, stream, k);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-  }
-  if (a.num_splits > 1 && a.num_decode > 0) {
-    const int64_t rows = (int64_t)a.num_decode * a.hq;
-    const int64_t cgrid = (rows + kDecWaves - 1) / kDecWaves;
-    hipLaunchKernelGGL(combine_kernel<D>, dim3((unsigned)cgrid), dim3(256), 0, stream, a.part_o,
-                       a.part_lse, (bf16_t*)a.o, a.kv_lens, a.cu_q, a.num_decode, a.hq,
-                       a.num_splits, k.pps);
-    return hipGetLastError();
   }
   return hipSuccess;
 }

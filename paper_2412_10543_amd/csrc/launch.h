@@ -32,6 +32,7 @@ struct PagedArgs {
   float scale;
   float* part_o;                // workspace (null when num_splits == 1)
   float* part_lse;
+  int* arrivals;
 };
 
 // Launch-grid sizes, exposed so the host can check them before launching.

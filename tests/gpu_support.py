@@ -75,7 +75,7 @@ def oracle_prefill(orc, q, k, v, lens_q, lens_k, scale, causal=True):
 def workspace_for(num_decode, hq, hkv, d, max_blocks, num_splits=0):
     n = binding.rag_attn_decode_workspace_size(num_decode, hq, hkv, d, max_blocks, 16,
                                                num_splits)
-    return torch.empty(max(n, 1), dtype=torch.uint8, device="cuda") if n else None
+    return torch.zeros(max(n, 1), dtype=torch.uint8, device="cuda") if n else None
 
 
 def gpu_paged(q, pool, hq, hkv, d, scale, cu_q=None, num_decode=None, max_seqlen_q=1,

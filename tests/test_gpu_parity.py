@@ -130,6 +130,26 @@ def test_decode_matches_prefill_last_row():
     assert mx <= 2 * G.MAX_ABS and mean <= 2 * G.MEAN_ABS
 
 
+def test_decode_workspace_left_zeroed(orc):
+    """The in-kernel split merge counts arrivals in the workspace; every call
+    must leave the counters at zero, so back-to-back calls stay correct."""
+    q, pool = G.decode_case([3000, 70, 1500], 32, 8, 128, seed=41)
+    ws = G.workspace_for(3, 32, 8, 128, pool.block_tables.shape[1], num_splits=6)
+    ro = G.oracle_paged(orc, q, pool, G.scale_for(128))
+    outs = []
+    for _ in range(3):
+        o = torch.empty_like(q)
+        from paper_2412_10543_amd import binding
+        binding.rag_attn_decode_paged(q, pool.k_cache, pool.v_cache, o, pool.block_tables,
+                                      G.to_dev_i32(pool.kv_lens), G.scale_for(128),
+                                      num_splits=6, workspace=ws)
+        torch.cuda.synchronize()
+        assert int(ws[:3 * 8 * 4].count_nonzero()) == 0, "arrival counters not reset"
+        G.assert_parity(o, ro, "repeated split call")
+        outs.append(o)
+    assert torch.equal(outs[0], outs[1]) and torch.equal(outs[1], outs[2])
+
+
 def test_decode_splits_agree():
     q, pool = G.decode_case([5000, 3000], 32, 8, 128, seed=4)
     o1 = G.gpu_paged(q, pool, 32, 8, 128, G.scale_for(128), num_splits=1)
