@@ -215,7 +215,9 @@ def bench_phase_stuff(torch, w, dev, reps):
     return out
 
 
-def bench_phase_mixed(torch, dev, reps):
+def setup_mixed(torch, dev, n_pools=2):
+    """The mixed workload: 256 decode rows followed by 4 chunked-prefill
+    pieces, in one paged batch."""
     from paper_2412_10543_amd import binding
     from paper_2412_10543_amd.workloads import mixed, normal_bf16, paged_pool
     w = mixed()
@@ -224,26 +226,38 @@ def bench_phase_mixed(torch, dev, reps):
     cu = [0]
     for n in q_lens:
         cu.append(cu[-1] + n)
-    pools = [paged_pool(kv, w.hkv, w.d, w.seed + i, device=dev) for i in range(2)]
-    q = normal_bf16((cu[-1], w.hq, w.d), w.seed + 9, dev)
-    o = torch.empty_like(q)
-    nd = len(w.decode_kv_lens)
-    mb = pools[0].block_tables.shape[1]
-    n = binding.rag_attn_decode_workspace_size(nd, w.hq, w.hkv, w.d, mb)
-    ws = torch.zeros(max(n, 256), dtype=torch.uint8, device=dev)
-    cu_t = torch.tensor(cu, dtype=torch.int32, device=dev)
-    kv_t = torch.tensor(kv, dtype=torch.int32, device=dev)
+    st = {"w": w, "kv": kv, "q_lens": q_lens, "cu": cu, "nd": len(w.decode_kv_lens)}
+    st["pools"] = [paged_pool(kv, w.hkv, w.d, w.seed + i, device=dev) for i in range(n_pools)]
+    st["q"] = normal_bf16((cu[-1], w.hq, w.d), w.seed + 9, dev)
+    st["o"] = torch.empty_like(st["q"])
+    mb = st["pools"][0].block_tables.shape[1]
+    n = binding.rag_attn_decode_workspace_size(st["nd"], w.hq, w.hkv, w.d, mb)
+    st["ws"] = torch.zeros(max(n, 256), dtype=torch.uint8, device=dev)
+    st["cu_t"] = torch.tensor(cu, dtype=torch.int32, device=dev)
+    st["kv_t"] = torch.tensor(kv, dtype=torch.int32, device=dev)
+    st["splits"] = binding.rag_attn_decode_num_splits(st["nd"], w.hkv, mb)
+    return st
 
-    def call(pool):
-        binding.rag_attn_decode_paged(q, pool.k_cache, pool.v_cache, o, pool.block_tables, kv_t,
-                                      w.scale, cu_seqlens_q=cu_t, num_decode_seqs=nd,
-                                      max_seqlen_q=w.piece_len, workspace=ws)
-    call(pools[0])
+
+def run_mixed(st, pool_index=0):
+    from paper_2412_10543_amd import binding
+    w = st["w"]
+    pool = st["pools"][pool_index]
+    binding.rag_attn_decode_paged(st["q"], pool.k_cache, pool.v_cache, st["o"], pool.block_tables,
+                                  st["kv_t"], w.scale, cu_seqlens_q=st["cu_t"],
+                                  num_decode_seqs=st["nd"], max_seqlen_q=w.piece_len,
+                                  workspace=st["ws"])
+
+
+def bench_phase_mixed(torch, dev, reps):
+    st = setup_mixed(torch, dev)
+    w = st["w"]
+    run_mixed(st, 0)
     torch.cuda.synchronize()
     timer = Timer(torch)
     for r in range(reps):
         timer.start("mixed")
-        call(pools[r % 2])
+        run_mixed(st, r % 2)
         timer.stop("mixed")
     torch.cuda.synchronize()
     ms = median(timer.ms("mixed"))
@@ -254,14 +268,14 @@ def bench_phase_mixed(torch, dev, reps):
     pbytes = decode_bytes(pl_k, w.hq, w.hkv, w.d, q_rows=pl_q)
     t_hbm = (dbytes + pbytes) / (PEAK_HBM_GBS * 1e6)
     t_mfma = pfl / (PEAK_BF16_TFLOPS * 1e9)
-    out = {"decode_seqs": nd, "pieces": len(w.piece_prior), "piece_len": w.piece_len,
+    out = {"decode_seqs": st["nd"], "pieces": len(w.piece_prior), "piece_len": w.piece_len,
            "ms": round(ms, 4), "kv_gbs": round((dbytes + pbytes) / ms / 1e6, 1),
            "piece_tflops": round(pfl / ms / 1e9, 1),
            "roofline_ms_overlapped": round(max(t_hbm, t_mfma), 4),
            "roofline_ms_serial": round(t_hbm + t_mfma, 4),
            "frac_of_overlapped_roofline": round(max(t_hbm, t_mfma) / ms, 4),
-           "splits": binding.rag_attn_decode_num_splits(nd, w.hkv, mb)}
-    del pools, q, o
+           "splits": st["splits"]}
+    del st
     torch.cuda.empty_cache()
     return out
 

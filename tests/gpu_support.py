@@ -109,3 +109,45 @@ def decode_case(kv_lens, hq, hkv, d, seed, q_scale=1.0):
 
 def scale_for(d):
     return 1.0 / math.sqrt(d)
+
+
+# ---------------------------------------------------------------------------
+# full-size workloads: sampled rows
+# ---------------------------------------------------------------------------
+def sample_rows(L, chunk_len, rng, n_random=16):
+    """Row 0, the last row, both sides of every chunk boundary and seeded
+    random rows of a prompt of L tokens."""
+    rows = {0, L - 1}
+    for b in range(chunk_len, L, chunk_len):
+        rows.update((b - 1, b))
+    rows.update(int(x) for x in rng.integers(0, L, size=n_random))
+    return sorted(r for r in rows if 0 <= r < L)
+
+
+def heads_for_row(row, hq, hkv):
+    """One q head per kv group, rotating inside the group with the row."""
+    g = hq // hkv
+    return [kv * g + (row + kv) % g for kv in range(hkv)]
+
+
+def dense_kv_of_seq(pool, s, n):
+    """Keys and values 0..n-1 of sequence s gathered from the paged pool
+    (test-side gather through the block table), as bf16 bit arrays
+    [n, hkv, d]."""
+    nb = (n + 15) // 16
+    blocks = pool.block_tables[s, :nb].long()
+    hkv, d = pool.k_cache.shape[1], pool.k_cache.shape[3]
+    k = pool.k_cache[blocks].permute(0, 2, 1, 3).reshape(nb * 16, hkv, d)[:n]
+    v = pool.v_cache[blocks].permute(0, 2, 1, 3).reshape(nb * 16, hkv, d)[:n]
+    return bf16_bits(k), bf16_bits(v)
+
+
+def oracle_seq_rows(orc, q_seq, k_bits, v_bits, nq, rows, heads, scale):
+    """Oracle rows of one sequence.  q_seq: GPU tensor [nq, hq, d] of that
+    sequence; rows/heads: parallel lists."""
+    idx_r = torch.as_tensor(rows, device=q_seq.device).long()
+    idx_h = torch.as_tensor(heads, device=q_seq.device).long()
+    qr = bf16_bits(q_seq[idx_r, idx_h])
+    o, lse = orc.seq_rows(qr, k_bits, v_bits, nq, np.asarray(rows), np.asarray(heads),
+                          q_seq.shape[1], scale)
+    return o, lse
