@@ -114,10 +114,20 @@ __device__ __forceinline__ void xcd_slot(int n, int& xcd, int& local) {
   local = n / kNumXcd;
 }
 
-// Prefill tiling shared by host and device.
-constexpr int kPfBM = 128;          // query rows per workgroup
+// Prefill tiling shared by host and device.  A workgroup is 4 waves of 32
+// query rows each; the waves cover the q heads of one GQA group that read the
+// same K/V (pf_heads_per_wg of them) times pf_row_blocks 32-row blocks.
+constexpr int kPfRowsPerWave = 32;
 constexpr int kPfBN = 64;           // keys per K/V tile
-constexpr int kPfThreads = 256;     // 4 waves x 32 query rows
+constexpr int kPfThreads = 256;
+constexpr int kPfWaves = 4;
+
+__host__ __device__ constexpr int pf_heads_per_wg(int group) {
+  return group % 4 == 0 ? 4 : (group % 2 == 0 ? 2 : 1);
+}
+__host__ __device__ constexpr int pf_rows_per_tile(int group) {
+  return kPfRowsPerWave * (kPfWaves / pf_heads_per_wg(group));
+}
 
 // K and V tiles are both row-major [key][d] in LDS.  K rows are padded by
 // 16 B (consecutive rows land 4 banks apart: the 16-byte A-operand reads of 8

@@ -16,41 +16,50 @@ namespace rag {
 
 // ---------------------------------------------------------------------------
 // Work order of prefill tiles.  A "stream" is one (sequence, kv head) pair;
-// all q heads of its GQA group and all its query tiles read the same K/V.
-// Stream sigma runs on XCD sigma % 8, so every XCD gets the same mix of
-// sequences (and, with 8 kv heads, exactly one kv head of each).  On an XCD
-// the order is: stream, then query tile from the last (most keys) to the
-// first, then the q heads of the group -- the workgroups resident on one XCD
-// at a time share K/V tiles through its L2.
+// all q heads of its GQA group and all its query tiles read the same K/V.  A
+// workgroup takes up to four of the group's q heads for one query tile, so
+// each K/V tile it stages in LDS serves all of them.  Stream sigma runs on XCD
+// sigma % 8, so every XCD gets the same mix of sequences (and, with 8 kv
+// heads, exactly one kv head of each).  On an XCD the order is: stream, then
+// query tile from the last (most keys) to the first, then the head groups --
+// the workgroups resident on one XCD at a time share K/V tiles through its L2.
 // ---------------------------------------------------------------------------
 struct TileCoord {
-  int seq, kvh, head, qt;
+  int seq, kvh, head, qt, q0, rows, r0;
   bool valid;
 };
 
+// Workgroup -> (stream, query tile, head group); wave -> (head, row block).
 __device__ __forceinline__ TileCoord prefill_coord(int block, int num_streams, int hkv,
                                                    int group, int n_qt) {
+  const int hw = pf_heads_per_wg(group);
+  const int ng = group / hw;
   int xcd, local;
   xcd_slot(block, xcd, local);
-  const int g = local % group;
-  const int rest = local / group;
+  const int hg = local % ng;
+  const int rest = local / ng;
   const int tile_rank = rest % n_qt;
   const int r = rest / n_qt;
   const int stream = xcd + kNumXcd * r;
+  const int wave = threadIdx.x >> 6;
   TileCoord t;
   t.valid = stream < num_streams;
   t.seq = stream / hkv;
   t.kvh = stream % hkv;
-  t.head = t.kvh * group + g;
+  t.head = t.kvh * group + hg * hw + wave % hw;
   t.qt = n_qt - 1 - tile_rank;
+  t.rows = pf_rows_per_tile(group);
+  t.q0 = t.qt * t.rows;
+  t.r0 = t.q0 + kPfRowsPerWave * (wave / hw);
   return t;
 }
 
 int64_t prefill_grid(int num_seqs, int hkv, int group, int max_seqlen_q) {
   const int64_t streams = (int64_t)num_seqs * hkv;
   const int64_t per_xcd = (streams + kNumXcd - 1) / kNumXcd;
-  const int64_t n_qt = (max_seqlen_q + kPfBM - 1) / kPfBM;
-  return (int64_t)kNumXcd * per_xcd * n_qt * group;
+  const int rows = pf_rows_per_tile(group);
+  const int64_t n_qt = (max_seqlen_q + rows - 1) / rows;
+  return (int64_t)kNumXcd * per_xcd * n_qt * (group / pf_heads_per_wg(group));
 }
 
 int64_t paged_prefill_grid(int num_pieces, int hkv, int group, int max_seqlen_q) {
@@ -73,14 +82,14 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_varlen_kernel(
   if (!tc.valid) return;
   const int qb = cu_q[tc.seq], nq = cu_q[tc.seq + 1] - qb;
   const int kb = cu_k[tc.seq], nk = cu_k[tc.seq + 1] - kb;
-  if (tc.qt * kPfBM >= nq) return;
+  if (tc.q0 >= nq) return;
   const int tq = cu_q[num_seqs];
   const size_t qs = (size_t)hq * D;
   DenseKV kv{k + ((size_t)kb * hkv + tc.kvh) * D, v + ((size_t)kb * hkv + tc.kvh) * D,
              (size_t)hkv * D};
   prefill_tile<D>(q + ((size_t)qb * hq + tc.head) * D, qs, o + ((size_t)qb * hq + tc.head) * D,
-                  qs, lse ? lse + (size_t)tc.head * tq + qb : nullptr, kv, nq, nk, tc.qt, scale,
-                  causal, lds);
+                  qs, lse ? lse + (size_t)tc.head * tq + qb : nullptr, kv, nq, nk, tc.q0, tc.rows,
+                  tc.r0, scale, causal, lds);
 }
 
 // ---------------------------------------------------------------------------
@@ -122,14 +131,14 @@ __global__ __launch_bounds__(256, 2) void paged_kernel(PagedKernelArgs a) {
       if (!tc.valid) return;
       const int s = a.num_decode + tc.seq;
       const int qb = a.cu_q[s], nq = a.cu_q[s + 1] - qb;
-      if (tc.qt * kPfBM >= nq) return;
+      if (tc.q0 >= nq) return;
       const int nk = a.kv_lens[s];
       const size_t qs = (size_t)a.hq * D;
       PagedKV<D> kv{a.kc + (size_t)tc.kvh * 16 * D, a.vc + (size_t)tc.kvh * 16 * D,
                     a.tables + (size_t)s * a.max_blocks, block_stride};
       prefill_tile<D>(a.q + ((size_t)qb * a.hq + tc.head) * D, qs,
-                      a.o + ((size_t)qb * a.hq + tc.head) * D, qs, nullptr, kv, nq, nk, tc.qt,
-                      a.scale, 1, lds);
+                      a.o + ((size_t)qb * a.hq + tc.head) * D, qs, nullptr, kv, nq, nk, tc.q0,
+                      tc.rows, tc.r0, a.scale, 1, lds);
       return;
     }
     block -= a.n_pf_blocks;
@@ -171,7 +180,8 @@ static hipError_t launch_prefill_d(const PrefillArgs& a, hipStream_t stream) {
   const int group = a.hq / a.hkv;
   const int64_t grid = prefill_grid(a.num_seqs, a.hkv, group, a.max_seqlen_q);
   if (grid == 0) return hipSuccess;
-  const int n_qt = (a.max_seqlen_q + kPfBM - 1) / kPfBM;
+  const int rows = pf_rows_per_tile(group);
+  const int n_qt = (a.max_seqlen_q + rows - 1) / rows;
   hipLaunchKernelGGL(prefill_varlen_kernel<D>, dim3((unsigned)grid), dim3(kPfThreads), 0, stream,
                      (const bf16_t*)a.q, (const bf16_t*)a.k, (const bf16_t*)a.v, (bf16_t*)a.o,
                      a.lse, a.cu_q, a.cu_k, a.num_seqs, a.hq, a.hkv, n_qt, a.scale, a.causal);
@@ -205,7 +215,8 @@ static hipError_t launch_paged_d(const PagedArgs& a, hipStream_t stream) {
   k.pps = std::max(1, (a.max_blocks + a.num_splits - 1) / a.num_splits);
   k.scale = a.scale;
   const bool mixed = a.cu_q != nullptr && a.num_seqs > a.num_decode;
-  k.n_qt = mixed ? (a.max_seqlen_q + kPfBM - 1) / kPfBM : 0;
+  const int pf_rows = pf_rows_per_tile(group);
+  k.n_qt = mixed ? (a.max_seqlen_q + pf_rows - 1) / pf_rows : 0;
   const int64_t pf = mixed ? paged_prefill_grid(a.num_seqs - a.num_decode, a.hkv, group,
                                                 a.max_seqlen_q)
                            : 0;

@@ -1,11 +1,14 @@
-// Causal (or full) attention of one 128-row query tile of one q head against
-// the keys of its sequence, for gfx950.
+// Causal (or full) attention of one query tile against the keys of its
+// sequence, for gfx950: four waves of 32 rows each, covering up to four q heads
+// of one GQA group (which share every K/V tile) times the row blocks of the
+// tile.
 //
 // Method: exact tiled attention with an online softmax (FlashAttention's
 // forward pass; the running-max rescaling of Milakov & Gimelshein), laid out
 // for CDNA4:
-//   * 4 waves, each owning 32 query rows; the wave keeps its Q rows in
-//     registers as the B operand of v_mfma_f32_32x32x16_bf16;
+//   * 4 waves, each owning 32 query rows of one head; the wave keeps its Q
+//     rows in registers as the B operand of v_mfma_f32_32x32x16_bf16; K/V
+//     tiles are shared by all heads of the group in the workgroup;
 //   * K/V tiles of 64 keys are staged through LDS row-major ([key][d]),
 //     double-buffered, with one barrier per tile; the global loads of tile
 //     t+1 are in flight while tile t is computed;
@@ -51,12 +54,14 @@ struct PagedKV {
   __device__ __forceinline__ const bf16_t* vrow(int j) const { return v + off(j); }
 };
 
+// q, o and lse point at row 0 of the sequence for this wave's head; the
+// workgroup covers rows [q0, q0 + wg_rows) and this wave rows [r0, r0 + 32).
 template <int D, class KV>
 __device__ __forceinline__ void prefill_tile(
-    const bf16_t* __restrict__ q, size_t q_stride,   // row 0 of this seq, this head
+    const bf16_t* __restrict__ q, size_t q_stride,
     bf16_t* __restrict__ o, size_t o_stride,
     float* __restrict__ lse,                         // lse of row 0 (stride 1) or null
-    const KV& kv, int nq, int nk, int qt, float scale, int causal,
+    const KV& kv, int nq, int nk, int q0, int wg_rows, int r0, float scale, int causal,
     bf16_t* __restrict__ lds) {
   using L = PfLds<D>;
   constexpr int kCh = D / 8;                  // 16-byte chunks per row
@@ -66,14 +71,12 @@ __device__ __forceinline__ void prefill_tile(
   constexpr int kDt = D / 32;                 // 32-row d tiles of O^T
 
   const int tid = threadIdx.x;
-  const int wave = tid >> 6, lane = tid & 63;
+  const int lane = tid & 63;
   const int l32 = lane & 31, half = lane >> 5;
-  const int q0 = qt * kPfBM;
   const int off = nk - nq;                    // bottom-right causal offset
-  const int r0 = q0 + 32 * wave;
   const int row = r0 + l32;
 
-  const int wg_last = min(q0 + kPfBM, nq) - 1;
+  const int wg_last = min(q0 + wg_rows, nq) - 1;
   const int kend = causal ? min(nk, wg_last + off + 1) : nk;
   const int w_last = min(r0 + 32, nq) - 1;
   const int kend_w = (r0 >= nq) ? 0 : (causal ? min(nk, w_last + off + 1) : nk);
