@@ -114,19 +114,22 @@ __device__ __forceinline__ void xcd_slot(int n, int& xcd, int& local) {
   local = n / kNumXcd;
 }
 
-// Prefill tiling shared by host and device.  A workgroup is 4 waves of 32
+// Prefill tiling shared by host and device.  A workgroup is W waves of 32
 // query rows each; the waves cover the q heads of one GQA group that read the
-// same K/V (pf_heads_per_wg of them) times pf_row_blocks 32-row blocks.
+// same K/V (pf_heads_per_wg of them) times W / pf_heads_per_wg row blocks.  The
+// dense prefill kernel uses 8 waves, which lets it hold two tiles of K/V
+// loads in flight per thread; the chunked-prefill pieces of the mixed paged
+// kernel use 4 (that kernel's decode units are 4-wave workgroups).
 constexpr int kPfRowsPerWave = 32;
 constexpr int kPfBN = 64;           // keys per K/V tile
-constexpr int kPfThreads = 256;
-constexpr int kPfWaves = 4;
+constexpr int kPfWavesDense = 8;
+constexpr int kPfWavesMixed = 4;
 
 __host__ __device__ constexpr int pf_heads_per_wg(int group) {
   return group % 4 == 0 ? 4 : (group % 2 == 0 ? 2 : 1);
 }
-__host__ __device__ constexpr int pf_rows_per_tile(int group) {
-  return kPfRowsPerWave * (kPfWaves / pf_heads_per_wg(group));
+__host__ __device__ constexpr int pf_rows_per_tile(int group, int waves) {
+  return kPfRowsPerWave * (waves / pf_heads_per_wg(group));
 }
 
 // K and V tiles are both row-major [key][d] in LDS.  K rows are padded by

@@ -30,6 +30,7 @@ struct TileCoord {
 };
 
 // Workgroup -> (stream, query tile, head group); wave -> (head, row block).
+template <int W>
 __device__ __forceinline__ TileCoord prefill_coord(int block, int num_streams, int hkv,
                                                    int group, int n_qt) {
   const int hw = pf_heads_per_wg(group);
@@ -48,22 +49,26 @@ __device__ __forceinline__ TileCoord prefill_coord(int block, int num_streams, i
   t.kvh = stream % hkv;
   t.head = t.kvh * group + hg * hw + wave % hw;
   t.qt = n_qt - 1 - tile_rank;
-  t.rows = pf_rows_per_tile(group);
+  t.rows = pf_rows_per_tile(group, W);
   t.q0 = t.qt * t.rows;
   t.r0 = t.q0 + kPfRowsPerWave * (wave / hw);
   return t;
 }
 
-int64_t prefill_grid(int num_seqs, int hkv, int group, int max_seqlen_q) {
+static int64_t tile_grid(int num_seqs, int hkv, int group, int max_seqlen_q, int waves) {
   const int64_t streams = (int64_t)num_seqs * hkv;
   const int64_t per_xcd = (streams + kNumXcd - 1) / kNumXcd;
-  const int rows = pf_rows_per_tile(group);
+  const int rows = pf_rows_per_tile(group, waves);
   const int64_t n_qt = (max_seqlen_q + rows - 1) / rows;
   return (int64_t)kNumXcd * per_xcd * n_qt * (group / pf_heads_per_wg(group));
 }
 
+int64_t prefill_grid(int num_seqs, int hkv, int group, int max_seqlen_q) {
+  return tile_grid(num_seqs, hkv, group, max_seqlen_q, kPfWavesDense);
+}
+
 int64_t paged_prefill_grid(int num_pieces, int hkv, int group, int max_seqlen_q) {
-  return prefill_grid(num_pieces, hkv, group, max_seqlen_q);
+  return tile_grid(num_pieces, hkv, group, max_seqlen_q, kPfWavesMixed);
 }
 
 int64_t paged_decode_grid(int num_decode, int hkv, int num_splits) {
@@ -71,14 +76,15 @@ int64_t paged_decode_grid(int num_decode, int hkv, int num_splits) {
 }
 
 template <int D>
-__global__ __launch_bounds__(kPfThreads, 2) void prefill_varlen_kernel(
+__global__ __launch_bounds__(64 * kPfWavesDense, 2) void prefill_varlen_kernel(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ k,
     const bf16_t* __restrict__ v, bf16_t* __restrict__ o, float* __restrict__ lse,
     const int32_t* __restrict__ cu_q, const int32_t* __restrict__ cu_k, int num_seqs,
     int hq, int hkv, int n_qt, float scale, int causal) {
   __shared__ __attribute__((aligned(16))) bf16_t lds[PfLds<D>::kBytes / 2];
   const int group = hq / hkv;
-  const TileCoord tc = prefill_coord(blockIdx.x, num_seqs * hkv, hkv, group, n_qt);
+  const TileCoord tc =
+      prefill_coord<kPfWavesDense>(blockIdx.x, num_seqs * hkv, hkv, group, n_qt);
   if (!tc.valid) return;
   const int qb = cu_q[tc.seq], nq = cu_q[tc.seq + 1] - qb;
   const int kb = cu_k[tc.seq], nk = cu_k[tc.seq + 1] - kb;
@@ -87,7 +93,8 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_varlen_kernel(
   const size_t qs = (size_t)hq * D;
   DenseKV kv{k + ((size_t)kb * hkv + tc.kvh) * D, v + ((size_t)kb * hkv + tc.kvh) * D,
              (size_t)hkv * D};
-  prefill_tile<D>(q + ((size_t)qb * hq + tc.head) * D, qs, o + ((size_t)qb * hq + tc.head) * D,
+  prefill_tile<D, kPfWavesDense, 2>(q + ((size_t)qb * hq + tc.head) * D, qs,
+                                    o + ((size_t)qb * hq + tc.head) * D,
                   qs, lse ? lse + (size_t)tc.head * tq + qb : nullptr, kv, nq, nk, tc.q0, tc.rows,
                   tc.r0, scale, causal, lds);
 }
@@ -127,7 +134,8 @@ __global__ __launch_bounds__(256, 2) void paged_kernel(PagedKernelArgs a) {
   if constexpr (kMixed) {
     if (block < a.n_pf_blocks) {
       const int num_pieces = a.num_seqs - a.num_decode;
-      const TileCoord tc = prefill_coord(block, num_pieces * a.hkv, a.hkv, group, a.n_qt);
+      const TileCoord tc =
+          prefill_coord<kPfWavesMixed>(block, num_pieces * a.hkv, a.hkv, group, a.n_qt);
       if (!tc.valid) return;
       const int s = a.num_decode + tc.seq;
       const int qb = a.cu_q[s], nq = a.cu_q[s + 1] - qb;
@@ -136,7 +144,7 @@ __global__ __launch_bounds__(256, 2) void paged_kernel(PagedKernelArgs a) {
       const size_t qs = (size_t)a.hq * D;
       PagedKV<D> kv{a.kc + (size_t)tc.kvh * 16 * D, a.vc + (size_t)tc.kvh * 16 * D,
                     a.tables + (size_t)s * a.max_blocks, block_stride};
-      prefill_tile<D>(a.q + ((size_t)qb * a.hq + tc.head) * D, qs,
+      prefill_tile<D, kPfWavesMixed, 1>(a.q + ((size_t)qb * a.hq + tc.head) * D, qs,
                       a.o + ((size_t)qb * a.hq + tc.head) * D, qs, nullptr, kv, nq, nk, tc.q0,
                       tc.rows, tc.r0, a.scale, 1, lds);
       return;
@@ -180,9 +188,10 @@ static hipError_t launch_prefill_d(const PrefillArgs& a, hipStream_t stream) {
   const int group = a.hq / a.hkv;
   const int64_t grid = prefill_grid(a.num_seqs, a.hkv, group, a.max_seqlen_q);
   if (grid == 0) return hipSuccess;
-  const int rows = pf_rows_per_tile(group);
+  const int rows = pf_rows_per_tile(group, kPfWavesDense);
   const int n_qt = (a.max_seqlen_q + rows - 1) / rows;
-  hipLaunchKernelGGL(prefill_varlen_kernel<D>, dim3((unsigned)grid), dim3(kPfThreads), 0, stream,
+  hipLaunchKernelGGL(prefill_varlen_kernel<D>, dim3((unsigned)grid), dim3(64 * kPfWavesDense), 0,
+                     stream,
                      (const bf16_t*)a.q, (const bf16_t*)a.k, (const bf16_t*)a.v, (bf16_t*)a.o,
                      a.lse, a.cu_q, a.cu_k, a.num_seqs, a.hq, a.hkv, n_qt, a.scale, a.causal);
   return hipGetLastError();
@@ -215,7 +224,7 @@ static hipError_t launch_paged_d(const PagedArgs& a, hipStream_t stream) {
   k.pps = std::max(1, (a.max_blocks + a.num_splits - 1) / a.num_splits);
   k.scale = a.scale;
   const bool mixed = a.cu_q != nullptr && a.num_seqs > a.num_decode;
-  const int pf_rows = pf_rows_per_tile(group);
+  const int pf_rows = pf_rows_per_tile(group, kPfWavesMixed);
   k.n_qt = mixed ? (a.max_seqlen_q + pf_rows - 1) / pf_rows : 0;
   const int64_t pf = mixed ? paged_prefill_grid(a.num_seqs - a.num_decode, a.hkv, group,
                                                 a.max_seqlen_q)

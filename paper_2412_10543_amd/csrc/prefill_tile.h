@@ -6,12 +6,12 @@
 // Method: exact tiled attention with an online softmax (FlashAttention's
 // forward pass; the running-max rescaling of Milakov & Gimelshein), laid out
 // for CDNA4:
-//   * 4 waves, each owning 32 query rows of one head; the wave keeps its Q
+//   * 4 or 8 waves, each owning 32 query rows of one head; the wave keeps its Q
 //     rows in registers as the B operand of v_mfma_f32_32x32x16_bf16; K/V
 //     tiles are shared by all heads of the group in the workgroup;
 //   * K/V tiles of 64 keys are staged through LDS row-major ([key][d]),
-//     double-buffered, with one barrier per tile; the global loads of tile
-//     t+1 are in flight while tile t is computed;
+//     double-buffered, with one barrier per tile; the global loads of the
+//     next one or two tiles are in flight while a tile is computed;
 //   * scores are computed transposed, S^T = K Q^T, so each lane owns one query
 //     row and its scores already sit where the B operand of O^T = V^T P^T
 //     needs them; the matching V^T A operand comes straight from the
@@ -55,8 +55,10 @@ struct PagedKV {
 };
 
 // q, o and lse point at row 0 of the sequence for this wave's head; the
-// workgroup covers rows [q0, q0 + wg_rows) and this wave rows [r0, r0 + 32).
-template <int D, class KV>
+// workgroup (W waves) covers rows [q0, q0 + wg_rows) and this wave rows
+// [r0, r0 + 32).  DEPTH = number of K/V tiles whose global loads are in
+// flight while a tile is computed (1 or 2).
+template <int D, int W, int DEPTH, class KV>
 __device__ __forceinline__ void prefill_tile(
     const bf16_t* __restrict__ q, size_t q_stride,
     bf16_t* __restrict__ o, size_t o_stride,
@@ -64,9 +66,12 @@ __device__ __forceinline__ void prefill_tile(
     const KV& kv, int nq, int nk, int q0, int wg_rows, int r0, float scale, int causal,
     bf16_t* __restrict__ lds) {
   using L = PfLds<D>;
+  static_assert(DEPTH == 1 || DEPTH == 2, "prefetch depth");
+  constexpr int kThreads = 64 * W;
   constexpr int kCh = D / 8;                  // 16-byte chunks per row
-  constexpr int kRowsPerIt = kPfThreads / kCh;
+  constexpr int kRowsPerIt = kThreads / kCh;
   constexpr int kIt = kPfBN / kRowsPerIt;     // K (and V) loads per thread per tile
+  static_assert(kIt >= 1 && kPfBN % kRowsPerIt == 0, "tile staging layout");
   constexpr int kKs = D / 16;                 // MFMA k-steps over d
   constexpr int kDt = D / 32;                 // 32-row d tiles of O^T
 
@@ -102,32 +107,46 @@ __device__ __forceinline__ void prefill_tile(
   float l = 0.f;
 
   // ---- staging: K and V rows copied as 16-byte chunks ----------------------
+  // DEPTH register sets.  DEPTH 1: the loads of tile t+1 go out at the start
+  // of step t and are written to LDS after its compute.  DEPTH 2: on entry to
+  // step t the loads of tiles t+1 and t+2 are already in flight (one per set);
+  // after the compute, tile t+1 is written to LDS and the loads of tile t+3 go
+  // out into the set just freed, so every load has two steps to arrive.
   const int ld_ch = tid % kCh;
   const int ld_row = tid / kCh;
-  u32x4 kreg[kIt], vreg[kIt];
-  auto load_tile = [&](int k0) {
+  struct Stage {
+    u32x4 k[kIt], v[kIt];
+  };
+  Stage st0, st1;
+  auto load_tile = [&](Stage& sg, int k0) {
 #pragma unroll
     for (int it = 0; it < kIt; ++it) {
       const int j = k0 + it * kRowsPerIt + ld_row;
       u32x4 z = {0, 0, 0, 0};
-      kreg[it] = j < nk ? load16(kv.krow(j) + ld_ch * 8) : z;
-      vreg[it] = j < nk ? load16(kv.vrow(j) + ld_ch * 8) : z;
+      sg.k[it] = j < nk ? load16(kv.krow(j) + ld_ch * 8) : z;
+      sg.v[it] = j < nk ? load16(kv.vrow(j) + ld_ch * 8) : z;
     }
   };
-  auto store_tile = [&](int buf) {
+  auto store_tile = [&](const Stage& sg, int buf) {
     bf16_t* kl = lds + buf * L::kElemsBuf;
     bf16_t* vl = kl + L::kElemsK;
 #pragma unroll
     for (int it = 0; it < kIt; ++it) {
       const int r = it * kRowsPerIt + ld_row;
-      *reinterpret_cast<u32x4*>(kl + r * L::kStrK + ld_ch * 8) = kreg[it];
-      *reinterpret_cast<u32x4*>(vl + r * L::kStrV + ld_ch * 8) = vreg[it];
+      *reinterpret_cast<u32x4*>(kl + r * L::kStrK + ld_ch * 8) = sg.k[it];
+      *reinterpret_cast<u32x4*>(vl + r * L::kStrV + ld_ch * 8) = sg.v[it];
     }
   };
 
   if (n_tiles > 0) {
-    load_tile(0);
-    store_tile(0);
+    load_tile(st0, 0);
+    if constexpr (DEPTH == 2) {
+      if (n_tiles > 1) load_tile(st1, kPfBN);
+      store_tile(st0, 0);
+      if (n_tiles > 2) load_tile(st0, 2 * kPfBN);
+    } else {
+      store_tile(st0, 0);
+    }
   }
   __syncthreads();
 
@@ -138,9 +157,11 @@ __device__ __forceinline__ void prefill_tile(
   const int g16 = lane >> 4, r16 = lane & 15;
   const int tr_off = (4 * half + (r16 >> 2)) * L::kStrV + 16 * (g16 & 1) + 4 * (r16 & 3);
 
-  for (int t = 0; t < n_tiles; ++t) {
+  // Tile t is computed from LDS buffer t % 2; with DEPTH 2 the register set
+  // holding tile t+1 is st1 for even t and st0 for odd t.
+  auto step = [&](int t, Stage& cur) {
     const int k0 = t * kPfBN;
-    if (t + 1 < n_tiles) load_tile(k0 + kPfBN);
+    if (DEPTH == 1 && t + 1 < n_tiles) load_tile(cur, k0 + kPfBN);
     const bf16_t* kl = lds + (t & 1) * L::kElemsBuf;
     const bf16_t* vl = kl + L::kElemsK;
 
@@ -222,9 +243,21 @@ __device__ __forceinline__ void prefill_tile(
         }
       }
     }
-    if (t + 1 < n_tiles) store_tile((t + 1) & 1);
+    if (t + 1 < n_tiles) store_tile(cur, (t + 1) & 1);
+    if (DEPTH == 2 && t + 3 < n_tiles) load_tile(cur, k0 + 3 * kPfBN);
     __syncthreads();
+  };
+  int t = 0;
+  for (; t + 1 < n_tiles; t += 2) {
+    if constexpr (DEPTH == 2) {
+      step(t, st1);
+      step(t + 1, st0);
+    } else {
+      step(t, st0);
+      step(t + 1, st0);
+    }
   }
+  if (t < n_tiles) step(t, DEPTH == 2 ? st1 : st0);
 
   // ---- epilogue: normalise, store bf16 rows and the log-sum-exp -------------
   const float lt = l + wave_xor(l, 32);
