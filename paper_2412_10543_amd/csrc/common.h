@@ -11,6 +11,7 @@ typedef uint16_t bf16_t;  // raw bf16 storage
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
@@ -99,6 +100,30 @@ __device__ __forceinline__ i16x4 lds_read_tr4(const bf16_t* p) {
   typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
   return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p));
 }
+// Direct global -> LDS copy of 16 bytes per lane (global_load_lds_dwordx4):
+// lane l's 16 bytes land at lds_dst + 16*l, lds_dst being the same for the
+// whole wave.  Counts as one vector-memory operation (vmcnt) and completes
+// asynchronously; the caller waits on vmcnt and synchronises before reading
+// the data.  Issued from inline assembly, so the compiler does not track the
+// LDS write (it would otherwise make every later LDS read wait for all such
+// copies whenever it cannot tell the destinations apart); M0, which holds
+// the LDS address, is saved and restored around it.
+__device__ __forceinline__ void dma16(const void* src, bf16_t* lds_dst) {
+  typedef __attribute__((address_space(3))) char lds_char;
+  const uint32_t base =
+      __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lds_char*)lds_dst);
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %2\n\t"
+      "s_nop 0\n\t"                       // one wait state after writing M0
+      "global_load_lds_dwordx4 %1, off\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(src), "s"(base)
+      : "memory");
+}
+
 __device__ __forceinline__ bf16x8 join_bf16x8(i16x4 lo, i16x4 hi) {
   typedef short i16x8 __attribute__((ext_vector_type(8)));
   i16x8 v = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
@@ -132,14 +157,15 @@ __host__ __device__ constexpr int pf_rows_per_tile(int group, int waves) {
   return kPfRowsPerWave * (waves / pf_heads_per_wg(group));
 }
 
-// K and V tiles are both row-major [key][d] in LDS.  K rows are padded by
-// 16 B (consecutive rows land 4 banks apart: the 16-byte A-operand reads of 8
-// lanes hit distinct banks); V rows by 32 B (the transposing reads of 16
-// lanes cover 4 rows x 32 B, which then map to distinct banks).
+// K and V tiles are both row-major [key][d] in LDS (64 banks of 4 bytes).
+// K rows are padded by 16 B: consecutive rows start one 16-byte bank group
+// apart, so the 16 lanes of an A-operand read (16 rows) hit distinct groups.
+// V rows by 64 B: the 32 lanes of a transposing read cover 4 rows x 64 B,
+// and rows four bank groups apart make those 16 groups distinct.
 template <int D>
 struct PfLds {
   static constexpr int kStrK = D + 8;
-  static constexpr int kStrV = D + 16;
+  static constexpr int kStrV = D + 32;
   static constexpr int kElemsK = kPfBN * kStrK;
   static constexpr int kElemsV = kPfBN * kStrV;
   static constexpr int kElemsBuf = kElemsK + kElemsV;

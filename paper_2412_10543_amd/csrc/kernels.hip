@@ -81,11 +81,12 @@ __global__ __launch_bounds__(64 * kPfWavesDense, 2) void prefill_varlen_kernel(
     const bf16_t* __restrict__ v, bf16_t* __restrict__ o, float* __restrict__ lse,
     const int32_t* __restrict__ cu_q, const int32_t* __restrict__ cu_k, int num_seqs,
     int hq, int hkv, int n_qt, float scale, int causal) {
-  // three K/V stages (separate arrays: the compiler then knows a DMA write to
+  // four K/V stages (separate arrays: the compiler then knows a DMA write to
   // one stage never aliases an LDS read of another)
   __shared__ __attribute__((aligned(16))) bf16_t st0[SwizzledLayout<D>::kElemsTile];
   __shared__ __attribute__((aligned(16))) bf16_t st1[SwizzledLayout<D>::kElemsTile];
   __shared__ __attribute__((aligned(16))) bf16_t st2[SwizzledLayout<D>::kElemsTile];
+  __shared__ __attribute__((aligned(16))) bf16_t st3[SwizzledLayout<D>::kElemsTile];
   const int group = hq / hkv;
   const TileCoord tc =
       prefill_coord<kPfWavesDense>(blockIdx.x, num_seqs * hkv, hkv, group, n_qt);
@@ -97,10 +98,10 @@ __global__ __launch_bounds__(64 * kPfWavesDense, 2) void prefill_varlen_kernel(
   const size_t qs = (size_t)hq * D;
   DenseKV kv{k + ((size_t)kb * hkv + tc.kvh) * D, v + ((size_t)kb * hkv + tc.kvh) * D,
              (size_t)hkv * D};
-  prefill_tile_dma<D, kPfWavesDense>(
+  prefill_tile_pipe<D, kPfWavesDense>(
       q + ((size_t)qb * hq + tc.head) * D, qs, o + ((size_t)qb * hq + tc.head) * D, qs,
       lse ? lse + (size_t)tc.head * tq + qb : nullptr, kv, nq, nk, tc.q0, tc.rows, tc.r0, scale,
-      causal, st0, st1, st2);
+      causal, st0, st1, st2, st3);
 }
 
 // ---------------------------------------------------------------------------

@@ -65,7 +65,7 @@ struct PagedKV {
 //   v_off(r, dt):  transposing read of the V slice starting at row r (r a
 //                  multiple of 8), d tile dt (see pf_tile)
 // ---------------------------------------------------------------------------
-// Padded rows (register staging): K rows +16 B, V rows +32 B (see PfLds).
+// Padded rows (register staging): K rows +16 B, V rows +64 B (see PfLds).
 template <int D>
 struct PaddedLayout {
   using L = PfLds<D>;
@@ -85,37 +85,47 @@ struct PaddedLayout {
 };
 
 // Unpadded rows with XOR-swizzled 16-byte chunks (DMA staging, whose lane
-// order fixes 64 consecutive chunks per wave instruction).  K chunk c of row
-// r sits at c ^ (r & 7): the eight rows an A-operand read group touches land
-// in distinct banks.  V chunk c of row r sits at c ^ 2*(r & 3): the four rows
-// x two chunks a transposing-read group touches land in distinct banks.
-// Written out per lane, K offsets depend on the lane only through
-// (ks & 3) ^ ((l32 >> 1) & 3) and V offsets through (dt & 1) ^ (r16 >> 3).
+// order fixes 64 consecutive chunks per wave instruction).  gfx950's LDS has
+// 64 four-byte banks; a 16-byte read is serviced 16 lanes at a time and an
+// 8-byte (transposing) read 32 lanes at a time, and each such group must
+// touch every bank once.  K chunk c of row r sits at c ^ kx(r): the 16 rows
+// of an A-operand read group then land in 16 distinct 16-byte bank groups.  V
+// chunk c of row r sits at c ^ vx(r): the 4 rows x 64 bytes of a transposing
+// read group land in 16 distinct bank groups.  (Rows are 256 bytes at
+// D = 128, so every row starts at bank 0; at D = 64 two rows share a bank
+// cycle, hence the r/2.)  The lane-dependent part of each read offset is one
+// register per K step (k_lane[ks]) and per V d-tile (v_lane[dt]).
 template <int D>
 struct SwizzledLayout {
   static constexpr int kElemsTile = 2 * kPfBN * D;   // K then V
-  int k_lane[4], v_lane[2];
+  int k_lane[D / 16], v_lane[D / 32];
+  __device__ __forceinline__ static int kx(int r) {
+    return D >= 128 ? (r & 15) : ((r >> 1) & 7);
+  }
+  __device__ __forceinline__ static int vx(int r) {
+    return D >= 128 ? 4 * (r & 3) : 4 * ((r >> 1) & 1);
+  }
   __device__ __forceinline__ SwizzledLayout() {
     const int lane = threadIdx.x & 63;
     const int l32 = lane & 31, half = lane >> 5, g16 = lane >> 4, r16 = lane & 15;
-    const int x2 = (l32 >> 1) & 3, hh = half ^ (l32 & 1);
+    // K read: row 32*mt + l32, logical chunk 2*ks + half (kx ignores 32*mt)
 #pragma unroll
-    for (int b = 0; b < 4; ++b) k_lane[b] = l32 * D + 16 * (b ^ x2) + 8 * hh;
-    const int y = r16 >> 2;                                  // row & 3 of the source row
-    const int cl = (2 * (g16 & 1) + ((r16 & 3) >> 1)) ^ (2 * (y & 1));
+    for (int ks = 0; ks < D / 16; ++ks) k_lane[ks] = l32 * D + 8 * ((2 * ks + half) ^ kx(l32));
+    // V read: row r + 4*half + r16/4 (r a multiple of 8, which vx ignores),
+    // bytes 64*dt + 32*(g16 % 2) + 8*(r16 % 4) of the row
+    const int row = 4 * half + (r16 >> 2);
 #pragma unroll
-    for (int e = 0; e < 2; ++e)
-      v_lane[e] = (4 * half + y) * D + 32 * (e ^ (y >> 1)) + 8 * cl + 4 * (r16 & 1);
+    for (int dt = 0; dt < D / 32; ++dt) {
+      const int byte = 64 * dt + 32 * (g16 & 1) + 8 * (r16 & 3);
+      v_lane[dt] = row * D + 8 * ((byte >> 4) ^ vx(row)) + ((byte & 15) >> 1);
+    }
   }
-  __device__ __forceinline__ int k_off(int mt, int ks) const {
-    return 32 * mt * D + 64 * (ks >> 2) + k_lane[ks & 3];
-  }
-  __device__ __forceinline__ int v_off(int r, int dt) const {
-    return r * D + 64 * (dt >> 1) + v_lane[dt & 1];
-  }
-  // physical chunk of logical chunk c in row r (the DMA side)
-  __device__ __forceinline__ static int k_phys(int r, int c) { return c ^ (r & 7); }
-  __device__ __forceinline__ static int v_phys(int r, int c) { return c ^ (2 * (r & 3)); }
+  __device__ __forceinline__ int k_off(int mt, int ks) const { return 32 * mt * D + k_lane[ks]; }
+  __device__ __forceinline__ int v_off(int r, int dt) const { return r * D + v_lane[dt]; }
+  // logical chunk held by physical chunk c of row r (the DMA side; XOR is its
+  // own inverse)
+  __device__ __forceinline__ static int k_phys(int r, int c) { return c ^ kx(r); }
+  __device__ __forceinline__ static int v_phys(int r, int c) { return c ^ vx(r); }
 };
 
 // ---------------------------------------------------------------------------
@@ -344,38 +354,286 @@ __device__ __forceinline__ void prefill_tile_regs(
 }
 
 // ---------------------------------------------------------------------------
-// DMA-staged tile loop for dense K/V (three LDS stages s0/s1/s2 of
-// SwizzledLayout).  The loads of tile t+2 go out at the start of step t into
-// the stage tile t-1 used; at the end of step t the wave waits until its
-// loads of tile t+1 have landed, then the workgroup barrier makes every
-// wave's share visible.  Rows past the sequence end are loaded from its last
-// row (finite data; those keys are masked).
+// Software-pipelined tile loop for dense K/V (DMA staging into four LDS
+// stages of SwizzledLayout).
+//
+// The unit of work is a block of 32 keys (half a tile).  For block b a wave
+// does QK(b) (S^T of 32 keys x its 32 rows: D/16 MFMAs), SM(b) (exp2 of the
+// scores, bf16 packing, row sums: vector ALU) and PV(b) (D/16 MFMAs).  Slot b
+// issues QK(b+1) and PV(b-1) on the matrix cores while SM(b) runs on the
+// vector ALU, so within each wave the two units work side by side instead of
+// taking turns (the two waves sharing a SIMD are held in step by the
+// per-tile barrier, so they could not fill each other's gaps).
+//
+// Each block is one online-softmax step.  Its weights are formed against the
+// current exponent reference m (the running maximum as last moved) and kept
+// if every lane's sum of its 16 weights is at most kPfSumBound, which bounds
+// each weight; otherwise -- the first block of a row (m = -inf makes the sum
+// inf or NaN), or scores far above m -- the block is redone exactly: m moves
+// to the new row maximum, output and sum are rescaled, weights recomputed.
+//
+// Stages: tile t lives in stage t % 4.  Slot 2t reads K of tile t (keys
+// 32..63) and V of tile t-1 (keys 32..63); slot 2t+1 reads K of tile t+1
+// (keys 0..31) and V of tile t (keys 0..31).  Between the two slots each wave
+// waits for its share of tile t+1, the workgroup barrier publishes it and
+// retires tile t-1, and the DMA of tile t+3 goes out into tile t-1's stage.
 // ---------------------------------------------------------------------------
+constexpr float kPfSumBound = 65536.f;   // 2^16: weights stay far inside fp32/bf16 range
+
+// Max of x over the two 32-lane halves (lanes l and l ^ 32 hold one row).
+__device__ __forceinline__ float max_halves(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x),
+                                                  false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
+// Workgroup barrier that no LDS access is moved across, by the compiler's IR
+// passes or by its instruction scheduler.
+__device__ __forceinline__ void pf_barrier() {
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_sched_barrier(0);
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_sched_barrier(0);
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
+// S^T of the 32 keys [32*H, 32*H + 32) of a staged tile against this wave's
+// rows; element j of the result is key 8*(j/4) + 4*half + j%4 of the block.
+template <int D, int H>
+__device__ __forceinline__ f32x16 pf_qk(const PfState<D>& st, const SwizzledLayout<D>& lay,
+                                        const bf16_t* __restrict__ kst) {
+  f32x16 s = {};
+#pragma unroll
+  for (int ks = 0; ks < D / 16; ++ks) {
+    const bf16x8 a = *reinterpret_cast<const bf16x8*>(kst + lay.k_off(H, ks));
+    s = mfma32(a, st.qf[ks], s);
+  }
+  return s;
+}
+
+// O^T += V^T P^T over the keys [32*H, 32*H + 32) of a staged tile (stage =
+// the tile's K then V); p[s2] is
+// the B operand of keys 16*s2 .. +16 of the block (see pf_tile for the order).
+template <int D, int H>
+__device__ __forceinline__ void pf_pv(PfState<D>& st, const SwizzledLayout<D>& lay,
+                                      const bf16_t* __restrict__ stage, const bf16x8 (&p)[2]) {
+  const bf16_t* vst = stage + kPfBN * D;   // V follows K in a stage
+#pragma unroll
+  for (int s2 = 0; s2 < 2; ++s2) {
+    const int rw = 32 * H + 16 * s2;
+#pragma unroll
+    for (int dt = 0; dt < D / 32; ++dt) {
+      const bf16x8 a = join_bf16x8(lds_read_tr4(vst + lay.v_off(rw, dt)),
+                                   lds_read_tr4(vst + lay.v_off(rw + 8, dt)));
+      st.oacc[dt] = mfma32(a, p[s2], st.oacc[dt]);
+    }
+  }
+}
+
+// Weights 2^(s*c + nm) of one block, packed to bf16 in pf_pv's operand order;
+// returns this lane's fp32 sum of the weights.
+__device__ __forceinline__ float pf_weights(const f32x16& s, float c, float nm,
+                                            bf16x8 (&p)[2]) {
+  float w[16];
+#pragma unroll
+  for (int j = 0; j < 16; ++j) w[j] = fast_exp2(fmaf(s[j], c, nm));
+  float sum = 0.f;
+#pragma unroll
+  for (int j = 0; j < 16; ++j) sum += w[j];
+#pragma unroll
+  for (int s2 = 0; s2 < 2; ++s2) {
+    const int b = 8 * s2;
+    p[s2] = to_bf16x8(w[b], w[b + 1], w[b + 2], w[b + 3], w[b + 4], w[b + 5], w[b + 6],
+                      w[b + 7]);
+  }
+  return sum;
+}
+
+// Keys past lim (this lane's last visible key) of the block starting at key0.
+__device__ __forceinline__ void pf_mask(f32x16& s, int key0, int lim) {
+  const int half = (threadIdx.x & 63) >> 5;
+#pragma unroll
+  for (int j = 0; j < 16; ++j) {
+    const int key = key0 + 8 * (j >> 2) + 4 * half + (j & 3);
+    if (key > lim) s[j] = -INFINITY;
+  }
+}
+
+// The exact path: move m to the row maximum, rescale, recompute the weights.
+template <int D>
+__device__ __forceinline__ float pf_reref(PfState<D>& st, const f32x16& s, float c,
+                                          bf16x8 (&p)[2]) {
+  // A side effect keeps the compiler from executing this rare path
+  // unconditionally and selecting its results.
+  asm volatile("");
+  float tmax = s[0];
+#pragma unroll
+  for (int j = 1; j < 16; ++j) tmax = fmaxf(tmax, s[j]);
+  tmax = max_halves(tmax);
+  const float m_new = fmaxf(st.m_used, tmax);
+  const float alpha = (st.m_used == -INFINITY) ? 0.f : fast_exp2((st.m_used - m_new) * c);
+  st.l *= alpha;
+#pragma unroll
+  for (int dt = 0; dt < D / 32; ++dt)
+#pragma unroll
+    for (int j = 0; j < 16; ++j) st.oacc[dt][j] *= alpha;
+  st.m_used = m_new;
+  return pf_weights(s, c, (m_new == -INFINITY) ? 0.f : -m_new * c, p);
+}
+
+// Per-wave constants of the pipelined loop.
+struct PfPipeCtx {
+  float c;     // scale * log2(e)
+  int nbw;     // 32-key blocks this wave computes
+  int lim;     // last key this lane's row sees
+  int mlim;    // blocks ending past this key need masking
+};
+
+// A full slot in an explicit instruction order: D/16 steps, each with the
+// LDS operand reads of the step two ahead, one QK(b+1) MFMA, vector work of
+// SM(b), one PV(b-1) MFMA.  The vector work is itself pipelined over the
+// steps -- step i forms the exponent arguments of step i+1's scores, the
+// exponentials of step i's and packs and sums step i-1's -- so no vector
+// instruction waits on the one before it (a wave issues in order, and such
+// a wait would hold back its next MFMA too).  A scheduling barrier after each
+// step and empty asm statements on the values each step produces keep the
+// compiler from regrouping the work (left alone it clusters the MFMAs, and
+// the two units take turns).
+template <int D, int HK, int HV>
+__device__ __forceinline__ float pf_full_slot(PfState<D>& st, const SwizzledLayout<D>& lay,
+                                              const bf16_t* __restrict__ kst,
+                                              const bf16_t* __restrict__ vstage,
+                                              const f32x16& s_cur, f32x16& s_next,
+                                              bf16x8 (&p_cur)[2], const bf16x8 (&p_prev)[2],
+                                              float c, float nm) {
+  const bf16_t* vst = vstage + kPfBN * D;   // V follows K in a stage
+  constexpr int kSteps = D / 16;          // QK MFMAs = PV MFMAs = steps
+  constexpr int kDt = D / 32;
+  constexpr int kPer = 16 / kSteps;       // scores (per lane) per step
+  static_assert(kPer % 2 == 0 && 16 % kSteps == 0, "step shape");
+  bf16x8 ka[kSteps], va[kSteps];
+  auto load = [&](int i) {
+    ka[i] = *reinterpret_cast<const bf16x8*>(kst + lay.k_off(HK, i));
+    const int rw = 32 * HV + 16 * (i / kDt), dt = i % kDt;
+    va[i] = join_bf16x8(lds_read_tr4(vst + lay.v_off(rw, dt)),
+                        lds_read_tr4(vst + lay.v_off(rw + 8, dt)));
+  };
+  float x[16], w[16];
+  bf16x2 pr[8];
+  float sum = 0.f;
+  auto arg = [&](int i) {          // exponent arguments of step i's scores
+#pragma unroll
+    for (int u = 0; u < kPer; ++u) {
+      x[i * kPer + u] = fmaf(s_cur[i * kPer + u], c, nm);
+      asm volatile("" : "+v"(x[i * kPer + u]));
+    }
+  };
+  auto expo = [&](int i) {
+#pragma unroll
+    for (int u = 0; u < kPer; ++u) {
+      w[i * kPer + u] = fast_exp2(x[i * kPer + u]);
+      asm volatile("" : "+v"(w[i * kPer + u]));
+    }
+  };
+  auto pack = [&](int i) {         // bf16 pairs and the row sum
+#pragma unroll
+    for (int u = 0; u < kPer; u += 2) {
+      const int e = i * kPer + u;
+      f32x2 pw = {w[e], w[e + 1]};
+      pr[e / 2] = __builtin_convertvector(pw, bf16x2);
+      asm volatile("" : "+v"(pr[e / 2]));
+      sum += w[e];
+      sum += w[e + 1];
+    }
+    asm volatile("" : "+v"(sum));
+  };
+  load(0);
+  if (kSteps > 1) load(1);
+  arg(0);
+  f32x16 acc = {};
+#pragma unroll
+  for (int i = 0; i < kSteps; ++i) {
+    if (i + 2 < kSteps) load(i + 2);
+    __builtin_amdgcn_sched_barrier(0);
+    acc = mfma32(ka[i], st.qf[i], acc);
+    if (i + 1 < kSteps) arg(i + 1);
+    expo(i);
+    if (i >= 1) pack(i - 1);
+    st.oacc[i % kDt] = mfma32(va[i], p_prev[i / kDt], st.oacc[i % kDt]);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  pack(kSteps - 1);
+  s_next = acc;
+#pragma unroll
+  for (int s2 = 0; s2 < 2; ++s2)
+    p_cur[s2] = __builtin_shufflevector(
+        __builtin_shufflevector(pr[4 * s2], pr[4 * s2 + 1], 0, 1, 2, 3),
+        __builtin_shufflevector(pr[4 * s2 + 2], pr[4 * s2 + 3], 0, 1, 2, 3), 0, 1, 2, 3, 4,
+        5, 6, 7);
+  return sum;
+}
+
+// Slot b: SM(b) on s_cur -> p_cur; QK(b+1) -> s_next from keys 32*HK.. of
+// the stage kst; PV(b-1) with p_prev over keys 32*HV.. of the stage vst.
+template <int D, int HK, int HV>
+__device__ __forceinline__ void pf_slot(PfState<D>& st, const SwizzledLayout<D>& lay,
+                                        const PfPipeCtx& cx, int b, f32x16& s_cur,
+                                        f32x16& s_next, bf16x8 (&p_cur)[2],
+                                        const bf16x8 (&p_prev)[2], const bf16_t* kst,
+                                        const bf16_t* vst) {
+  const bool do_sm = b < cx.nbw;
+  const bool do_qk = b + 1 < cx.nbw;
+  const bool do_pv = b >= 1 && b <= cx.nbw;
+  if (do_sm && 32 * b + 31 > cx.mlim) pf_mask(s_cur, 32 * b, cx.lim);
+  if (do_sm && do_qk && do_pv) {
+    float sum = pf_full_slot<D, HK, HV>(st, lay, kst, vst, s_cur, s_next, p_cur, p_prev, cx.c,
+                                        -st.m_used * cx.c);
+    if (__builtin_expect(wave_any(!(sum <= kPfSumBound)), 0))
+      sum = pf_reref(st, s_cur, cx.c, p_cur);
+    st.l += sum;
+    return;
+  }
+  if (do_qk) s_next = pf_qk<D, HK>(st, lay, kst);
+  if (do_pv) pf_pv<D, HV>(st, lay, vst, p_prev);
+  if (do_sm) {
+    float sum = pf_weights(s_cur, cx.c, -st.m_used * cx.c, p_cur);
+    if (__builtin_expect(wave_any(!(sum <= kPfSumBound)), 0))
+      sum = pf_reref(st, s_cur, cx.c, p_cur);
+    st.l += sum;
+  }
+}
+
 template <int D, int W>
-__device__ __forceinline__ void prefill_tile_dma(
+__device__ __forceinline__ void prefill_tile_pipe(
     const bf16_t* __restrict__ q, size_t q_stride, bf16_t* __restrict__ o, size_t o_stride,
     float* __restrict__ lse, const DenseKV& kv, int nq, int nk, int q0, int wg_rows, int r0,
     float scale, int causal, bf16_t* __restrict__ s0, bf16_t* __restrict__ s1,
-    bf16_t* __restrict__ s2) {
+    bf16_t* __restrict__ s2, bf16_t* __restrict__ s3) {
   using Lay = SwizzledLayout<D>;
   constexpr int kCh = D / 8;                     // 16-byte chunks per row
   constexpr int kInstr = kPfBN * kCh / (64 * W);  // K (and V) DMA instructions per wave per tile
   static_assert(kInstr >= 1 && (kPfBN * kCh) % (64 * W) == 0, "tile staging layout");
   constexpr int kLoadsPerTile = 2 * kInstr;      // vmcnt events per wave per tile
+  static_assert(2 * kLoadsPerTile < 64, "vmcnt range");
   const int tid = threadIdx.x;
   const int wave = tid >> 6, lane = tid & 63;
   const PfRange rg = pf_range(nq, nk, q0, wg_rows, r0, causal);
-  const float c = scale * kLog2e;
-  const float tau = kRescaleLog2 / c;
+  const int row = r0 + (lane & 31);
+  PfPipeCtx cx;
+  cx.c = scale * kLog2e;
+  cx.nbw = (rg.kend_w + 31) >> 5;
+  cx.lim = causal ? min(nk - 1, row + rg.off) : nk - 1;
+  cx.mlim = causal ? min(nk - 1, r0 + rg.off) : nk - 1;
 
   PfState<D> st;
-  pf_init(st, q, q_stride, r0 + (lane & 31), nq);
+  pf_init(st, q, q_stride, row, nq);
 
   // Instruction i of this wave writes physical chunks [64*gi, 64*gi + 64) of
   // the tile, gi = wave*kInstr + i; lane l's chunk P = 64*gi + l is physical
   // chunk P % kCh of row P / kCh, which holds logical chunk phys ^ swizzle.
+  // Rows past the sequence end are loaded from its last row (finite data;
+  // those keys are masked).
   auto issue_tile = [&](bf16_t* stage, int k0) {
-    typedef __attribute__((address_space(3))) void lds_void;
 #pragma unroll
     for (int i = 0; i < kInstr; ++i) {
       const int gi = wave * kInstr + i;
@@ -384,17 +642,18 @@ __device__ __forceinline__ void prefill_tile_dma(
       const int j = min(k0 + r, nk - 1);
       const bf16_t* ksrc = kv.krow(j) + Lay::k_phys(r, phys) * 8;
       const bf16_t* vsrc = kv.vrow(j) + Lay::v_phys(r, phys) * 8;
-      __builtin_amdgcn_global_load_lds(ksrc, (lds_void*)(stage + 64 * gi * 8), 16, 0, 0);
-      __builtin_amdgcn_global_load_lds(vsrc, (lds_void*)(stage + kPfBN * D + 64 * gi * 8), 16,
-                                       0, 0);
+      dma16(ksrc, stage + 64 * gi * 8);
+      dma16(vsrc, stage + kPfBN * D + 64 * gi * 8);
     }
   };
-  // vmcnt(n): wait until at most n vector-memory operations of this wave are
-  // outstanding (gfx9 encoding: vmcnt in bits 3:0 and 15:14; expcnt and
-  // lgkmcnt left at their maximum, i.e. not waited on).
-  auto wait_vm = [](bool keep_one_tile) {
-    if (keep_one_tile)
-      __builtin_amdgcn_s_waitcnt(0x0F70 | (kLoadsPerTile & 15) | ((kLoadsPerTile >> 4) << 14));
+  // Wait until at most `tiles` tiles of this wave's DMA are in flight
+  // (vmcnt in bits 3:0 and 15:14; expcnt and lgkmcnt left at their maximum).
+  auto wait_tiles = [](int tiles) {
+    constexpr int k1 = kLoadsPerTile, k2 = 2 * kLoadsPerTile;
+    if (tiles >= 2)
+      __builtin_amdgcn_s_waitcnt(0x0F70 | (k2 & 15) | ((k2 >> 4) << 14));
+    else if (tiles == 1)
+      __builtin_amdgcn_s_waitcnt(0x0F70 | (k1 & 15) | ((k1 >> 4) << 14));
     else
       __builtin_amdgcn_s_waitcnt(0x0F70);
   };
@@ -402,27 +661,42 @@ __device__ __forceinline__ void prefill_tile_dma(
   const Lay lay;
   const int nt = rg.n_tiles;
   if (nt > 0) issue_tile(s0, 0);
+  // Take delivery of Q here (with tile 0, both needed first): the compiler
+  // does not see the DMA, so a first use of Q inside the loop would make it
+  // wait there for every copy in flight, on every iteration.
+#pragma unroll
+  for (int ks = 0; ks < D / 16; ++ks) asm volatile("" : "+v"(st.qf[ks]));
   if (nt > 1) issue_tile(s1, kPfBN);
-  wait_vm(nt > 1);
-  __builtin_amdgcn_s_barrier();
+  if (nt > 2) issue_tile(s2, 2 * kPfBN);
+  wait_tiles(min(nt, 3) - 1);
+  pf_barrier();
 
-  auto step = [&](int t, const bf16_t* cur, bf16_t* ahead) {
-    const int k0 = t * kPfBN;
-    if (t + 2 < nt) issue_tile(ahead, k0 + 2 * kPfBN);
-    if (k0 < rg.kend_w)
-      pf_tile<D>(st, lay, cur, cur + kPfBN * D, k0, r0, nk, rg.off, causal, c, tau);
-    wait_vm(t + 2 < nt);
-    __builtin_amdgcn_s_barrier();
-  };
-  int t = 0;
-  for (; t + 2 < nt; t += 3) {
-    step(t, s0, s2);
-    step(t + 1, s1, s0);
-    step(t + 2, s2, s1);
+  f32x16 sE = {}, sO = {};
+  bf16x8 pE[2] = {}, pO[2] = {};
+  if (cx.nbw > 0) sE = pf_qk<D, 0>(st, lay, s0);
+
+  // Stage roles rotate by one each tile (tile t is in stage t % 4): prev
+  // holds tile t-1 and, once the barrier has retired it, receives tile t+3.
+  bf16_t* prev = s3;
+  bf16_t* cur = s0;
+  bf16_t* next = s1;
+  bf16_t* after = s2;
+  for (int t = 0; t < nt; ++t) {
+    pf_slot<D, 1, 1>(st, lay, cx, 2 * t, sE, sO, pE, pO, cur, prev);
+    wait_tiles(t + 2 < nt ? 1 : 0);
+    pf_barrier();
+    if (t + 3 < nt) issue_tile(prev, (t + 3) * kPfBN);
+    pf_slot<D, 0, 0>(st, lay, cx, 2 * t + 1, sO, sE, pO, pE, next, cur);
+    bf16_t* const retired = prev;
+    prev = cur;
+    cur = next;
+    next = after;
+    after = retired;
   }
-  if (t < nt) step(t, s0, s2);
-  if (t + 1 < nt) step(t + 1, s1, s0);
-  pf_store(st, o, o_stride, lse, r0 + (lane & 31), nq, scale);
+  // PV of the last block, when this wave computes the whole last tile (its
+  // stage is now prev).
+  if (nt > 0 && cx.nbw == 2 * nt) pf_pv<D, 1>(st, lay, prev, pO);
+  pf_store(st, o, o_stride, lse, row, nq, scale);
 }
 
 }  // namespace rag
