@@ -83,10 +83,10 @@ __global__ __launch_bounds__(64 * kPfWavesDense, 2) void prefill_varlen_kernel(
     int hq, int hkv, int n_qt, float scale, int causal) {
   // four K/V stages (separate arrays: the compiler then knows a DMA write to
   // one stage never aliases an LDS read of another)
-  __shared__ __attribute__((aligned(16))) bf16_t st0[SwizzledLayout<D>::kElemsTile];
-  __shared__ __attribute__((aligned(16))) bf16_t st1[SwizzledLayout<D>::kElemsTile];
-  __shared__ __attribute__((aligned(16))) bf16_t st2[SwizzledLayout<D>::kElemsTile];
-  __shared__ __attribute__((aligned(16))) bf16_t st3[SwizzledLayout<D>::kElemsTile];
+  __shared__ __attribute__((aligned(16))) bf16_t st0[ChunkLayout<D>::kElemsTile];
+  __shared__ __attribute__((aligned(16))) bf16_t st1[ChunkLayout<D>::kElemsTile];
+  __shared__ __attribute__((aligned(16))) bf16_t st2[ChunkLayout<D>::kElemsTile];
+  __shared__ __attribute__((aligned(16))) bf16_t st3[ChunkLayout<D>::kElemsTile];
   const int group = hq / hkv;
   const TileCoord tc =
       prefill_coord<kPfWavesDense>(blockIdx.x, num_seqs * hkv, hkv, group, n_qt);
@@ -127,6 +127,31 @@ struct PagedKernelArgs {
   float scale;
 };
 
+// One piece of a decode row: pages [p_begin, p_end) of (row s, kv head kvh),
+// split sp of n_sp.
+template <int D>
+__device__ __forceinline__ void decode_piece(const PagedKernelArgs& a, int group,
+                                             size_t block_stride, int s, int kvh, int kv_len,
+                                             int p_begin, int p_end, int sp, int n_sp,
+                                             bf16_t* lds) {
+  const int row = a.cu_q ? a.cu_q[s] : s;
+  const int h0 = kvh * group;
+  DecodeOut out;
+  out.o = a.o + ((size_t)row * a.hq + h0) * D;
+  out.part_o = a.part_o ? a.part_o + (size_t)s * a.hq * a.num_splits * D +
+                              (size_t)h0 * a.num_splits * D
+                        : nullptr;
+  out.part_lse = a.part_lse ? a.part_lse + ((size_t)s * a.hq + h0) * a.num_splits : nullptr;
+  out.arrival = a.arrivals ? a.arrivals + (size_t)s * a.hkv + kvh : nullptr;
+  out.sp = sp;
+  out.n_sp = n_sp;
+  out.num_splits = a.num_splits;
+  decode_unit<D, kDecPages>(a.q + ((size_t)row * a.hq + h0) * D, a.kc + (size_t)kvh * 16 * D,
+                            a.vc + (size_t)kvh * 16 * D, block_stride,
+                            a.tables + (size_t)s * a.max_blocks, kv_len, group, p_begin, p_end,
+                            a.scale, out, lds);
+}
+
 template <int D, bool kMixed>
 __global__ __launch_bounds__(256, 2) void paged_kernel(PagedKernelArgs a) {
   constexpr int kLdsBytes =
@@ -161,28 +186,13 @@ __global__ __launch_bounds__(256, 2) void paged_kernel(PagedKernelArgs a) {
   const int sp = (int)(block / pairs);
   const int pr = (int)(block % pairs);
   const int s = pr / a.hkv, kvh = pr % a.hkv;
-  const int kv_len = a.kv_lens[s];
+  const int kv_len = min(a.kv_lens[s], a.max_blocks * 16);
   const int n_pages = (kv_len + 15) >> 4;
   const int n_sp = (n_pages + a.pps - 1) / a.pps;
   if (sp >= n_sp && sp > 0) return;
   const int p_begin = sp * a.pps;
   const int p_end = min(n_pages, p_begin + a.pps);
-  const int row = a.cu_q ? a.cu_q[s] : s;
-  const int h0 = kvh * group;
-  DecodeOut out;
-  out.o = a.o + ((size_t)row * a.hq + h0) * D;
-  out.part_o = a.part_o ? a.part_o + (size_t)s * a.hq * a.num_splits * D +
-                              (size_t)h0 * a.num_splits * D
-                        : nullptr;
-  out.part_lse = a.part_lse ? a.part_lse + ((size_t)s * a.hq + h0) * a.num_splits : nullptr;
-  out.arrival = a.arrivals ? a.arrivals + (size_t)s * a.hkv + kvh : nullptr;
-  out.sp = sp;
-  out.n_sp = n_sp;
-  out.num_splits = a.num_splits;
-  decode_unit<D, kDecPages>(a.q + ((size_t)row * a.hq + h0) * D, a.kc + (size_t)kvh * 16 * D,
-                            a.vc + (size_t)kvh * 16 * D, block_stride,
-                            a.tables + (size_t)s * a.max_blocks, kv_len, group, p_begin, p_end,
-                            a.scale, out, lds);
+  decode_piece<D>(a, group, block_stride, s, kvh, kv_len, p_begin, p_end, sp, n_sp, lds);
 }
 
 // ---------------------------------------------------------------------------

@@ -84,48 +84,46 @@ struct PaddedLayout {
   }
 };
 
-// Unpadded rows with XOR-swizzled 16-byte chunks (DMA staging, whose lane
-// order fixes 64 consecutive chunks per wave instruction).  gfx950's LDS has
-// 64 four-byte banks; a 16-byte read is serviced 16 lanes at a time and an
-// 8-byte (transposing) read 32 lanes at a time, and each such group must
-// touch every bank once.  K chunk c of row r sits at c ^ kx(r): the 16 rows
-// of an A-operand read group then land in 16 distinct 16-byte bank groups.  V
-// chunk c of row r sits at c ^ vx(r): the 4 rows x 64 bytes of a transposing
-// read group land in 16 distinct bank groups.  (Rows are 256 bytes at
-// D = 128, so every row starts at bank 0; at D = 64 two rows share a bank
-// cycle, hence the r/2.)  The lane-dependent part of each read offset is one
-// register per K step (k_lane[ks]) and per V d-tile (v_lane[dt]).
+// DMA staging layout.  A DMA instruction writes 64 consecutive 16-byte
+// chunks (lane l at +16*l) but may gather them from anywhere, so the tile is
+// stored chunk-permuted.  gfx950's LDS has 64 four-byte banks; a 16-byte read
+// is serviced 16 lanes at a time and an 8-byte (transposing) read 32 lanes at
+// a time, and each such group must touch every bank once.
+//   K: chunk c of row r at chunk (r/16)*16*kCh + 16*c + r%16 -- the 16 rows
+//      of an A-operand read group are 16 consecutive chunks;
+//   V: the 32-d tiles (four chunks of a row) are stored one after another,
+//      each 64 rows x 64 bytes row-major -- the 4 rows x 64 bytes of a
+//      transposing read group are 256 consecutive bytes.
+// Every read is then one per-lane register (k_lane or v_lane) plus a
+// compile-time offset, and no read group hits a bank twice.
 template <int D>
-struct SwizzledLayout {
+struct ChunkLayout {
+  static constexpr int kCh = D / 8;                  // 16-byte chunks per row
   static constexpr int kElemsTile = 2 * kPfBN * D;   // K then V
-  int k_lane[D / 16], v_lane[D / 32];
-  __device__ __forceinline__ static int kx(int r) {
-    return D >= 128 ? (r & 15) : ((r >> 1) & 7);
-  }
-  __device__ __forceinline__ static int vx(int r) {
-    return D >= 128 ? 4 * (r & 3) : 4 * ((r >> 1) & 1);
-  }
-  __device__ __forceinline__ SwizzledLayout() {
+  int k_lane, v_lane;                                // in bf16 elements
+  __device__ __forceinline__ ChunkLayout() {
     const int lane = threadIdx.x & 63;
     const int l32 = lane & 31, half = lane >> 5, g16 = lane >> 4, r16 = lane & 15;
-    // K read: row 32*mt + l32, logical chunk 2*ks + half (kx ignores 32*mt)
-#pragma unroll
-    for (int ks = 0; ks < D / 16; ++ks) k_lane[ks] = l32 * D + 8 * ((2 * ks + half) ^ kx(l32));
-    // V read: row r + 4*half + r16/4 (r a multiple of 8, which vx ignores),
-    // bytes 64*dt + 32*(g16 % 2) + 8*(r16 % 4) of the row
-    const int row = 4 * half + (r16 >> 2);
-#pragma unroll
-    for (int dt = 0; dt < D / 32; ++dt) {
-      const int byte = 64 * dt + 32 * (g16 & 1) + 8 * (r16 & 3);
-      v_lane[dt] = row * D + 8 * ((byte >> 4) ^ vx(row)) + ((byte & 15) >> 1);
-    }
+    // K read: row 32*mt + l32, chunk 2*ks + half
+    k_lane = (l32 >> 4) * 128 * kCh + 128 * half + 8 * (l32 & 15);
+    // V read: row slice + 4*half + r16/4, bytes 64*dt + 32*(g16 % 2) + 8*(r16 % 4)
+    v_lane = 32 * (4 * half + (r16 >> 2)) + 16 * (g16 & 1) + 4 * (r16 & 3);
   }
-  __device__ __forceinline__ int k_off(int mt, int ks) const { return 32 * mt * D + k_lane[ks]; }
-  __device__ __forceinline__ int v_off(int r, int dt) const { return r * D + v_lane[dt]; }
-  // logical chunk held by physical chunk c of row r (the DMA side; XOR is its
-  // own inverse)
-  __device__ __forceinline__ static int k_phys(int r, int c) { return c ^ kx(r); }
-  __device__ __forceinline__ static int v_phys(int r, int c) { return c ^ vx(r); }
+  __device__ __forceinline__ int k_off(int mt, int ks) const {
+    return k_lane + 256 * kCh * mt + 256 * ks;
+  }
+  __device__ __forceinline__ int v_off(int r, int dt) const {
+    return v_lane + 2048 * dt + 32 * r;
+  }
+  // (row, chunk) of the tile held by staged chunk p (the DMA side)
+  __device__ __forceinline__ static void k_src(int p, int& r, int& c) {
+    r = (p / (16 * kCh)) * 16 + (p & 15);
+    c = (p >> 4) % kCh;
+  }
+  __device__ __forceinline__ static void v_src(int p, int& r, int& c) {
+    r = (p & 255) >> 2;
+    c = 4 * (p >> 8) + (p & 3);
+  }
 };
 
 // ---------------------------------------------------------------------------
@@ -355,7 +353,7 @@ __device__ __forceinline__ void prefill_tile_regs(
 
 // ---------------------------------------------------------------------------
 // Software-pipelined tile loop for dense K/V (DMA staging into four LDS
-// stages of SwizzledLayout).
+// stages of ChunkLayout).
 //
 // The unit of work is a block of 32 keys (half a tile).  For block b a wave
 // does QK(b) (S^T of 32 keys x its 32 rows: D/16 MFMAs), SM(b) (exp2 of the
@@ -400,7 +398,7 @@ __device__ __forceinline__ void pf_barrier() {
 // S^T of the 32 keys [32*H, 32*H + 32) of a staged tile against this wave's
 // rows; element j of the result is key 8*(j/4) + 4*half + j%4 of the block.
 template <int D, int H>
-__device__ __forceinline__ f32x16 pf_qk(const PfState<D>& st, const SwizzledLayout<D>& lay,
+__device__ __forceinline__ f32x16 pf_qk(const PfState<D>& st, const ChunkLayout<D>& lay,
                                         const bf16_t* __restrict__ kst) {
   f32x16 s = {};
 #pragma unroll
@@ -415,7 +413,7 @@ __device__ __forceinline__ f32x16 pf_qk(const PfState<D>& st, const SwizzledLayo
 // the tile's K then V); p[s2] is
 // the B operand of keys 16*s2 .. +16 of the block (see pf_tile for the order).
 template <int D, int H>
-__device__ __forceinline__ void pf_pv(PfState<D>& st, const SwizzledLayout<D>& lay,
+__device__ __forceinline__ void pf_pv(PfState<D>& st, const ChunkLayout<D>& lay,
                                       const bf16_t* __restrict__ stage, const bf16x8 (&p)[2]) {
   const bf16_t* vst = stage + kPfBN * D;   // V follows K in a stage
 #pragma unroll
@@ -500,7 +498,7 @@ struct PfPipeCtx {
 // compiler from regrouping the work (left alone it clusters the MFMAs, and
 // the two units take turns).
 template <int D, int HK, int HV>
-__device__ __forceinline__ float pf_full_slot(PfState<D>& st, const SwizzledLayout<D>& lay,
+__device__ __forceinline__ float pf_full_slot(PfState<D>& st, const ChunkLayout<D>& lay,
                                               const bf16_t* __restrict__ kst,
                                               const bf16_t* __restrict__ vstage,
                                               const f32x16& s_cur, f32x16& s_next,
@@ -576,7 +574,7 @@ __device__ __forceinline__ float pf_full_slot(PfState<D>& st, const SwizzledLayo
 // Slot b: SM(b) on s_cur -> p_cur; QK(b+1) -> s_next from keys 32*HK.. of
 // the stage kst; PV(b-1) with p_prev over keys 32*HV.. of the stage vst.
 template <int D, int HK, int HV>
-__device__ __forceinline__ void pf_slot(PfState<D>& st, const SwizzledLayout<D>& lay,
+__device__ __forceinline__ void pf_slot(PfState<D>& st, const ChunkLayout<D>& lay,
                                         const PfPipeCtx& cx, int b, f32x16& s_cur,
                                         f32x16& s_next, bf16x8 (&p_cur)[2],
                                         const bf16x8 (&p_prev)[2], const bf16_t* kst,
@@ -609,7 +607,7 @@ __device__ __forceinline__ void prefill_tile_pipe(
     float* __restrict__ lse, const DenseKV& kv, int nq, int nk, int q0, int wg_rows, int r0,
     float scale, int causal, bf16_t* __restrict__ s0, bf16_t* __restrict__ s1,
     bf16_t* __restrict__ s2, bf16_t* __restrict__ s3) {
-  using Lay = SwizzledLayout<D>;
+  using Lay = ChunkLayout<D>;
   constexpr int kCh = D / 8;                     // 16-byte chunks per row
   constexpr int kInstr = kPfBN * kCh / (64 * W);  // K (and V) DMA instructions per wave per tile
   static_assert(kInstr >= 1 && (kPfBN * kCh) % (64 * W) == 0, "tile staging layout");
@@ -628,22 +626,20 @@ __device__ __forceinline__ void prefill_tile_pipe(
   PfState<D> st;
   pf_init(st, q, q_stride, row, nq);
 
-  // Instruction i of this wave writes physical chunks [64*gi, 64*gi + 64) of
-  // the tile, gi = wave*kInstr + i; lane l's chunk P = 64*gi + l is physical
-  // chunk P % kCh of row P / kCh, which holds logical chunk phys ^ swizzle.
-  // Rows past the sequence end are loaded from its last row (finite data;
-  // those keys are masked).
+  // Instruction i of this wave writes staged chunks [64*gi, 64*gi + 64) of
+  // the K and of the V region, gi = wave*kInstr + i; lane l fetches the
+  // (row, chunk) that staged chunk 64*gi + l holds.  Rows past the sequence
+  // end are loaded from its last row (finite data; those keys are masked).
   auto issue_tile = [&](bf16_t* stage, int k0) {
 #pragma unroll
     for (int i = 0; i < kInstr; ++i) {
       const int gi = wave * kInstr + i;
       const int p = 64 * gi + lane;
-      const int r = p / kCh, phys = p % kCh;
-      const int j = min(k0 + r, nk - 1);
-      const bf16_t* ksrc = kv.krow(j) + Lay::k_phys(r, phys) * 8;
-      const bf16_t* vsrc = kv.vrow(j) + Lay::v_phys(r, phys) * 8;
-      dma16(ksrc, stage + 64 * gi * 8);
-      dma16(vsrc, stage + kPfBN * D + 64 * gi * 8);
+      int kr, kc, vr, vc;
+      Lay::k_src(p, kr, kc);
+      Lay::v_src(p, vr, vc);
+      dma16(kv.krow(min(k0 + kr, nk - 1)) + kc * 8, stage + 64 * gi * 8);
+      dma16(kv.vrow(min(k0 + vr, nk - 1)) + vc * 8, stage + kPfBN * D + 64 * gi * 8);
     }
   };
   // Wait until at most `tiles` tiles of this wave's DMA are in flight

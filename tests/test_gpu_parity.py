@@ -150,6 +150,30 @@ def test_decode_workspace_left_zeroed(orc):
     assert torch.equal(outs[0], outs[1]) and torch.equal(outs[1], outs[2])
 
 
+@pytest.mark.parametrize("n_rows,hq,hkv,splits", [(300, 32, 8, 0), (300, 32, 8, 2),
+                                                  (1100, 8, 1, 4), (60, 8, 8, 0)])
+def test_decode_uneven_rows(orc, n_rows, hq, hkv, splits):
+    """Many rows of very different length in one batch: one long row among
+    hundreds of short ones, so most splits of the short rows are empty while
+    the long row uses all of them."""
+    rng = np.random.Generator(np.random.PCG64(n_rows * 7 + splits))
+    kv = [int(x) for x in rng.integers(1, 400, size=n_rows)]
+    kv[n_rows // 3] = 5000
+    q, pool = G.decode_case(kv, hq, hkv, 128, seed=n_rows + hq)
+    o = G.gpu_paged(q, pool, hq, hkv, 128, G.scale_for(128), num_splits=splits)
+    G.assert_parity(o, G.oracle_paged(orc, q, pool, G.scale_for(128)), "balanced decode")
+
+
+def test_decode_one_row_max_pieces(orc):
+    """A single long row on one kv head is cut into close to the maximum of 64
+    splits, all merged in the kernel."""
+    q, pool = G.decode_case([20000], 4, 1, 128, seed=31)
+    from paper_2412_10543_amd import binding
+    assert binding.rag_attn_decode_num_splits(1, 1, pool.block_tables.shape[1]) >= 60
+    o = G.gpu_paged(q, pool, 4, 1, 128, G.scale_for(128))
+    G.assert_parity(o, G.oracle_paged(orc, q, pool, G.scale_for(128)), "64 pieces")
+
+
 def test_decode_splits_agree():
     q, pool = G.decode_case([5000, 3000], 32, 8, 128, seed=4)
     o1 = G.gpu_paged(q, pool, 32, 8, 128, G.scale_for(128), num_splits=1)
