@@ -65,6 +65,13 @@ __device__ __forceinline__ float wave_xor(float x, int mask) {
   return __shfl_xor(x, mask, kWave);
 }
 
+// Index of this thread's wave in the workgroup, as a wave-uniform (scalar)
+// value: everything derived from it then stays in scalar registers and
+// branches on it are scalar branches, not exec-mask (divergent) ones.
+__device__ __forceinline__ int wave_id() {
+  return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+}
+
 __device__ __forceinline__ bool wave_any(bool p) {
   return __builtin_amdgcn_ballot_w64(p) != 0;
 }

@@ -42,7 +42,7 @@ __device__ __forceinline__ TileCoord prefill_coord(int block, int num_streams, i
   const int tile_rank = rest % n_qt;
   const int r = rest / n_qt;
   const int stream = xcd + kNumXcd * r;
-  const int wave = threadIdx.x >> 6;
+  const int wave = wave_id();
   TileCoord t;
   t.valid = stream < num_streams;
   t.seq = stream / hkv;

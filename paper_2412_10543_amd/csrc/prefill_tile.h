@@ -614,7 +614,7 @@ __device__ __forceinline__ void prefill_tile_pipe(
   constexpr int kLoadsPerTile = 2 * kInstr;      // vmcnt events per wave per tile
   static_assert(2 * kLoadsPerTile < 64, "vmcnt range");
   const int tid = threadIdx.x;
-  const int wave = tid >> 6, lane = tid & 63;
+  const int wave = wave_id(), lane = tid & 63;
   const PfRange rg = pf_range(nq, nk, q0, wg_rows, r0, causal);
   const int row = r0 + (lane & 31);
   PfPipeCtx cx;
@@ -677,17 +677,62 @@ __device__ __forceinline__ void prefill_tile_pipe(
   bf16_t* cur = s0;
   bf16_t* next = s1;
   bf16_t* after = s2;
-  for (int t = 0; t < nt; ++t) {
-    pf_slot<D, 1, 1>(st, lay, cx, 2 * t, sE, sO, pE, pO, cur, prev);
-    wait_tiles(t + 2 < nt ? 1 : 0);
-    pf_barrier();
-    if (t + 3 < nt) issue_tile(prev, (t + 3) * kPfBN);
-    pf_slot<D, 0, 0>(st, lay, cx, 2 * t + 1, sO, sE, pO, pE, next, cur);
+  auto rotate = [&]() {
     bf16_t* const retired = prev;
     prev = cur;
     cur = next;
     next = after;
     after = retired;
+  };
+  // Any tile: slots decide per block what to do (first and last blocks,
+  // masks, DMA near the end).
+  auto general_step = [&](int t) {
+    pf_slot<D, 1, 1>(st, lay, cx, 2 * t, sE, sO, pE, pO, cur, prev);
+    wait_tiles(t + 2 < nt ? 1 : 0);
+    pf_barrier();
+    if (t + 3 < nt) issue_tile(prev, (t + 3) * kPfBN);
+    pf_slot<D, 0, 0>(st, lay, cx, 2 * t + 1, sO, sE, pO, pE, next, cur);
+  };
+  // A tile whose two slots are full and unmasked for every wave and whose
+  // DMA is due: straight-line code (a separate loop, so that its values never
+  // meet the general path's at a join, which would cost register copies).
+  auto steady_step = [&](int t) {
+    float sum = pf_full_slot<D, 1, 1>(st, lay, cur, prev, sE, sO, pE, pO, cx.c,
+                                      -st.m_used * cx.c);
+    if (__builtin_expect(wave_any(!(sum <= kPfSumBound)), 0)) sum = pf_reref(st, sE, cx.c, pE);
+    st.l += sum;
+    wait_tiles(1);
+    pf_barrier();
+    issue_tile(prev, (t + 3) * kPfBN);
+    sum = pf_full_slot<D, 0, 0>(st, lay, next, cur, sO, sE, pO, pE, cx.c, -st.m_used * cx.c);
+    if (__builtin_expect(wave_any(!(sum <= kPfSumBound)), 0)) sum = pf_reref(st, sO, cx.c, pO);
+    st.l += sum;
+  };
+  // Steady tiles are [1, t_end): the workgroup's first row block has the
+  // fewest visible keys, so its limits bind every wave.  Tile t needs blocks
+  // up to 2t+2 computed (2t+2 < nbw), keys up to 64t+63 unmasked and the DMA
+  // of tile t+3 to exist.
+  int t_end;
+  {
+    const int kend0 = causal ? min(nk, min(q0 + 32, nq) + rg.off) : nk;
+    const int nbw0 = q0 >= nq ? 0 : (kend0 + 31) >> 5;
+    const int mlim0 = causal ? min(nk - 1, q0 + rg.off) : nk - 1;
+    const int a = nbw0 >= 3 ? (nbw0 - 3) / 2 + 1 : 0;
+    const int b = mlim0 >= 63 ? (mlim0 - 63) / 64 + 1 : 0;
+    t_end = min(min(a, b), nt - 3);
+  }
+  int t = 0;
+  for (; t < min(nt, 1); ++t) {
+    general_step(t);
+    rotate();
+  }
+  for (; t < t_end; ++t) {
+    steady_step(t);
+    rotate();
+  }
+  for (; t < nt; ++t) {
+    general_step(t);
+    rotate();
   }
   // PV of the last block, when this wave computes the whole last tile (its
   // stage is now prev).
