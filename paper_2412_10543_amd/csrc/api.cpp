@@ -234,7 +234,7 @@ rag_status rag_attn_decode_paged(const void* q, const void* k_cache, const void*
   const int64_t grid =
       (mixed ? rag::paged_prefill_grid(num_seqs - num_decode, num_kv_heads, group, max_seqlen_q)
              : 0) +
-      rag::paged_decode_grid(num_decode, num_kv_heads, splits);
+      rag::paged_decode_grid(num_decode, num_kv_heads, splits) + 8;   // + group padding
   if (grid > INT_MAX) return fail(RAG_ERR_UNSUPPORTED, "decode: batch too large for one grid");
 
   if (check_mode()) {

@@ -105,11 +105,14 @@ __global__ __launch_bounds__(64 * kPfWavesDense, 2) void prefill_varlen_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// Paged kernel.  Blocks [0, n_pf_blocks) are chunked-prefill tiles (mixed
-// batches only); each remaining block is one decode unit: split
-// sp = u / (num_decode * hkv) of (sequence, kv head) u % (num_decode * hkv),
-// where split sp of a sequence with P pages is the page range
-// [sp * pps, min((sp + 1) * pps, P)).
+// Paged kernel.  In a mixed batch the grid holds n_pf_blocks chunked-prefill
+// tiles and the decode units, interleaved in groups of eight consecutive
+// blocks (all tiles or all units; tile groups spread evenly through the grid)
+// so that MFMA-bound tiles and HBM-bound units share the CUs instead of
+// running one after the other; a tile keeps its XCD (block % 8).  Decode
+// unit u is split sp = u / (num_decode * hkv) of (sequence, kv head)
+// u % (num_decode * hkv), where split sp of a sequence with P pages is the
+// page range [sp * pps, min((sp + 1) * pps, P)).
 // ---------------------------------------------------------------------------
 struct PagedKernelArgs {
   const bf16_t* q;
@@ -124,6 +127,7 @@ struct PagedKernelArgs {
   int* arrivals;              // one counter per (decode sequence, kv head)
   int num_seqs, num_decode, max_blocks, hq, hkv, num_splits, pps;
   int n_pf_blocks, n_qt;
+  int n_dec_groups;           // mixed batches: groups of eight decode units
   float scale;
 };
 
@@ -162,10 +166,15 @@ __global__ __launch_bounds__(256, 2) void paged_kernel(PagedKernelArgs a) {
   const size_t block_stride = (size_t)a.hkv * 16 * D;
   int block = blockIdx.x;
   if constexpr (kMixed) {
-    if (block < a.n_pf_blocks) {
+    const int64_t tile_groups = a.n_pf_blocks / kNumXcd;
+    const int64_t groups = tile_groups + a.n_dec_groups;
+    const int gi = block / kNumXcd, x = block % kNumXcd;
+    const int tiles_before = (int)((int64_t)gi * tile_groups / groups);
+    const bool is_tile = (int64_t)(gi + 1) * tile_groups / groups > tiles_before;
+    if (is_tile) {
       const int num_pieces = a.num_seqs - a.num_decode;
-      const TileCoord tc =
-          prefill_coord<kPfWavesMixed>(block, num_pieces * a.hkv, a.hkv, group, a.n_qt);
+      const TileCoord tc = prefill_coord<kPfWavesMixed>(kNumXcd * tiles_before + x,
+                                                        num_pieces * a.hkv, a.hkv, group, a.n_qt);
       if (!tc.valid) return;
       const int s = a.num_decode + tc.seq;
       const int qb = a.cu_q[s], nq = a.cu_q[s + 1] - qb;
@@ -179,7 +188,7 @@ __global__ __launch_bounds__(256, 2) void paged_kernel(PagedKernelArgs a) {
                                            kv, nq, nk, tc.q0, tc.rows, tc.r0, a.scale, 1, lds);
       return;
     }
-    block -= a.n_pf_blocks;
+    block = kNumXcd * (gi - tiles_before) + x;
   }
   const int64_t pairs = (int64_t)a.num_decode * a.hkv;
   if ((int64_t)block >= pairs * a.num_splits) return;
@@ -245,7 +254,9 @@ static hipError_t launch_paged_d(const PagedArgs& a, hipStream_t stream) {
                                                 a.max_seqlen_q)
                            : 0;
   k.n_pf_blocks = (int)pf;
-  const int64_t dec = paged_decode_grid(a.num_decode, a.hkv, a.num_splits);
+  int64_t dec = paged_decode_grid(a.num_decode, a.hkv, a.num_splits);
+  if (pf > 0) dec = (dec + kNumXcd - 1) / kNumXcd * kNumXcd;   // whole groups of eight
+  k.n_dec_groups = (int)(dec / kNumXcd);
   const int64_t grid = pf + dec;
   if (grid > 0) {
     if (pf > 0)
