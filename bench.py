@@ -252,7 +252,8 @@ def run_mixed(st, pool_index=0):
 def bench_phase_mixed(torch, dev, reps):
     st = setup_mixed(torch, dev)
     w = st["w"]
-    run_mixed(st, 0)
+    for i in range(len(st["pools"])):   # first touch of each pool (page-table walks)
+        run_mixed(st, i)
     torch.cuda.synchronize()
     timer = Timer(torch)
     for r in range(reps):

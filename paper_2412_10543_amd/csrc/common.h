@@ -148,14 +148,11 @@ __device__ __forceinline__ void xcd_slot(int n, int& xcd, int& local) {
 
 // Prefill tiling shared by host and device.  A workgroup is W waves of 32
 // query rows each; the waves cover the q heads of one GQA group that read the
-// same K/V (pf_heads_per_wg of them) times W / pf_heads_per_wg row blocks.  The
-// dense prefill kernel uses 8 waves, which lets it hold two tiles of K/V
-// loads in flight per thread; the chunked-prefill pieces of the mixed paged
-// kernel use 4 (that kernel's decode units are 4-wave workgroups).
+// same K/V (pf_heads_per_wg of them) times W / pf_heads_per_wg row blocks.
+// Prefill workgroups (dense and chunked-prefill pieces) have 8 waves.
 constexpr int kPfRowsPerWave = 32;
 constexpr int kPfBN = 64;           // keys per K/V tile
 constexpr int kPfWavesDense = 8;
-constexpr int kPfWavesMixed = 4;
 
 __host__ __device__ constexpr int pf_heads_per_wg(int group) {
   return group % 4 == 0 ? 4 : (group % 2 == 0 ? 2 : 1);
@@ -164,23 +161,9 @@ __host__ __device__ constexpr int pf_rows_per_tile(int group, int waves) {
   return kPfRowsPerWave * (waves / pf_heads_per_wg(group));
 }
 
-// K and V tiles are both row-major [key][d] in LDS (64 banks of 4 bytes).
-// K rows are padded by 16 B: consecutive rows start one 16-byte bank group
-// apart, so the 16 lanes of an A-operand read (16 rows) hit distinct groups.
-// V rows by 64 B: the 32 lanes of a transposing read cover 4 rows x 64 B,
-// and rows four bank groups apart make those 16 groups distinct.
-template <int D>
-struct PfLds {
-  static constexpr int kStrK = D + 8;
-  static constexpr int kStrV = D + 32;
-  static constexpr int kElemsK = kPfBN * kStrK;
-  static constexpr int kElemsV = kPfBN * kStrV;
-  static constexpr int kElemsBuf = kElemsK + kElemsV;
-  static constexpr int kBytes = 2 * kElemsBuf * 2;   // two buffers of bf16
-};
-
-// Decode tiling: one wave per (sequence, kv head, split) unit, two 16-token
-// pages per step.
+// Decode tiling: one four-wave workgroup per (sequence, kv head, split) unit
+// (eight waves inside the mixed launch), each wave two 16-token pages per
+// step.
 constexpr int kDecThreads = 256;
 constexpr int kDecWaves = kDecThreads / kWave;
 constexpr int kDecMaxGroup = 16;           // q heads per kv head (MFMA N)
@@ -190,11 +173,15 @@ constexpr int kDecMaxGroup = 16;           // q heads per kv head (MFMA N)
 #define RAG_DEC_PAGES 2
 #endif
 constexpr int kDecPages = RAG_DEC_PAGES;   // pages per decode step
-template <int D, int NP = kDecPages>
+#ifndef RAG_MIXED_DEC_PAGES
+#define RAG_MIXED_DEC_PAGES 2
+#endif
+constexpr int kMixedDecPages = RAG_MIXED_DEC_PAGES;   // the same, in the mixed launch
+template <int D, int NP = kDecPages, int W = kDecWaves>
 struct DecLds {
   static constexpr int kStrV = D + 16;
   static constexpr int kElemsWave = 16 * NP * kStrV;
-  static constexpr int kBytes = kDecWaves * kElemsWave * 2;
+  static constexpr int kBytes = W * kElemsWave * 2;
 };
 
 }  // namespace rag

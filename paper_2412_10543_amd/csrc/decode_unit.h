@@ -1,4 +1,5 @@
-// One decode unit on gfx950: a workgroup of four waves attends the query row
+// One decode unit on gfx950: a workgroup of W waves (four, or eight inside the
+// mixed launch) attends the query row
 // of every q head of one GQA group (one decode token of one sequence) to a
 // contiguous range of pages of that sequence's paged KV cache.
 //
@@ -6,7 +7,7 @@
 // with a log-sum-exp merge of the partial results (Flash-Decoding), online
 // softmax in fp32.  Layout choices for CDNA4:
 //   * every K/V byte of the range is read once, for all G heads of the group,
-//     with 16-byte loads; the four waves take interleaved steps of NP pages,
+//     with 16-byte loads; the W waves take interleaved steps of NP pages,
 //     so at any time they stream neighbouring pages;
 //   * both products run on v_mfma_f32_16x16x32_bf16 with the G query heads as
 //     the N dimension (padded to 16): S^T = K Q^T straight from registers,
@@ -14,7 +15,7 @@
 //     slice and read back as V^T fragments by the transposing LDS read;
 //   * one register set per step is refilled as soon as it has been consumed,
 //     so the next step's pages are in flight while the current one computes;
-//   * the four waves' states are merged through LDS; a unit that covers only
+//   * the W waves' states are merged through LDS; a unit that covers only
 //     part of its sequence (a split) writes a normalised partial output and
 //     its log-sum-exp, and the last split of the sequence to finish merges
 //     all of them in the same kernel.
@@ -196,15 +197,15 @@ __device__ __forceinline__ void decode_wave(
 }
 
 // Merge of the n_sp split partials of the q heads assigned to this wave (h =
-// wave, wave + 4, ...), in split order.  Lane sp holds split sp's weight; the
+// wave, wave + W, ...), in split order.  Lane sp holds split sp's weight; the
 // partial rows are read with device-coherent loads, 16 splits at a time, each
 // lane owning D/64 consecutive output values.
-template <int D>
+template <int D, int W>
 __device__ __forceinline__ void merge_splits(const DecodeOut& out, int group) {
   constexpr int kPer = D / 64;                 // 2 (D = 128) or 1 (D = 64)
   constexpr int kBatch = 16;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  for (int h = wave; h < group; h += kDecWaves) {
+  for (int h = wave; h < group; h += W) {
     const float* pl = out.part_lse + (size_t)h * out.num_splits;
     const float* po = out.part_o + (size_t)h * out.num_splits * D + lane * kPer;
     const float lse = lane < out.n_sp ? load_coherent(pl + lane) : -INFINITY;
@@ -244,23 +245,23 @@ __device__ __forceinline__ void merge_splits(const DecodeOut& out, int group) {
   }
 }
 
-// Bytes of LDS the merge of four waves needs (it reuses the V slices).
-template <int D>
+// Bytes of LDS the merge of W waves needs (it reuses the V slices).
+template <int D, int W>
 constexpr int dec_merge_bytes() {
-  return (kDecWaves * 16 * D + 2 * kDecWaves * 16 + 1) * 4;
+  return (W * 16 * D + 2 * W * 16 + 1) * 4;
 }
 
-// The whole unit: the workgroup's four waves cover the page range
+// The whole unit: the workgroup's W waves cover the page range
 // [p_begin, p_end) in interleaved steps of NP pages, merge through LDS and
 // write either the final rows (n_sp == 1) or this split's partial rows; the
 // last split of the row to arrive then merges all partials.
-template <int D, int NP>
+template <int D, int NP, int W>
 __device__ __forceinline__ void decode_unit(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ kc, const bf16_t* __restrict__ vc,
     size_t block_stride, const int32_t* __restrict__ table, int kv_len, int group,
     int p_begin, int p_end, float scale, const DecodeOut& out, bf16_t* __restrict__ lds) {
-  using L = DecLds<D, NP>;
-  static_assert(dec_merge_bytes<D>() <= L::kBytes, "merge area must fit in the V slices");
+  using L = DecLds<D, NP, W>;
+  static_assert(dec_merge_bytes<D, W>() <= L::kBytes, "merge area must fit in the V slices");
   constexpr int kDt = D / 16;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int l16 = lane & 15, gq = lane >> 4;
@@ -268,13 +269,13 @@ __device__ __forceinline__ void decode_unit(
   f32x4 oacc[kDt];
   float m_used, l;
   decode_wave<D, NP>(q, kc, vc, block_stride, table, kv_len, group, p_begin + wave * NP, p_end,
-                     kDecWaves * NP, scale, lds + wave * L::kElemsWave, oacc, m_used, l);
+                     W * NP, scale, lds + wave * L::kElemsWave, oacc, m_used, l);
 
-  // ---- merge the four waves through LDS (reusing the V slices) -------------
+  // ---- merge the W waves through LDS (reusing the V slices) -------------
   // floats: O [wave][16 heads][D], then m [wave][16], then l [wave][16]
   float* mo = reinterpret_cast<float*>(lds);
-  float* mm = mo + kDecWaves * 16 * D;
-  float* ml = mm + kDecWaves * 16;
+  float* mm = mo + W * 16 * D;
+  float* ml = mm + W * 16;
   __syncthreads();
   if (l16 < group) {
 #pragma unroll
@@ -288,15 +289,15 @@ __device__ __forceinline__ void decode_unit(
   __syncthreads();
   const float c = scale * kLog2e;
   constexpr int kPer = D / 64;
-  for (int h = wave; h < group; h += kDecWaves) {
+  for (int h = wave; h < group; h += W) {
     float m = -INFINITY;
 #pragma unroll
-    for (int w = 0; w < kDecWaves; ++w) m = fmaxf(m, mm[w * 16 + h]);
+    for (int w = 0; w < W; ++w) m = fmaxf(m, mm[w * 16 + h]);
     float den = 0.f, acc[kPer];
 #pragma unroll
     for (int e = 0; e < kPer; ++e) acc[e] = 0.f;
 #pragma unroll
-    for (int w = 0; w < kDecWaves; ++w) {
+    for (int w = 0; w < W; ++w) {
       const float mw = mm[w * 16 + h];
       const float f = (mw == -INFINITY) ? 0.f : fast_exp2((mw - m) * c);
       den += f * ml[w * 16 + h];
@@ -330,12 +331,12 @@ __device__ __forceinline__ void decode_unit(
   // between calls.
   wait_all_memory();
   __syncthreads();
-  int* flag = reinterpret_cast<int*>(ml + kDecWaves * 16);
+  int* flag = reinterpret_cast<int*>(ml + W * 16);
   if (threadIdx.x == 0)
     *flag = __hip_atomic_fetch_add(out.arrival, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   __syncthreads();
   if (*flag != out.n_sp - 1) return;
-  merge_splits<D>(out, group);
+  merge_splits<D, W>(out, group);
   if (threadIdx.x == 0)
     __hip_atomic_store(out.arrival, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }

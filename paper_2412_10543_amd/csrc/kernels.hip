@@ -1,9 +1,10 @@
 // gfx950 kernels of the RAG-synthesis attention path and their launchers:
 //   prefill_varlen_kernel  packed variable-length prefill (dense K/V)
-//   paged_kernel           decode rows against a paged KV cache, optionally
-//                          with chunked-prefill pieces in the same launch
-//                          (split-KV partials are merged inside it by the
-//                          last split of each sequence to finish)
+//   paged_decode_kernel    decode rows against a paged KV cache (split-KV
+//                          partials are merged inside it by the last split
+//                          of each sequence to finish)
+//   mixed_kernel           decode rows and chunked-prefill pieces of a
+//                          paged cache in one launch
 #include <algorithm>
 #include <climits>
 
@@ -68,7 +69,7 @@ int64_t prefill_grid(int num_seqs, int hkv, int group, int max_seqlen_q) {
 }
 
 int64_t paged_prefill_grid(int num_pieces, int hkv, int group, int max_seqlen_q) {
-  return tile_grid(num_pieces, hkv, group, max_seqlen_q, kPfWavesMixed);
+  return tile_grid(num_pieces, hkv, group, max_seqlen_q, kPfWavesDense);
 }
 
 int64_t paged_decode_grid(int num_decode, int hkv, int num_splits) {
@@ -98,7 +99,7 @@ __global__ __launch_bounds__(64 * kPfWavesDense, 2) void prefill_varlen_kernel(
   const size_t qs = (size_t)hq * D;
   DenseKV kv{k + ((size_t)kb * hkv + tc.kvh) * D, v + ((size_t)kb * hkv + tc.kvh) * D,
              (size_t)hkv * D};
-  prefill_tile_pipe<D, kPfWavesDense>(
+  prefill_tile_pipe<D, kPfWavesDense, DenseKV>(
       q + ((size_t)qb * hq + tc.head) * D, qs, o + ((size_t)qb * hq + tc.head) * D, qs,
       lse ? lse + (size_t)tc.head * tq + qb : nullptr, kv, nq, nk, tc.q0, tc.rows, tc.r0, scale,
       causal, st0, st1, st2, st3);
@@ -132,8 +133,8 @@ struct PagedKernelArgs {
 };
 
 // One piece of a decode row: pages [p_begin, p_end) of (row s, kv head kvh),
-// split sp of n_sp.
-template <int D>
+// split sp of n_sp, on W waves taking NP pages a step.
+template <int D, int NP, int W>
 __device__ __forceinline__ void decode_piece(const PagedKernelArgs& a, int group,
                                              size_t block_stride, int s, int kvh, int kv_len,
                                              int p_begin, int p_end, int sp, int n_sp,
@@ -150,50 +151,20 @@ __device__ __forceinline__ void decode_piece(const PagedKernelArgs& a, int group
   out.sp = sp;
   out.n_sp = n_sp;
   out.num_splits = a.num_splits;
-  decode_unit<D, kDecPages>(a.q + ((size_t)row * a.hq + h0) * D, a.kc + (size_t)kvh * 16 * D,
+  decode_unit<D, NP, W>(a.q + ((size_t)row * a.hq + h0) * D, a.kc + (size_t)kvh * 16 * D,
                             a.vc + (size_t)kvh * 16 * D, block_stride,
                             a.tables + (size_t)s * a.max_blocks, kv_len, group, p_begin, p_end,
                             a.scale, out, lds);
 }
 
-template <int D, bool kMixed>
-__global__ __launch_bounds__(256, 2) void paged_kernel(PagedKernelArgs a) {
-  constexpr int kLdsBytes =
-      kMixed ? (PfLds<D>::kBytes > DecLds<D>::kBytes ? PfLds<D>::kBytes : DecLds<D>::kBytes)
-             : DecLds<D>::kBytes;
-  __shared__ __attribute__((aligned(16))) bf16_t lds[kLdsBytes / 2];
-  const int group = a.hq / a.hkv;
-  const size_t block_stride = (size_t)a.hkv * 16 * D;
-  int block = blockIdx.x;
-  if constexpr (kMixed) {
-    const int64_t tile_groups = a.n_pf_blocks / kNumXcd;
-    const int64_t groups = tile_groups + a.n_dec_groups;
-    const int gi = block / kNumXcd, x = block % kNumXcd;
-    const int tiles_before = (int)((int64_t)gi * tile_groups / groups);
-    const bool is_tile = (int64_t)(gi + 1) * tile_groups / groups > tiles_before;
-    if (is_tile) {
-      const int num_pieces = a.num_seqs - a.num_decode;
-      const TileCoord tc = prefill_coord<kPfWavesMixed>(kNumXcd * tiles_before + x,
-                                                        num_pieces * a.hkv, a.hkv, group, a.n_qt);
-      if (!tc.valid) return;
-      const int s = a.num_decode + tc.seq;
-      const int qb = a.cu_q[s], nq = a.cu_q[s + 1] - qb;
-      if (tc.q0 >= nq) return;
-      const int nk = a.kv_lens[s];
-      const size_t qs = (size_t)a.hq * D;
-      PagedKV<D> kv{a.kc + (size_t)tc.kvh * 16 * D, a.vc + (size_t)tc.kvh * 16 * D,
-                    a.tables + (size_t)s * a.max_blocks, block_stride};
-      prefill_tile_regs<D, kPfWavesMixed>(a.q + ((size_t)qb * a.hq + tc.head) * D, qs,
-                                           a.o + ((size_t)qb * a.hq + tc.head) * D, qs, nullptr,
-                                           kv, nq, nk, tc.q0, tc.rows, tc.r0, a.scale, 1, lds);
-      return;
-    }
-    block = kNumXcd * (gi - tiles_before) + x;
-  }
+// Decode unit u with fixed page ranges (see above), on W waves.
+template <int D, int NP, int W>
+__device__ __forceinline__ void decode_block(const PagedKernelArgs& a, int u, int group,
+                                             size_t block_stride, bf16_t* lds) {
   const int64_t pairs = (int64_t)a.num_decode * a.hkv;
-  if ((int64_t)block >= pairs * a.num_splits) return;
-  const int sp = (int)(block / pairs);
-  const int pr = (int)(block % pairs);
+  if ((int64_t)u >= pairs * a.num_splits) return;
+  const int sp = (int)(u / pairs);
+  const int pr = (int)(u % pairs);
   const int s = pr / a.hkv, kvh = pr % a.hkv;
   const int kv_len = min(a.kv_lens[s], a.max_blocks * 16);
   const int n_pages = (kv_len + 15) >> 4;
@@ -201,7 +172,54 @@ __global__ __launch_bounds__(256, 2) void paged_kernel(PagedKernelArgs a) {
   if (sp >= n_sp && sp > 0) return;
   const int p_begin = sp * a.pps;
   const int p_end = min(n_pages, p_begin + a.pps);
-  decode_piece<D>(a, group, block_stride, s, kvh, kv_len, p_begin, p_end, sp, n_sp, lds);
+  decode_piece<D, NP, W>(a, group, block_stride, s, kvh, kv_len, p_begin, p_end, sp, n_sp, lds);
+}
+
+// Decode rows only: one four-wave workgroup per decode unit.
+template <int D>
+__global__ __launch_bounds__(kDecThreads, 2) void paged_decode_kernel(PagedKernelArgs a) {
+  __shared__ __attribute__((aligned(16))) bf16_t lds[DecLds<D>::kBytes / 2];
+  decode_block<D, kDecPages, kDecWaves>(a, blockIdx.x, a.hq / a.hkv, (size_t)a.hkv * 16 * D, lds);
+}
+
+// Mixed batch: eight-wave workgroups.  A chunked-prefill tile runs the dense
+// prefill's pipelined tile loop with K/V gathered from the paged cache; a
+// decode unit runs on all eight waves (a tile workgroup fills the CU's
+// registers, so a decode unit has the CU to itself and needs twice the pages
+// in flight of a four-wave unit to keep its share of HBM bandwidth).
+template <int D>
+__global__ __launch_bounds__(64 * kPfWavesDense, 2) void mixed_kernel(PagedKernelArgs a) {
+  constexpr int kE = ChunkLayout<D>::kElemsTile;
+  using DL = DecLds<D, kMixedDecPages, kPfWavesDense>;
+  __shared__ __attribute__((aligned(16))) bf16_t lds[4 * kE > DL::kBytes / 2 ? 4 * kE
+                                                                           : DL::kBytes / 2];
+  const int group = a.hq / a.hkv;
+  const size_t block_stride = (size_t)a.hkv * 16 * D;
+  const int64_t tile_groups = a.n_pf_blocks / kNumXcd;
+  const int64_t groups = tile_groups + a.n_dec_groups;
+  const int gi = blockIdx.x / kNumXcd, x = blockIdx.x % kNumXcd;
+  const int tiles_before = (int)((int64_t)gi * tile_groups / groups);
+  const bool is_tile = (int64_t)(gi + 1) * tile_groups / groups > tiles_before;
+  if (is_tile) {
+    const int num_pieces = a.num_seqs - a.num_decode;
+    const TileCoord tc = prefill_coord<kPfWavesDense>(kNumXcd * tiles_before + x,
+                                                      num_pieces * a.hkv, a.hkv, group, a.n_qt);
+    if (!tc.valid) return;
+    const int s = a.num_decode + tc.seq;
+    const int qb = a.cu_q[s], nq = a.cu_q[s + 1] - qb;
+    if (tc.q0 >= nq) return;
+    const int nk = min(a.kv_lens[s], a.max_blocks * 16);
+    const size_t qs = (size_t)a.hq * D;
+    const PagedDmaKV<D> kv{a.kc + (size_t)tc.kvh * 16 * D, a.vc + (size_t)tc.kvh * 16 * D,
+                           a.tables + (size_t)s * a.max_blocks, block_stride};
+    prefill_tile_pipe<D, kPfWavesDense, PagedDmaKV<D>>(
+        a.q + ((size_t)qb * a.hq + tc.head) * D, qs, a.o + ((size_t)qb * a.hq + tc.head) * D, qs,
+        nullptr, kv, nq, nk, tc.q0, tc.rows, tc.r0, a.scale, 1, lds, lds + kE, lds + 2 * kE,
+        lds + 3 * kE);
+    return;
+  }
+  decode_block<D, kMixedDecPages, kPfWavesDense>(a, kNumXcd * (gi - tiles_before) + x, group,
+                                                 block_stride, lds);
 }
 
 // ---------------------------------------------------------------------------
@@ -248,7 +266,7 @@ static hipError_t launch_paged_d(const PagedArgs& a, hipStream_t stream) {
   k.pps = std::max(1, (a.max_blocks + a.num_splits - 1) / a.num_splits);
   k.scale = a.scale;
   const bool mixed = a.cu_q != nullptr && a.num_seqs > a.num_decode;
-  const int pf_rows = pf_rows_per_tile(group, kPfWavesMixed);
+  const int pf_rows = pf_rows_per_tile(group, kPfWavesDense);
   k.n_qt = mixed ? (a.max_seqlen_q + pf_rows - 1) / pf_rows : 0;
   const int64_t pf = mixed ? paged_prefill_grid(a.num_seqs - a.num_decode, a.hkv, group,
                                                 a.max_seqlen_q)
@@ -260,9 +278,11 @@ static hipError_t launch_paged_d(const PagedArgs& a, hipStream_t stream) {
   const int64_t grid = pf + dec;
   if (grid > 0) {
     if (pf > 0)
-      hipLaunchKernelGGL((paged_kernel<D, true>), dim3((unsigned)grid), dim3(256), 0, stream, k);
+      hipLaunchKernelGGL(mixed_kernel<D>, dim3((unsigned)grid), dim3(64 * kPfWavesDense), 0,
+                         stream, k);
     else
-      hipLaunchKernelGGL((paged_kernel<D, false>), dim3((unsigned)grid), dim3(256), 0, stream, k);
+      hipLaunchKernelGGL(paged_decode_kernel<D>, dim3((unsigned)grid), dim3(kDecThreads), 0,
+                         stream, k);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }

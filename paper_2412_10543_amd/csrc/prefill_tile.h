@@ -11,21 +11,19 @@
 //     shared through LDS by all waves (all heads of the group) of the tile;
 //   * scores are computed transposed, S^T = K Q^T, so each lane owns one query
 //     row and its scores already sit where the B operand of O^T = V^T P^T
-//     needs them; the matching V^T A operand comes straight from the
-//     row-major V tile through the transposing LDS read (ds_read_b64_tr_b16),
-//     so no data is shuffled between the two products and nothing is
-//     transposed on the way into LDS;
+//     needs them; the matching V^T A operand comes straight from the V tile
+//     through the transposing LDS read (ds_read_b64_tr_b16), so no data is
+//     shuffled between the two products;
+//   * K/V tiles go from HBM straight into LDS (global_load_lds_dwordx4),
+//     four stages, issued three tiles ahead; dense rows or pages of a paged
+//     cache (each DMA instruction covers one page);
+//   * the work of each wave is software-pipelined over blocks of 32 keys so
+//     that the matrix cores and the vector ALU work side by side;
 //   * softmax statistics in fp32 with exp2 and the scale folded into one
-//     FMA; the reference maximum is moved lazily (only when a score exceeds
-//     it by 2^8), which keeps rescales of the output off the common path;
-//   * masking only on tiles that cross the causal diagonal or the sequence
-//     end; tiles fully above the diagonal are skipped per wave;
-//   * two ways to stage K/V: (a) DMA -- global_load_lds_dwordx4 writes the
-//     tile straight into one of three LDS stages two tiles ahead of its use,
-//     with XOR-swizzled rows so every LDS read group is conflict-free (dense
-//     K/V); (b) registers -- 16-byte loads into registers, then LDS rows
-//     padded against bank conflicts; this path can zero rows past the
-//     sequence end, which a paged cache's tail slots need.
+//     FMA; the exponent reference moves only when a block's weights would
+//     grow past 2^16, which keeps rescales of the output off the common path;
+//   * masking only on blocks that cross the causal diagonal or the sequence
+//     end; blocks fully above the diagonal are skipped per wave.
 #pragma once
 
 #include "common.h"
@@ -34,6 +32,7 @@ namespace rag {
 
 // K/V rows of one (sequence, kv head) stored densely: token j at k + j*stride.
 struct DenseKV {
+  static constexpr bool kPaged = false;
   const bf16_t* k;
   const bf16_t* v;
   size_t stride;
@@ -42,48 +41,35 @@ struct DenseKV {
 };
 
 // K/V rows of one (sequence, kv head) in a paged cache: token j lives in
-// physical block table[j / 16], slot j % 16.  k and v already point at the kv
-// head inside block 0; block_stride is the distance between blocks.
+// physical block table[j / 16], slot j % 16.  k and v point at the kv head
+// inside block 0; block_stride is the distance between blocks.  A DMA
+// instruction covers 16 consecutive rows of a tile, i.e. one page, so its
+// page id is the same for the whole wave and is read with a scalar load.
 template <int D>
-struct PagedKV {
+struct PagedDmaKV {
+  static constexpr bool kPaged = true;
   const bf16_t* k;
   const bf16_t* v;
   const int32_t* table;
   size_t block_stride;
-  __device__ __forceinline__ size_t off(int j) const {
-    return (size_t)table[j >> 4] * block_stride + (size_t)(j & 15) * D;
+  // The block table is read-only for the whole launch; reading it through
+  // the constant address space lets the wave-uniform reads be scalar loads
+  // (a vector load would make the compiler wait for every DMA in flight).
+  __device__ __forceinline__ int page(int p) const {
+    typedef __attribute__((address_space(4))) const int32_t const_i32;
+    return ((const_i32*)table)[p];
   }
-  __device__ __forceinline__ const bf16_t* krow(int j) const { return k + off(j); }
-  __device__ __forceinline__ const bf16_t* vrow(int j) const { return v + off(j); }
-};
-
-// ---------------------------------------------------------------------------
-// LDS layouts of one K/V tile (64 keys, row-major [key][d]).  Each layout
-// object holds the lane-dependent part of its read offsets, so that every
-// LDS read in the tile loop is one register plus a compile-time immediate.
-//   k_off(mt, ks): A-operand read of K rows 32*mt + l32, d = 16*ks + 8*half
-//   v_off(r, dt):  transposing read of the V slice starting at row r (r a
-//                  multiple of 8), d tile dt (see pf_tile)
-// ---------------------------------------------------------------------------
-// Padded rows (register staging): K rows +16 B, V rows +64 B (see PfLds).
-template <int D>
-struct PaddedLayout {
-  using L = PfLds<D>;
-  int k_lane, v_lane;
-  __device__ __forceinline__ PaddedLayout() {
-    const int lane = threadIdx.x & 63;
-    const int l32 = lane & 31, half = lane >> 5, g16 = lane >> 4, r16 = lane & 15;
-    k_lane = l32 * L::kStrK + 8 * half;
-    v_lane = (4 * half + (r16 >> 2)) * L::kStrV + 16 * (g16 & 1) + 4 * (r16 & 3);
-  }
-  __device__ __forceinline__ int k_off(int mt, int ks) const {
-    return 32 * mt * L::kStrK + 16 * ks + k_lane;
-  }
-  __device__ __forceinline__ int v_off(int r, int dt) const {
-    return r * L::kStrV + 32 * dt + v_lane;
+  __device__ __forceinline__ size_t at(int page_id, int slot) const {
+    return (size_t)page_id * block_stride + (size_t)slot * D;
   }
 };
 
+// ---------------------------------------------------------------------------
+// LDS layout of one staged K/V tile (64 keys): k_off(mt, ks) is the A-operand
+// read of K rows 32*mt + l32 at d = 16*ks + 8*half; v_off(r, dt) the
+// transposing read of the V slice starting at row r (r a multiple of 8),
+// d tile dt (see pf_pv).
+// ---------------------------------------------------------------------------
 // DMA staging layout.  A DMA instruction writes 64 consecutive 16-byte
 // chunks (lane l at +16*l) but may gather them from anywhere, so the tile is
 // stored chunk-permuted.  gfx950's LDS has 64 four-byte banks; a 16-byte read
@@ -154,98 +140,6 @@ __device__ __forceinline__ void pf_init(PfState<D>& st, const bf16_t* __restrict
   st.l = 0.f;
 }
 
-// One 64-key tile for this wave's 32 rows [r0, r0 + 32).
-template <int D, class Layout>
-__device__ __forceinline__ void pf_tile(PfState<D>& st, const Layout& lay,
-                                        const bf16_t* __restrict__ kl,
-                                        const bf16_t* __restrict__ vl, int k0, int r0, int nk,
-                                        int off, int causal, float c, float tau) {
-  constexpr int kKs = D / 16;
-  constexpr int kDt = D / 32;
-  const int lane = threadIdx.x & 63;
-  const int l32 = lane & 31, half = lane >> 5;
-  const int row = r0 + l32;
-
-  // ---- S^T = K Q^T for 64 keys x 32 rows ------------------------------------
-  // accumulator element j of m-tile mt holds key 32*mt + 8*(j/4) + 4*half +
-  // j%4 of this lane's query row.
-  f32x16 s[2];
-#pragma unroll
-  for (int mt = 0; mt < 2; ++mt)
-#pragma unroll
-    for (int j = 0; j < 16; ++j) s[mt][j] = 0.f;
-#pragma unroll
-  for (int ks = 0; ks < kKs; ++ks) {
-#pragma unroll
-    for (int mt = 0; mt < 2; ++mt) {
-      const bf16x8 a = *reinterpret_cast<const bf16x8*>(kl + lay.k_off(mt, ks));
-      s[mt] = mfma32(a, st.qf[ks], s[mt]);
-    }
-  }
-  // ---- mask (diagonal / ragged tiles only) ----------------------------------
-  const bool need_mask = (k0 + kPfBN > nk) || (causal && k0 + kPfBN - 1 > r0 + off);
-  if (need_mask) {
-    const int lim = causal ? min(nk - 1, row + off) : nk - 1;
-#pragma unroll
-    for (int mt = 0; mt < 2; ++mt)
-#pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        const int key = k0 + 32 * mt + 8 * (j >> 2) + 4 * half + (j & 3);
-        if (key > lim) s[mt][j] = -INFINITY;
-      }
-  }
-  // ---- online softmax ---------------------------------------------------------
-  float tmax = s[0][0];
-#pragma unroll
-  for (int mt = 0; mt < 2; ++mt)
-#pragma unroll
-    for (int j = 0; j < 16; ++j) tmax = fmaxf(tmax, s[mt][j]);
-  tmax = fmaxf(tmax, wave_xor(tmax, 32));
-  if (wave_any(tmax > st.m_used + tau)) {
-    const float m_new = fmaxf(st.m_used, tmax);
-    const float alpha = (st.m_used == -INFINITY) ? 0.f : fast_exp2((st.m_used - m_new) * c);
-    st.l *= alpha;
-#pragma unroll
-    for (int dt = 0; dt < kDt; ++dt)
-#pragma unroll
-      for (int j = 0; j < 16; ++j) st.oacc[dt][j] *= alpha;
-    st.m_used = m_new;
-  }
-  const float mref = (st.m_used == -INFINITY) ? 0.f : st.m_used * c;
-#pragma unroll
-  for (int mt = 0; mt < 2; ++mt)
-#pragma unroll
-    for (int j = 0; j < 16; ++j) {
-      const float p = fast_exp2(fmaf(s[mt][j], c, -mref));
-      s[mt][j] = p;
-      st.l += p;
-    }
-  // ---- O^T += V^T P^T ---------------------------------------------------------
-  // k-step (mt, s2) covers keys 32*mt + 16*s2 + [0, 16); B-operand slot
-  // 8*half + t is accumulator element 8*s2 + t, i.e. key
-  // 32*mt + 16*s2 + 8*(t/4) + 4*half + t%4, which the two transposing reads
-  // (slices +0 and +8) deliver in the same order.  Transposing-read source:
-  // lane (group g = lane/16, r = lane%16) points at key slice + 4*half + r/4,
-  // d = 32*dt + 16*(g%2) + 4*(r%4); the group's result gives lane l the
-  // values V[slice + 4*half + k][32*dt + l%32], k = 0..3.
-#pragma unroll
-  for (int mt = 0; mt < 2; ++mt) {
-#pragma unroll
-    for (int s2 = 0; s2 < 2; ++s2) {
-      const int b = 8 * s2;
-      const bf16x8 pb = to_bf16x8(s[mt][b], s[mt][b + 1], s[mt][b + 2], s[mt][b + 3],
-                                  s[mt][b + 4], s[mt][b + 5], s[mt][b + 6], s[mt][b + 7]);
-      const int rw = 32 * mt + 16 * s2;
-#pragma unroll
-      for (int dt = 0; dt < kDt; ++dt) {
-        const bf16x8 a = join_bf16x8(lds_read_tr4(vl + lay.v_off(rw, dt)),
-                                     lds_read_tr4(vl + lay.v_off(rw + 8, dt)));
-        st.oacc[dt] = mfma32(a, pb, st.oacc[dt]);
-      }
-    }
-  }
-}
-
 // Normalise and store this wave's rows and their log-sum-exp.
 template <int D>
 __device__ __forceinline__ void pf_store(const PfState<D>& st, bf16_t* __restrict__ o,
@@ -286,74 +180,8 @@ __device__ __forceinline__ PfRange pf_range(int nq, int nk, int q0, int wg_rows,
 }
 
 // ---------------------------------------------------------------------------
-// Register-staged tile loop (padded LDS rows, double buffer, one tile ahead).
-// q, o and lse point at row 0 of the sequence for this wave's head; the
-// workgroup (W waves) covers rows [q0, q0 + wg_rows) and this wave rows
-// [r0, r0 + 32).  Rows past the sequence end are staged as zeros.
-// ---------------------------------------------------------------------------
-template <int D, int W, class KV>
-__device__ __forceinline__ void prefill_tile_regs(
-    const bf16_t* __restrict__ q, size_t q_stride, bf16_t* __restrict__ o, size_t o_stride,
-    float* __restrict__ lse, const KV& kv, int nq, int nk, int q0, int wg_rows, int r0,
-    float scale, int causal, bf16_t* __restrict__ lds) {
-  using L = PfLds<D>;
-  constexpr int kThreads = 64 * W;
-  constexpr int kCh = D / 8;                  // 16-byte chunks per row
-  constexpr int kRowsPerIt = kThreads / kCh;
-  constexpr int kIt = kPfBN / kRowsPerIt;     // K (and V) loads per thread per tile
-  static_assert(kIt >= 1 && kPfBN % kRowsPerIt == 0, "tile staging layout");
-  const int tid = threadIdx.x;
-  const PfRange rg = pf_range(nq, nk, q0, wg_rows, r0, causal);
-  const float c = scale * kLog2e;
-  const float tau = kRescaleLog2 / c;
-
-  PfState<D> st;
-  pf_init(st, q, q_stride, r0 + (tid & 31), nq);
-
-  const int ld_ch = tid % kCh;
-  const int ld_row = tid / kCh;
-  u32x4 kreg[kIt], vreg[kIt];
-  auto load_tile = [&](int k0) {
-#pragma unroll
-    for (int it = 0; it < kIt; ++it) {
-      const int j = k0 + it * kRowsPerIt + ld_row;
-      u32x4 z = {0, 0, 0, 0};
-      kreg[it] = j < nk ? load16(kv.krow(j) + ld_ch * 8) : z;
-      vreg[it] = j < nk ? load16(kv.vrow(j) + ld_ch * 8) : z;
-    }
-  };
-  auto store_tile = [&](int buf) {
-    bf16_t* kl = lds + buf * L::kElemsBuf;
-    bf16_t* vl = kl + L::kElemsK;
-#pragma unroll
-    for (int it = 0; it < kIt; ++it) {
-      const int r = it * kRowsPerIt + ld_row;
-      *reinterpret_cast<u32x4*>(kl + r * L::kStrK + ld_ch * 8) = kreg[it];
-      *reinterpret_cast<u32x4*>(vl + r * L::kStrV + ld_ch * 8) = vreg[it];
-    }
-  };
-
-  const PaddedLayout<D> lay;
-  if (rg.n_tiles > 0) {
-    load_tile(0);
-    store_tile(0);
-  }
-  __syncthreads();
-  for (int t = 0; t < rg.n_tiles; ++t) {
-    const int k0 = t * kPfBN;
-    if (t + 1 < rg.n_tiles) load_tile(k0 + kPfBN);
-    const bf16_t* kl = lds + (t & 1) * L::kElemsBuf;
-    if (k0 < rg.kend_w)
-      pf_tile<D>(st, lay, kl, kl + L::kElemsK, k0, r0, nk, rg.off, causal, c, tau);
-    if (t + 1 < rg.n_tiles) store_tile((t + 1) & 1);
-    __syncthreads();
-  }
-  pf_store(st, o, o_stride, lse, r0 + (tid & 31), nq, scale);
-}
-
-// ---------------------------------------------------------------------------
-// Software-pipelined tile loop for dense K/V (DMA staging into four LDS
-// stages of ChunkLayout).
+// Software-pipelined tile loop (K/V DMA-staged into four LDS stages of
+// ChunkLayout; KV is DenseKV or PagedDmaKV).
 //
 // The unit of work is a block of 32 keys (half a tile).  For block b a wave
 // does QK(b) (S^T of 32 keys x its 32 rows: D/16 MFMAs), SM(b) (exp2 of the
@@ -601,10 +429,10 @@ __device__ __forceinline__ void pf_slot(PfState<D>& st, const ChunkLayout<D>& la
   }
 }
 
-template <int D, int W>
+template <int D, int W, class KV>
 __device__ __forceinline__ void prefill_tile_pipe(
     const bf16_t* __restrict__ q, size_t q_stride, bf16_t* __restrict__ o, size_t o_stride,
-    float* __restrict__ lse, const DenseKV& kv, int nq, int nk, int q0, int wg_rows, int r0,
+    float* __restrict__ lse, const KV& kv, int nq, int nk, int q0, int wg_rows, int r0,
     float scale, int causal, bf16_t* __restrict__ s0, bf16_t* __restrict__ s1,
     bf16_t* __restrict__ s2, bf16_t* __restrict__ s3) {
   using Lay = ChunkLayout<D>;
@@ -629,7 +457,27 @@ __device__ __forceinline__ void prefill_tile_pipe(
   // Instruction i of this wave writes staged chunks [64*gi, 64*gi + 64) of
   // the K and of the V region, gi = wave*kInstr + i; lane l fetches the
   // (row, chunk) that staged chunk 64*gi + l holds.  Rows past the sequence
-  // end are loaded from its last row (finite data; those keys are masked).
+  // end are loaded from its last row (finite data; those keys are masked --
+  // the tail slots of a cache page may hold anything).  The 16 rows of one
+  // instruction lie in one page: for a paged cache its id is read once for
+  // the wave, from ids loaded while the previous tile was issued.
+  static_assert(kPfBN == 64, "a tile spans four pages");
+  const int last_page = (nk - 1) >> 4;
+  int pid0 = 0, pid1 = 0, pid2 = 0, pid3 = 0;   // page ids of the next tile issued
+  auto load_ids = [&](int k0) {
+    if constexpr (KV::kPaged) {
+      const int p0 = k0 >> 4;
+      pid0 = kv.page(min(p0, last_page));
+      pid1 = kv.page(min(p0 + 1, last_page));
+      pid2 = kv.page(min(p0 + 2, last_page));
+      pid3 = kv.page(min(p0 + 3, last_page));
+    }
+  };
+  auto pick = [&](int qi) {   // qi wave-uniform, 0..3; selects values, not lvalues
+    const int lo = (qi & 1) ? pid1 : pid0;   // (selecting lvalues would put the
+    const int hi = (qi & 1) ? pid3 : pid2;   // four ids in private memory)
+    return (qi & 2) ? hi : lo;
+  };
   auto issue_tile = [&](bf16_t* stage, int k0) {
 #pragma unroll
     for (int i = 0; i < kInstr; ++i) {
@@ -638,9 +486,20 @@ __device__ __forceinline__ void prefill_tile_pipe(
       int kr, kc, vr, vc;
       Lay::k_src(p, kr, kc);
       Lay::v_src(p, vr, vc);
-      dma16(kv.krow(min(k0 + kr, nk - 1)) + kc * 8, stage + 64 * gi * 8);
-      dma16(kv.vrow(min(k0 + vr, nk - 1)) + vc * 8, stage + kPfBN * D + 64 * gi * 8);
+      if constexpr (KV::kPaged) {
+        int kr0, vr0, unused;
+        Lay::k_src(64 * gi, kr0, unused);
+        Lay::v_src(64 * gi, vr0, unused);
+        dma16(kv.k + kv.at(pick(kr0 >> 4), min(k0 + kr, nk - 1) & 15) + kc * 8,
+              stage + 64 * gi * 8);
+        dma16(kv.v + kv.at(pick(vr0 >> 4), min(k0 + vr, nk - 1) & 15) + vc * 8,
+              stage + kPfBN * D + 64 * gi * 8);
+      } else {
+        dma16(kv.krow(min(k0 + kr, nk - 1)) + kc * 8, stage + 64 * gi * 8);
+        dma16(kv.vrow(min(k0 + vr, nk - 1)) + vc * 8, stage + kPfBN * D + 64 * gi * 8);
+      }
     }
+    load_ids(k0 + kPfBN);   // the next tile issued is always the following one
   };
   // Wait until at most `tiles` tiles of this wave's DMA are in flight
   // (vmcnt in bits 3:0 and 15:14; expcnt and lgkmcnt left at their maximum).
@@ -656,6 +515,7 @@ __device__ __forceinline__ void prefill_tile_pipe(
 
   const Lay lay;
   const int nt = rg.n_tiles;
+  if (nt > 0) load_ids(0);
   if (nt > 0) issue_tile(s0, 0);
   // Take delivery of Q here (with tile 0, both needed first): the compiler
   // does not see the DMA, so a first use of Q inside the loop would make it
