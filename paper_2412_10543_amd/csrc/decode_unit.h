@@ -25,14 +25,6 @@
 
 namespace rag {
 
-// Orders LDS traffic between the lanes of one wave (a wave-scope fence plus
-// a scheduling barrier; no workgroup barrier is needed).
-__device__ __forceinline__ void wave_lds_sync() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-}
-
 // Where a unit's result goes.  h0 is the first q head of the group.
 struct DecodeOut {
   bf16_t* o;            // final output row of head h0

@@ -140,26 +140,41 @@ __device__ __forceinline__ void pf_init(PfState<D>& st, const bf16_t* __restrict
   st.l = 0.f;
 }
 
-// Normalise and store this wave's rows and their log-sum-exp.
+// Normalise and store this wave's rows and their log-sum-exp.  The O^T
+// accumulators hold, per lane, one row and scattered groups of four d values,
+// so the tile goes through this wave's 32 x D slice of LDS (16-byte chunk c of
+// row r at chunk c ^ (r mod D/8): the 8-byte writes of a row group and the
+// 16-byte reads of a row touch distinct banks) and leaves as whole rows, each
+// D/8-lane group of a store instruction writing one contiguous row.
 template <int D>
 __device__ __forceinline__ void pf_store(const PfState<D>& st, bf16_t* __restrict__ o,
                                          size_t o_stride, float* __restrict__ lse, int row,
-                                         int nq, float scale) {
-  const int half = (threadIdx.x & 63) >> 5;
+                                         int nq, float scale, bf16_t* __restrict__ stage) {
+  constexpr int kCh = D / 8;                    // 16-byte chunks per row
+  constexpr int kRowsPerInstr = 64 / kCh;       // rows written per store instruction
+  constexpr int kSwz = kCh - 1;
+  const int lane = threadIdx.x & 63;
+  const int half = lane >> 5, r = lane & 31;
   const float lt = st.l + wave_xor(st.l, 32);
   const float inv = lt > 0.f ? 1.f / lt : 0.f;
-  if (row >= nq) return;
-  bf16_t* orow = o + (size_t)row * o_stride;
 #pragma unroll
   for (int dt = 0; dt < D / 32; ++dt)
 #pragma unroll
     for (int g4 = 0; g4 < 4; ++g4) {
-      const int d = 32 * dt + 8 * g4 + 4 * half;
+      const int c = 4 * dt + g4;                // chunk of d = 32*dt + 8*g4 + 4*half
       const bf16x4 w = to_bf16x4(st.oacc[dt][4 * g4] * inv, st.oacc[dt][4 * g4 + 1] * inv,
                                  st.oacc[dt][4 * g4 + 2] * inv, st.oacc[dt][4 * g4 + 3] * inv);
-      *reinterpret_cast<bf16x4*>(orow + d) = w;
+      *reinterpret_cast<bf16x4*>(stage + r * D + 8 * (c ^ (r & kSwz)) + 4 * half) = w;
     }
-  if (lse != nullptr && half == 0)
+  wave_lds_sync();
+  const int r0 = row - r;                       // first row of this wave
+#pragma unroll
+  for (int i = 0; i < 32 / kRowsPerInstr; ++i) {
+    const int rr = kRowsPerInstr * i + lane / kCh, c = lane % kCh;
+    const u32x4 v = *reinterpret_cast<const u32x4*>(stage + rr * D + 8 * (c ^ (rr & kSwz)));
+    if (r0 + rr < nq) *reinterpret_cast<u32x4*>(o + (size_t)(r0 + rr) * o_stride + 8 * c) = v;
+  }
+  if (lse != nullptr && half == 0 && row < nq)
     lse[row] = lt > 0.f ? st.m_used * scale + logf(lt) : -INFINITY;
 }
 
@@ -597,7 +612,11 @@ __device__ __forceinline__ void prefill_tile_pipe(
   // PV of the last block, when this wave computes the whole last tile (its
   // stage is now prev).
   if (nt > 0 && cx.nbw == 2 * nt) pf_pv<D, 1>(st, lay, prev, pO);
-  pf_store(st, o, o_stride, lse, row, nq, scale);
+  // Every tile before the last has been retired by the last barrier, so the
+  // stages other than prev are free: waves 0-3 stage their rows in cur,
+  // waves 4-7 in next (32 x D elements each).
+  static_assert(W <= 8 && 4 * 32 * D <= Lay::kElemsTile, "output staging");
+  pf_store(st, o, o_stride, lse, row, nq, scale, (wave < 4 ? cur : next) + (wave & 3) * 32 * D);
 }
 
 }  // namespace rag
