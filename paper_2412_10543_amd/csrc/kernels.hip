@@ -18,58 +18,88 @@ namespace rag {
 // ---------------------------------------------------------------------------
 // Work order of prefill tiles.  A "stream" is one (sequence, kv head) pair;
 // all q heads of its GQA group and all its query tiles read the same K/V.  A
-// workgroup takes up to four of the group's q heads for one query tile, so
-// each K/V tile it stages in LDS serves all of them.  Stream sigma runs on XCD
-// sigma % 8, so every XCD gets the same mix of sequences (and, with 8 kv
-// heads, exactly one kv head of each).  On an XCD the order is: stream, then
-// query tile from the last (most keys) to the first, then the head groups --
-// the workgroups resident on one XCD at a time share K/V tiles through its L2.
+// workgroup takes up to four of the group's q heads (a head group) and a set
+// of `items` query tiles of one stream, which it runs one after another
+// (prefill_items overlaps each tile's start with the end of the one before).
+// The tiles of a stream are dealt to its `per` workgroups in a snake order --
+// workgroup j takes tiles j, 2*per-1-j, 2*per+j, ... -- so that under the
+// causal mask, where tile t costs t+1 key tiles, every workgroup of a stream
+// gets nearly the same work.  Stream sigma runs on XCD sigma % 8, so every XCD
+// gets the same mix of sequences (and, with 8 kv heads, exactly one kv head
+// of each); on an XCD the workgroups of a stream are consecutive, so those
+// resident at one time share K/V tiles through its L2.
 // ---------------------------------------------------------------------------
+#ifndef RAG_PF_WG_PER_CU
+#define RAG_PF_WG_PER_CU 32
+#endif
+constexpr int kPfWgPerCu = RAG_PF_WG_PER_CU;  // workgroups per CU aimed at (load balance)
+constexpr int kPfCus = 256;
+constexpr int kPfMaxItems = 32;
+
 struct TileCoord {
-  int seq, kvh, head, qt, q0, rows, r0;
+  int seq, kvh, h0, j;
   bool valid;
 };
 
-// Workgroup -> (stream, query tile, head group); wave -> (head, row block).
-template <int W>
+// Workgroup -> (stream, head group, workgroup j of the stream).
 __device__ __forceinline__ TileCoord prefill_coord(int block, int num_streams, int hkv,
-                                                   int group, int n_qt) {
+                                                   int group, int per) {
   const int hw = pf_heads_per_wg(group);
   const int ng = group / hw;
   int xcd, local;
   xcd_slot(block, xcd, local);
   const int hg = local % ng;
   const int rest = local / ng;
-  const int tile_rank = rest % n_qt;
-  const int r = rest / n_qt;
-  const int stream = xcd + kNumXcd * r;
-  const int wave = wave_id();
   TileCoord t;
+  t.j = rest % per;
+  const int stream = xcd + kNumXcd * (rest / per);
   t.valid = stream < num_streams;
   t.seq = stream / hkv;
   t.kvh = stream % hkv;
-  t.head = t.kvh * group + hg * hw + wave % hw;
-  t.qt = n_qt - 1 - tile_rank;
-  t.rows = pf_rows_per_tile(group, W);
-  t.q0 = t.qt * t.rows;
-  t.r0 = t.q0 + kPfRowsPerWave * (wave / hw);
+  t.h0 = t.kvh * group + hg * hw;
   return t;
 }
 
-static int64_t tile_grid(int num_seqs, int hkv, int group, int max_seqlen_q, int waves) {
+// Query tile of item k of workgroup j (snake order over the per workgroups).
+__device__ __forceinline__ int snake_tile(int j, int k, int per) {
+  return (k & 1) ? (k + 1) * per - 1 - j : k * per + j;
+}
+
+// Items per workgroup and workgroups per (stream, head group) for a launch.
+struct PfSplit {
+  int items, per, n_qt;
+};
+static PfSplit pf_split(int num_seqs, int hkv, int group, int max_seqlen_q, bool multi) {
+  const int rows = pf_rows_per_tile(group, kPfWavesDense);
+  PfSplit p;
+  p.n_qt = (max_seqlen_q + rows - 1) / rows;
+  const int64_t streams = (int64_t)num_seqs * hkv * (group / pf_heads_per_wg(group));
+  if (!multi || p.n_qt <= 1) {
+    p.items = 1;
+    p.per = p.n_qt;
+    return p;
+  }
+  const int64_t want = (int64_t)kPfWgPerCu * kPfCus;
+  const int64_t per = std::max<int64_t>(1, (want + streams - 1) / std::max<int64_t>(streams, 1));
+  int items = (int)std::min<int64_t>(kPfMaxItems, (p.n_qt + per - 1) / per);
+  items = std::max(1, items);
+  p.items = items;
+  p.per = (p.n_qt + items - 1) / items;
+  return p;
+}
+
+static int64_t tile_grid(int num_seqs, int hkv, int group, const PfSplit& sp) {
   const int64_t streams = (int64_t)num_seqs * hkv;
   const int64_t per_xcd = (streams + kNumXcd - 1) / kNumXcd;
-  const int rows = pf_rows_per_tile(group, waves);
-  const int64_t n_qt = (max_seqlen_q + rows - 1) / rows;
-  return (int64_t)kNumXcd * per_xcd * n_qt * (group / pf_heads_per_wg(group));
+  return (int64_t)kNumXcd * per_xcd * sp.per * (group / pf_heads_per_wg(group));
 }
 
 int64_t prefill_grid(int num_seqs, int hkv, int group, int max_seqlen_q) {
-  return tile_grid(num_seqs, hkv, group, max_seqlen_q, kPfWavesDense);
+  return tile_grid(num_seqs, hkv, group, pf_split(num_seqs, hkv, group, max_seqlen_q, true));
 }
 
 int64_t paged_prefill_grid(int num_pieces, int hkv, int group, int max_seqlen_q) {
-  return tile_grid(num_pieces, hkv, group, max_seqlen_q, kPfWavesDense);
+  return tile_grid(num_pieces, hkv, group, pf_split(num_pieces, hkv, group, max_seqlen_q, false));
 }
 
 int64_t paged_decode_grid(int num_decode, int hkv, int num_splits) {
@@ -81,7 +111,7 @@ __global__ __launch_bounds__(64 * kPfWavesDense, 2) void prefill_varlen_kernel(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ k,
     const bf16_t* __restrict__ v, bf16_t* __restrict__ o, float* __restrict__ lse,
     const int32_t* __restrict__ cu_q, const int32_t* __restrict__ cu_k, int num_seqs,
-    int hq, int hkv, int n_qt, float scale, int causal) {
+    int hq, int hkv, int items, int per, float scale, int causal) {
   // four K/V stages (separate arrays: the compiler then knows a DMA write to
   // one stage never aliases an LDS read of another)
   __shared__ __attribute__((aligned(16))) bf16_t st0[ChunkLayout<D>::kElemsTile];
@@ -89,20 +119,31 @@ __global__ __launch_bounds__(64 * kPfWavesDense, 2) void prefill_varlen_kernel(
   __shared__ __attribute__((aligned(16))) bf16_t st2[ChunkLayout<D>::kElemsTile];
   __shared__ __attribute__((aligned(16))) bf16_t st3[ChunkLayout<D>::kElemsTile];
   const int group = hq / hkv;
-  const TileCoord tc =
-      prefill_coord<kPfWavesDense>(blockIdx.x, num_seqs * hkv, hkv, group, n_qt);
+  const TileCoord tc = prefill_coord(blockIdx.x, num_seqs * hkv, hkv, group, per);
   if (!tc.valid) return;
   const int qb = cu_q[tc.seq], nq = cu_q[tc.seq + 1] - qb;
   const int kb = cu_k[tc.seq], nk = cu_k[tc.seq + 1] - kb;
-  if (tc.q0 >= nq) return;
+  const int rows = pf_rows_per_tile(group, kPfWavesDense);
+  if (tc.j * rows >= nq) return;
   const int tq = cu_q[num_seqs];
-  const size_t qs = (size_t)hq * D;
+  PfGroup g;
+  g.q = q + ((size_t)qb * hq + tc.h0) * D;
+  g.o = o + ((size_t)qb * hq + tc.h0) * D;
+  g.lse = lse ? lse + (size_t)tc.h0 * tq + qb : nullptr;
+  g.q_stride = (size_t)hq * D;
+  g.lse_stride = (size_t)tq;
+  g.hw = pf_heads_per_wg(group);
+  g.nq = nq;
+  g.nk = nk;
+  g.wg_rows = rows;
+  g.causal = causal;
+  g.scale = scale;
   DenseKV kv{k + ((size_t)kb * hkv + tc.kvh) * D, v + ((size_t)kb * hkv + tc.kvh) * D,
              (size_t)hkv * D};
-  prefill_tile_pipe<D, kPfWavesDense, DenseKV>(
-      q + ((size_t)qb * hq + tc.head) * D, qs, o + ((size_t)qb * hq + tc.head) * D, qs,
-      lse ? lse + (size_t)tc.head * tq + qb : nullptr, kv, nq, nk, tc.q0, tc.rows, tc.r0, scale,
-      causal, st0, st1, st2, st3);
+  const int j = tc.j;
+  prefill_items<D, kPfWavesDense, DenseKV>(
+      g, kv, [j, per, rows](int it) { return snake_tile(j, it, per) * rows; }, items, st0, st1,
+      st2, st3);
 }
 
 // ---------------------------------------------------------------------------
@@ -202,20 +243,30 @@ __global__ __launch_bounds__(64 * kPfWavesDense, 2) void mixed_kernel(PagedKerne
   const bool is_tile = (int64_t)(gi + 1) * tile_groups / groups > tiles_before;
   if (is_tile) {
     const int num_pieces = a.num_seqs - a.num_decode;
-    const TileCoord tc = prefill_coord<kPfWavesDense>(kNumXcd * tiles_before + x,
-                                                      num_pieces * a.hkv, a.hkv, group, a.n_qt);
+    const TileCoord tc = prefill_coord(kNumXcd * tiles_before + x, num_pieces * a.hkv, a.hkv,
+                                       group, a.n_qt);
     if (!tc.valid) return;
     const int s = a.num_decode + tc.seq;
     const int qb = a.cu_q[s], nq = a.cu_q[s + 1] - qb;
-    if (tc.q0 >= nq) return;
-    const int nk = min(a.kv_lens[s], a.max_blocks * 16);
-    const size_t qs = (size_t)a.hq * D;
+    const int rows = pf_rows_per_tile(group, kPfWavesDense);
+    const int q0 = (a.n_qt - 1 - tc.j) * rows;   // tiles with the most keys first
+    if (q0 >= nq) return;
+    PfGroup g;
+    g.q = a.q + ((size_t)qb * a.hq + tc.h0) * D;
+    g.o = a.o + ((size_t)qb * a.hq + tc.h0) * D;
+    g.lse = nullptr;
+    g.q_stride = (size_t)a.hq * D;
+    g.lse_stride = 0;
+    g.hw = pf_heads_per_wg(group);
+    g.nq = nq;
+    g.nk = min(a.kv_lens[s], a.max_blocks * 16);
+    g.wg_rows = rows;
+    g.causal = 1;
+    g.scale = a.scale;
     const PagedDmaKV<D> kv{a.kc + (size_t)tc.kvh * 16 * D, a.vc + (size_t)tc.kvh * 16 * D,
                            a.tables + (size_t)s * a.max_blocks, block_stride};
-    prefill_tile_pipe<D, kPfWavesDense, PagedDmaKV<D>>(
-        a.q + ((size_t)qb * a.hq + tc.head) * D, qs, a.o + ((size_t)qb * a.hq + tc.head) * D, qs,
-        nullptr, kv, nq, nk, tc.q0, tc.rows, tc.r0, a.scale, 1, lds, lds + kE, lds + 2 * kE,
-        lds + 3 * kE);
+    prefill_tile_pipe<D, kPfWavesDense, PagedDmaKV<D>>(g, kv, q0, lds, lds + kE, lds + 2 * kE,
+                                                       lds + 3 * kE);
     return;
   }
   decode_block<D, kMixedDecPages, kPfWavesDense>(a, kNumXcd * (gi - tiles_before) + x, group,
@@ -228,14 +279,14 @@ __global__ __launch_bounds__(64 * kPfWavesDense, 2) void mixed_kernel(PagedKerne
 template <int D>
 static hipError_t launch_prefill_d(const PrefillArgs& a, hipStream_t stream) {
   const int group = a.hq / a.hkv;
-  const int64_t grid = prefill_grid(a.num_seqs, a.hkv, group, a.max_seqlen_q);
+  const PfSplit sp = pf_split(a.num_seqs, a.hkv, group, a.max_seqlen_q, true);
+  const int64_t grid = tile_grid(a.num_seqs, a.hkv, group, sp);
   if (grid == 0) return hipSuccess;
-  const int rows = pf_rows_per_tile(group, kPfWavesDense);
-  const int n_qt = (a.max_seqlen_q + rows - 1) / rows;
   hipLaunchKernelGGL(prefill_varlen_kernel<D>, dim3((unsigned)grid), dim3(64 * kPfWavesDense), 0,
                      stream,
                      (const bf16_t*)a.q, (const bf16_t*)a.k, (const bf16_t*)a.v, (bf16_t*)a.o,
-                     a.lse, a.cu_q, a.cu_k, a.num_seqs, a.hq, a.hkv, n_qt, a.scale, a.causal);
+                     a.lse, a.cu_q, a.cu_k, a.num_seqs, a.hq, a.hkv, sp.items, sp.per, a.scale,
+                     a.causal);
   return hipGetLastError();
 }
 

@@ -122,16 +122,31 @@ struct PfState {
   float m_used, l;
 };
 
+// Q of the items: the rows of waves [4*part, 4*part + 4) of one item fill
+// one stage, wave slot w4 (32 rows x D) at w4 * 32 * D, 16-byte chunk c of
+// row r at chunk c ^ (r mod D/8) (the B-operand reads of 16 rows then hit
+// distinct banks).  Each wave reads its own slot into the Q^T fragments.
+// The lane index is made opaque to the compiler in the helpers used at item
+// boundaries: their per-lane address arithmetic is then recomputed at each
+// use instead of being kept live (or spilled) across the item loop.
+__device__ __forceinline__ int opaque_lane() {
+  int l = threadIdx.x & 63;
+  asm volatile("" : "+v"(l));
+  return l;
+}
+
 template <int D>
-__device__ __forceinline__ void pf_init(PfState<D>& st, const bf16_t* __restrict__ q,
-                                        size_t q_stride, int row, int nq) {
-  const int half = (threadIdx.x & 63) >> 5;
+__device__ __forceinline__ void pf_read_q(PfState<D>& st, const bf16_t* __restrict__ slot) {
+  constexpr int kSwz = D / 8 - 1;
+  const int lane = opaque_lane();
+  const int r = lane & 31, half = lane >> 5;
 #pragma unroll
-  for (int ks = 0; ks < D / 16; ++ks) {
-    u32x4 z = {0, 0, 0, 0};
-    st.qf[ks] =
-        as_bf16x8(row < nq ? load16(q + (size_t)row * q_stride + ks * 16 + half * 8) : z);
-  }
+  for (int ks = 0; ks < D / 16; ++ks)
+    st.qf[ks] = *reinterpret_cast<const bf16x8*>(slot + r * D + 8 * ((2 * ks + half) ^ (r & kSwz)));
+}
+
+template <int D>
+__device__ __forceinline__ void pf_reset(PfState<D>& st) {
 #pragma unroll
   for (int dt = 0; dt < D / 32; ++dt)
 #pragma unroll
@@ -142,38 +157,54 @@ __device__ __forceinline__ void pf_init(PfState<D>& st, const bf16_t* __restrict
 
 // Normalise and store this wave's rows and their log-sum-exp.  The O^T
 // accumulators hold, per lane, one row and scattered groups of four d values,
-// so the tile goes through this wave's 32 x D slice of LDS (16-byte chunk c of
-// row r at chunk c ^ (r mod D/8): the 8-byte writes of a row group and the
-// 16-byte reads of a row touch distinct banks) and leaves as whole rows, each
-// D/8-lane group of a store instruction writing one contiguous row.
+// so the tile goes through this wave's 32 x D/2 slice of LDS, one half of the
+// columns at a time (16-byte chunk c of a half row r at chunk c ^ (r mod
+// D/16)), and leaves as whole half rows, each D/16-lane group of a store
+// instruction writing one contiguous 128-byte (D = 128) piece of a row.
 template <int D>
 __device__ __forceinline__ void pf_store(const PfState<D>& st, bf16_t* __restrict__ o,
-                                         size_t o_stride, float* __restrict__ lse, int row,
-                                         int nq, float scale, bf16_t* __restrict__ stage) {
-  constexpr int kCh = D / 8;                    // 16-byte chunks per row
-  constexpr int kRowsPerInstr = 64 / kCh;       // rows written per store instruction
+                                         size_t o_stride, float* __restrict__ lse, int r0,
+                                         int nq, float scale, bf16_t* __restrict__ slot) {
+  constexpr int kHalf = D / 2;                  // columns per pass
+  constexpr int kCh = kHalf / 8;                // 16-byte chunks per half row
+  constexpr int kRowsPerInstr = 64 / kCh;
   constexpr int kSwz = kCh - 1;
-  const int lane = threadIdx.x & 63;
+  constexpr int kDtHalf = D / 64;               // 32-column tiles per pass
+  const int lane = opaque_lane();
   const int half = lane >> 5, r = lane & 31;
   const float lt = st.l + wave_xor(st.l, 32);
   const float inv = lt > 0.f ? 1.f / lt : 0.f;
 #pragma unroll
-  for (int dt = 0; dt < D / 32; ++dt)
+  for (int hf = 0; hf < 2; ++hf) {
 #pragma unroll
-    for (int g4 = 0; g4 < 4; ++g4) {
-      const int c = 4 * dt + g4;                // chunk of d = 32*dt + 8*g4 + 4*half
-      const bf16x4 w = to_bf16x4(st.oacc[dt][4 * g4] * inv, st.oacc[dt][4 * g4 + 1] * inv,
-                                 st.oacc[dt][4 * g4 + 2] * inv, st.oacc[dt][4 * g4 + 3] * inv);
-      *reinterpret_cast<bf16x4*>(stage + r * D + 8 * (c ^ (r & kSwz)) + 4 * half) = w;
+    for (int dl = 0; dl < kDtHalf; ++dl) {
+      const int dt = hf * kDtHalf + dl;
+#pragma unroll
+      for (int g4 = 0; g4 < 4; ++g4) {
+        const int c = 4 * dl + g4;              // chunk of d = 32*dt + 8*g4 + 4*half in the pass
+        const bf16x4 w = to_bf16x4(st.oacc[dt][4 * g4] * inv, st.oacc[dt][4 * g4 + 1] * inv,
+                                   st.oacc[dt][4 * g4 + 2] * inv, st.oacc[dt][4 * g4 + 3] * inv);
+        *reinterpret_cast<bf16x4*>(slot + r * kHalf + 8 * (c ^ (r & kSwz)) + 4 * half) = w;
+      }
     }
-  wave_lds_sync();
-  const int r0 = row - r;                       // first row of this wave
+    wave_lds_sync();
+    // all reads first (one wait), then the stores of the rows that exist
+    constexpr int kN = 32 / kRowsPerInstr;
+    u32x4 v[kN];
+    const int rl = lane / kCh, c = lane % kCh;
 #pragma unroll
-  for (int i = 0; i < 32 / kRowsPerInstr; ++i) {
-    const int rr = kRowsPerInstr * i + lane / kCh, c = lane % kCh;
-    const u32x4 v = *reinterpret_cast<const u32x4*>(stage + rr * D + 8 * (c ^ (rr & kSwz)));
-    if (r0 + rr < nq) *reinterpret_cast<u32x4*>(o + (size_t)(r0 + rr) * o_stride + 8 * c) = v;
+    for (int i = 0; i < kN; ++i) {
+      const int rr = kRowsPerInstr * i + rl;
+      v[i] = *reinterpret_cast<const u32x4*>(slot + rr * kHalf + 8 * (c ^ (rr & kSwz)));
+    }
+    bf16_t* const ol = o + (size_t)(r0 + rl) * o_stride + hf * kHalf + 8 * c;
+#pragma unroll
+    for (int i = 0; i < kN; ++i)
+      if (r0 + kRowsPerInstr * i + rl < nq)
+        *reinterpret_cast<u32x4*>(ol + (size_t)(kRowsPerInstr * i) * o_stride) = v[i];
+    wave_lds_sync();
   }
+  const int row = r0 + r;
   if (lse != nullptr && half == 0 && row < nq)
     lse[row] = lt > 0.f ? st.m_used * scale + logf(lt) : -INFINITY;
 }
@@ -444,33 +475,59 @@ __device__ __forceinline__ void pf_slot(PfState<D>& st, const ChunkLayout<D>& la
   }
 }
 
-template <int D, int W, class KV>
-__device__ __forceinline__ void prefill_tile_pipe(
-    const bf16_t* __restrict__ q, size_t q_stride, bf16_t* __restrict__ o, size_t o_stride,
-    float* __restrict__ lse, const KV& kv, int nq, int nk, int q0, int wg_rows, int r0,
-    float scale, int causal, bf16_t* __restrict__ s0, bf16_t* __restrict__ s1,
-    bf16_t* __restrict__ s2, bf16_t* __restrict__ s3) {
+// What the items of one workgroup share: the sequence, the GQA head group
+// and the output.  Items are query tiles of that sequence (item k starts at
+// query row q0_of(k)); wave w owns head h0 + w % hw and the 32 rows starting
+// at q0 + 32 * (w / hw) of every item.
+struct PfGroup {
+  const bf16_t* q;     // row 0 of the sequence, head h0
+  bf16_t* o;           // row 0 of the sequence, head h0
+  float* lse;          // [head][row] from head h0, row 0 (null: none)
+  size_t q_stride;     // elements between rows of q and o
+  size_t lse_stride;   // elements between heads of lse
+  int hw;              // q heads per workgroup
+  int nq, nk;          // query rows and keys of the sequence
+  int wg_rows;         // rows of an item (a query tile)
+  int causal;
+  float scale;
+};
+
+// ---------------------------------------------------------------------------
+// The items of one workgroup, one after another, each over the pipelined
+// tile loop above, with the work at an item boundary overlapped:
+//   * the next item's Q (two stages: waves 0-3, waves 4-7) and its first K/V
+//     tile are copied into LDS in the last three tiles of the current item,
+//     each into the stage the current item has just retired (so the HBM
+//     latency of Q is hidden behind the current item's compute);
+//   * the current item's output leaves (through LDS) after the next item's
+//     first tiles have been requested, and is not waited for.
+// Rows past the sequence end are read from its last row (finite data; those
+// rows are never stored).
+// ---------------------------------------------------------------------------
+template <int D, int W, class KV, class Q0Of>
+__device__ __forceinline__ void prefill_items(const PfGroup& g, const KV& kv, const Q0Of& q0_of,
+                                              int n_items, bf16_t* __restrict__ s0,
+                                              bf16_t* __restrict__ s1, bf16_t* __restrict__ s2,
+                                              bf16_t* __restrict__ s3) {
   using Lay = ChunkLayout<D>;
   constexpr int kCh = D / 8;                     // 16-byte chunks per row
   constexpr int kInstr = kPfBN * kCh / (64 * W);  // K (and V) DMA instructions per wave per tile
   static_assert(kInstr >= 1 && (kPfBN * kCh) % (64 * W) == 0, "tile staging layout");
   constexpr int kLoadsPerTile = 2 * kInstr;      // vmcnt events per wave per tile
   static_assert(2 * kLoadsPerTile < 64, "vmcnt range");
+  static_assert(W == 8, "Q staging: two stages of four waves");
+  static_assert(4 * 32 * D == Lay::kElemsTile, "a stage holds the Q rows of four waves");
+  // a Q stage takes as many DMA instructions per wave as a K/V tile
+  static_assert(4 * 32 * kCh == 64 * W * kLoadsPerTile, "Q staging instruction count");
   const int tid = threadIdx.x;
   const int wave = wave_id(), lane = tid & 63;
-  const PfRange rg = pf_range(nq, nk, q0, wg_rows, r0, causal);
-  const int row = r0 + (lane & 31);
-  PfPipeCtx cx;
-  cx.c = scale * kLog2e;
-  cx.nbw = (rg.kend_w + 31) >> 5;
-  cx.lim = causal ? min(nk - 1, row + rg.off) : nk - 1;
-  cx.mlim = causal ? min(nk - 1, r0 + rg.off) : nk - 1;
+  const int nq = g.nq, nk = g.nk;
+  const int rb = wave / g.hw;                    // this wave's row block
+  const int hoff = (wave % g.hw) * D;            // this wave's head
 
-  PfState<D> st;
-  pf_init(st, q, q_stride, row, nq);
-
-  // Instruction i of this wave writes staged chunks [64*gi, 64*gi + 64) of
-  // the K and of the V region, gi = wave*kInstr + i; lane l fetches the
+  // ---- DMA helpers ----------------------------------------------------------
+  // K/V tile: instruction i of this wave writes staged chunks [64*gi, 64*gi +
+  // 64) of the K and of the V region, gi = wave*kInstr + i; lane l fetches the
   // (row, chunk) that staged chunk 64*gi + l holds.  Rows past the sequence
   // end are loaded from its last row (finite data; those keys are masked --
   // the tail slots of a cache page may hold anything).  The 16 rows of one
@@ -494,10 +551,11 @@ __device__ __forceinline__ void prefill_tile_pipe(
     return (qi & 2) ? hi : lo;
   };
   auto issue_tile = [&](bf16_t* stage, int k0) {
+    const int ln = opaque_lane();
 #pragma unroll
     for (int i = 0; i < kInstr; ++i) {
       const int gi = wave * kInstr + i;
-      const int p = 64 * gi + lane;
+      const int p = 64 * gi + ln;
       int kr, kc, vr, vc;
       Lay::k_src(p, kr, kc);
       Lay::v_src(p, vr, vc);
@@ -514,10 +572,25 @@ __device__ __forceinline__ void prefill_tile_pipe(
         dma16(kv.vrow(min(k0 + vr, nk - 1)) + vc * 8, stage + kPfBN * D + 64 * gi * 8);
       }
     }
-    load_ids(k0 + kPfBN);   // the next tile issued is always the following one
+    load_ids(k0 + kPfBN);   // the tile issued next is the following one
   };
-  // Wait until at most `tiles` tiles of this wave's DMA are in flight
-  // (vmcnt in bits 3:0 and 15:14; expcnt and lgkmcnt left at their maximum).
+  // Q rows of waves [4*part, 4*part + 4) of the item starting at row q0 (the
+  // layout pf_read_q expects).
+  auto issue_q = [&](bf16_t* stage, int part, int q0) {
+    const int ln = opaque_lane();
+#pragma unroll
+    for (int i = 0; i < kLoadsPerTile; ++i) {
+      const int gi = wave * kLoadsPerTile + i;
+      const int p = 64 * gi + ln;
+      const int w4 = p / (32 * kCh), rem = p % (32 * kCh);
+      const int r = rem / kCh, c = (rem % kCh) ^ (r & (kCh - 1));
+      const int w = 4 * part + w4;
+      const int qrow = min(q0 + 32 * (w / g.hw) + r, nq - 1);
+      dma16(g.q + (size_t)qrow * g.q_stride + (w % g.hw) * D + 8 * c, stage + 64 * gi * 8);
+    }
+  };
+  // Wait until at most `tiles` DMA jobs (K/V tiles or Q stages) of this wave
+  // are in flight (vmcnt in bits 3:0 and 15:14; expcnt and lgkmcnt at max).
   auto wait_tiles = [](int tiles) {
     constexpr int k1 = kLoadsPerTile, k2 = 2 * kLoadsPerTile;
     if (tiles >= 2)
@@ -527,96 +600,200 @@ __device__ __forceinline__ void prefill_tile_pipe(
     else
       __builtin_amdgcn_s_waitcnt(0x0F70);
   };
+  // Key tiles of the item starting at q0 (the workgroup's last row bounds it).
+  auto item_tiles = [&](int q0) {
+    const int wg_last = min(q0 + g.wg_rows, nq) - 1;
+    const int kend = g.causal ? min(nk, wg_last + (nk - nq) + 1) : nk;
+    return kend > 0 ? (kend + kPfBN - 1) / kPfBN : 0;
+  };
+  // Index of the first item at or after k that has rows, or n_items.
+  auto next_item = [&](int k) {
+#pragma clang loop vectorize(disable) unroll(disable)
+    while (k < n_items && q0_of(k) >= nq) ++k;
+    return k;
+  };
 
   const Lay lay;
-  const int nt = rg.n_tiles;
-  if (nt > 0) load_ids(0);
-  if (nt > 0) issue_tile(s0, 0);
-  // Take delivery of Q here (with tile 0, both needed first): the compiler
-  // does not see the DMA, so a first use of Q inside the loop would make it
-  // wait there for every copy in flight, on every iteration.
-#pragma unroll
-  for (int ks = 0; ks < D / 16; ++ks) asm volatile("" : "+v"(st.qf[ks]));
-  if (nt > 1) issue_tile(s1, kPfBN);
-  if (nt > 2) issue_tile(s2, 2 * kPfBN);
-  wait_tiles(min(nt, 3) - 1);
-  pf_barrier();
-
-  f32x16 sE = {}, sO = {};
-  bf16x8 pE[2] = {}, pO[2] = {};
-  if (cx.nbw > 0) sE = pf_qk<D, 0>(st, lay, s0);
-
-  // Stage roles rotate by one each tile (tile t is in stage t % 4): prev
-  // holds tile t-1 and, once the barrier has retired it, receives tile t+3.
+  PfState<D> st;
   bf16_t* prev = s3;
   bf16_t* cur = s0;
   bf16_t* next = s1;
   bf16_t* after = s2;
-  auto rotate = [&]() {
-    bf16_t* const retired = prev;
-    prev = cur;
-    cur = next;
-    next = after;
-    after = retired;
-  };
-  // Any tile: slots decide per block what to do (first and last blocks,
-  // masks, DMA near the end).
-  auto general_step = [&](int t) {
-    pf_slot<D, 1, 1>(st, lay, cx, 2 * t, sE, sO, pE, pO, cur, prev);
-    wait_tiles(t + 2 < nt ? 1 : 0);
-    pf_barrier();
-    if (t + 3 < nt) issue_tile(prev, (t + 3) * kPfBN);
-    pf_slot<D, 0, 0>(st, lay, cx, 2 * t + 1, sO, sE, pO, pE, next, cur);
-  };
-  // A tile whose two slots are full and unmasked for every wave and whose
-  // DMA is due: straight-line code (a separate loop, so that its values never
-  // meet the general path's at a join, which would cost register copies).
-  auto steady_step = [&](int t) {
-    float sum = pf_full_slot<D, 1, 1>(st, lay, cur, prev, sE, sO, pE, pO, cx.c,
-                                      -st.m_used * cx.c);
-    if (__builtin_expect(wave_any(!(sum <= kPfSumBound)), 0)) sum = pf_reref(st, sE, cx.c, pE);
-    st.l += sum;
-    wait_tiles(1);
-    pf_barrier();
-    issue_tile(prev, (t + 3) * kPfBN);
-    sum = pf_full_slot<D, 0, 0>(st, lay, next, cur, sO, sE, pO, pE, cx.c, -st.m_used * cx.c);
-    if (__builtin_expect(wave_any(!(sum <= kPfSumBound)), 0)) sum = pf_reref(st, sO, cx.c, pO);
-    st.l += sum;
-  };
-  // Steady tiles are [1, t_end): the workgroup's first row block has the
-  // fewest visible keys, so its limits bind every wave.  Tile t needs blocks
-  // up to 2t+2 computed (2t+2 < nbw), keys up to 64t+63 unmasked and the DMA
-  // of tile t+3 to exist.
-  int t_end;
-  {
-    const int kend0 = causal ? min(nk, min(q0 + 32, nq) + rg.off) : nk;
-    const int nbw0 = q0 >= nq ? 0 : (kend0 + 31) >> 5;
-    const int mlim0 = causal ? min(nk - 1, q0 + rg.off) : nk - 1;
-    const int a = nbw0 >= 3 ? (nbw0 - 3) / 2 + 1 : 0;
-    const int b = mlim0 >= 63 ? (mlim0 - 63) / 64 + 1 : 0;
-    t_end = min(min(a, b), nt - 3);
+
+  int k = next_item(0);
+  if (k >= n_items) return;
+  int q0 = q0_of(k);
+  int nt = item_tiles(q0);
+  // ---- first item: Q to s0/s1, tile 0 to s2, tile 1 to s3 -----------------
+  issue_q(s0, 0, q0);
+  issue_q(s1, 1, q0);
+  if (nt > 0) {
+    load_ids(0);
+    issue_tile(s2, 0);
   }
-  int t = 0;
-  for (; t < min(nt, 1); ++t) {
-    general_step(t);
-    rotate();
+  if (nt > 1) issue_tile(s3, kPfBN);
+  wait_tiles(nt > 1 ? 1 : 0);
+  pf_barrier();
+  pf_read_q(st, (wave < 4 ? s0 : s1) + (wave & 3) * 32 * D);
+  pf_barrier();                                  // Q read: s0 free
+  if (nt > 2) issue_tile(s0, 2 * kPfBN);
+  prev = s1;
+  cur = s2;
+  next = s3;
+  after = s0;
+
+  while (true) {
+    // ---- one item -------------------------------------------------------
+    const int r0 = q0 + 32 * rb;
+    const int row = r0 + (lane & 31);
+    const PfRange rg = pf_range(nq, nk, q0, g.wg_rows, r0, g.causal);
+    PfPipeCtx cx;
+    cx.c = g.scale * kLog2e;
+    cx.nbw = (rg.kend_w + 31) >> 5;
+    cx.lim = g.causal ? min(nk - 1, row + rg.off) : nk - 1;
+    cx.mlim = g.causal ? min(nk - 1, r0 + rg.off) : nk - 1;
+    pf_reset(st);
+    const int k_next = next_item(k + 1);
+    const bool has_next = k_next < n_items;
+    const int q0n = has_next ? q0_of(k_next) : 0;
+    const int ntn = has_next ? item_tiles(q0n) : 0;
+    // DMA jobs for the next item, issued as stages retire: 0 = Q of waves
+    // 0-3, 1 = Q of waves 4-7, 2 = its first K/V tile (none if it has no
+    // keys).  Job j goes to the stage that is cur, next, after (j = 0, 1, 2)
+    // once the loop has ended: the stage of tile nt-4+j, retired at tile
+    // nt-3+j, where the loop issues it (jobs whose tile is before 0 are
+    // issued after the loop).  `jobs` counts those issued, for the waits.
+    int jobs = 0;
+    auto issue_job = [&](bf16_t* stage, int j) {
+      if (j < 2)
+        issue_q(stage, j, q0n);
+      else if (ntn > 0) {
+        load_ids(0);
+        issue_tile(stage, 0);
+      } else {
+        return;
+      }
+      ++jobs;
+    };
+
+    f32x16 sE = {}, sO = {};
+    bf16x8 pE[2] = {}, pO[2] = {};
+    if (cx.nbw > 0) sE = pf_qk<D, 0>(st, lay, cur);
+
+    auto rotate = [&]() {
+      bf16_t* const retired = prev;
+      prev = cur;
+      cur = next;
+      next = after;
+      after = retired;
+    };
+    // Any tile: slots decide per block what to do (first and last blocks,
+    // masks, DMA near the end).  Tile t needs tile t+1 in LDS after the
+    // first slot; issued after it are tile t+2 (if any) and the next item's
+    // jobs of the tiles before t.
+    auto general_step = [&](int t) {
+      pf_slot<D, 1, 1>(st, lay, cx, 2 * t, sE, sO, pE, pO, cur, prev);
+      wait_tiles((t + 2 < nt ? 1 : 0) + jobs);
+      pf_barrier();
+      if (t + 3 < nt)
+        issue_tile(prev, (t + 3) * kPfBN);
+      else if (has_next)
+        issue_job(prev, t + 3 - nt);
+      pf_slot<D, 0, 0>(st, lay, cx, 2 * t + 1, sO, sE, pO, pE, next, cur);
+    };
+    // A tile whose two slots are full and unmasked for every wave and whose
+    // DMA is due: straight-line code (a separate loop, so that its values
+    // never meet the general path's at a join, which would cost register
+    // copies).
+    auto steady_step = [&](int t) {
+      float sum = pf_full_slot<D, 1, 1>(st, lay, cur, prev, sE, sO, pE, pO, cx.c,
+                                        -st.m_used * cx.c);
+      if (__builtin_expect(wave_any(!(sum <= kPfSumBound)), 0))
+        sum = pf_reref(st, sE, cx.c, pE);
+      st.l += sum;
+      wait_tiles(1);
+      pf_barrier();
+      issue_tile(prev, (t + 3) * kPfBN);
+      sum = pf_full_slot<D, 0, 0>(st, lay, next, cur, sO, sE, pO, pE, cx.c, -st.m_used * cx.c);
+      if (__builtin_expect(wave_any(!(sum <= kPfSumBound)), 0))
+        sum = pf_reref(st, sO, cx.c, pO);
+      st.l += sum;
+    };
+    // Steady tiles are [1, t_end): the item's first row block has the fewest
+    // visible keys, so its limits bind every wave.  Tile t needs blocks up to
+    // 2t+2 computed (2t+2 < nbw), keys up to 64t+63 unmasked and the DMA of
+    // tile t+3 to exist.
+    int t_end;
+    {
+      const int kend0 = g.causal ? min(nk, min(q0 + 32, nq) + rg.off) : nk;
+      const int nbw0 = (kend0 + 31) >> 5;
+      const int mlim0 = g.causal ? min(nk - 1, q0 + rg.off) : nk - 1;
+      const int a = nbw0 >= 3 ? (nbw0 - 3) / 2 + 1 : 0;
+      const int b = mlim0 >= 63 ? (mlim0 - 63) / 64 + 1 : 0;
+      t_end = min(min(a, b), nt - 3);
+    }
+    int t = 0;
+    for (; t < min(nt, 1); ++t) {
+      general_step(t);
+      rotate();
+    }
+    for (; t < t_end; ++t) {
+      steady_step(t);
+      rotate();
+    }
+    for (; t < nt; ++t) {
+      general_step(t);
+      rotate();
+    }
+    // PV of the last block, when this wave computes the whole last tile (its
+    // stage is now prev).
+    if (nt > 0 && cx.nbw == 2 * nt) pf_pv<D, 1>(st, lay, prev, pO);
+
+    bf16_t* const o_w = g.o + hoff;
+    float* const lse_w = g.lse ? g.lse + (size_t)(wave % g.hw) * g.lse_stride : nullptr;
+    if (!has_next) {
+      // Every tile before the last has been retired by the last barrier:
+      // cur is free for the output.
+      pf_store(st, o_w, g.q_stride, lse_w, r0, nq, g.scale, cur + wave * 16 * D);
+      return;
+    }
+    // ---- item boundary ------------------------------------------------------
+    // The next item's jobs the loop did not issue (those of tiles before 0)
+    // go out now; the stages of tiles before nt-1 were retired by the last
+    // barrier.
+    if (nt < 3) issue_job(cur, 0);
+    if (nt < 2) issue_job(next, 1);
+    if (nt < 1) issue_job(after, 2);
+    wait_tiles(0);
+    pf_barrier();                                // its Q and first tile are in LDS
+    // The Q^T fragments are free (the last product with them is done); the
+    // output accumulators are untouched by the read.
+    pf_read_q(st, (wave < 4 ? cur : next) + (wave & 3) * 32 * D);
+    pf_barrier();                                // Q read, last PV done: cur, next, prev free
+    if (ntn > 1) issue_tile(prev, kPfBN);
+    if (ntn > 2) issue_tile(next, 2 * kPfBN);
+    pf_store(st, o_w, g.q_stride, lse_w, r0, nq, g.scale, cur + wave * 16 * D);
+    // next item's stages: tile 0 in after, tile 1 in prev, tile 2 in next;
+    // cur (the output staging) receives tile 3.
+    bf16_t* const st_out = cur;
+    cur = after;
+    after = next;
+    next = prev;
+    prev = st_out;
+    k = k_next;
+    q0 = q0n;
+    nt = ntn;
   }
-  for (; t < t_end; ++t) {
-    steady_step(t);
-    rotate();
-  }
-  for (; t < nt; ++t) {
-    general_step(t);
-    rotate();
-  }
-  // PV of the last block, when this wave computes the whole last tile (its
-  // stage is now prev).
-  if (nt > 0 && cx.nbw == 2 * nt) pf_pv<D, 1>(st, lay, prev, pO);
-  // Every tile before the last has been retired by the last barrier, so the
-  // stages other than prev are free: waves 0-3 stage their rows in cur,
-  // waves 4-7 in next (32 x D elements each).
-  static_assert(W <= 8 && 4 * 32 * D <= Lay::kElemsTile, "output staging");
-  pf_store(st, o, o_stride, lse, row, nq, scale, (wave < 4 ? cur : next) + (wave & 3) * 32 * D);
+}
+
+// One query tile (a single item), for the chunked-prefill pieces of the mixed
+// launch.
+template <int D, int W, class KV>
+__device__ __forceinline__ void prefill_tile_pipe(const PfGroup& g, const KV& kv, int q0,
+                                                  bf16_t* __restrict__ s0, bf16_t* __restrict__ s1,
+                                                  bf16_t* __restrict__ s2,
+                                                  bf16_t* __restrict__ s3) {
+  prefill_items<D, W, KV>(g, kv, [q0](int) { return q0; }, 1, s0, s1, s2, s3);
 }
 
 }  // namespace rag
