@@ -139,6 +139,26 @@ __device__ __forceinline__ void dma16(const void* src, bf16_t* lds_dst) {
       : "memory");
 }
 
+// The same copy with a wave-uniform 64-bit base in SGPRs plus a per-lane
+// 32-bit byte offset (the global instruction's SADDR form): no per-lane 64-bit
+// address arithmetic.  (The instruction's immediate offset would move the LDS
+// destination too, so it stays 0.)
+__device__ __forceinline__ void dma16_s(const void* sbase, uint32_t voff, bf16_t* lds_dst) {
+  typedef __attribute__((address_space(3))) char lds_char;
+  const uint32_t base =
+      __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lds_char*)lds_dst);
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %3\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, %2\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(voff), "s"(sbase), "s"(base)
+      : "memory");
+}
+
 __device__ __forceinline__ bf16x8 join_bf16x8(i16x4 lo, i16x4 hi) {
   typedef short i16x8 __attribute__((ext_vector_type(8)));
   i16x8 v = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);

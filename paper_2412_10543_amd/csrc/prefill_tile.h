@@ -550,7 +550,35 @@ __device__ __forceinline__ void prefill_items(const PfGroup& g, const KV& kv, co
     const int hi = (qi & 1) ? pid3 : pid2;   // four ids in private memory)
     return (qi & 2) ? hi : lo;
   };
+  // Full tiles of dense K/V: per-lane byte offsets of the first instruction,
+  // computed once; instruction i then adds 64*i bytes (K) or 16*i rows (V),
+  // folded into the scalar base.  (The pattern holds for D = 64 and
+  // 128 with eight waves: the chunks of instruction i are those of
+  // instruction 0 moved by four chunks of the same rows (K) or by 16 rows (V).)
+  uint32_t k_off0 = 0, v_off0 = 0;
+  if constexpr (!KV::kPaged) {
+    int kr, kc, vr, vc;
+    Lay::k_src(64 * wave * kInstr + lane, kr, kc);
+    Lay::v_src(64 * wave * kInstr + lane, vr, vc);
+    k_off0 = (uint32_t)((kr * kv.stride + kc * 8) * sizeof(bf16_t));
+    v_off0 = (uint32_t)((vr * kv.stride + vc * 8) * sizeof(bf16_t));
+  }
   auto issue_tile = [&](bf16_t* stage, int k0) {
+    if constexpr (!KV::kPaged) {
+      if (k0 + kPfBN <= nk) {
+        const bf16_t* kb = kv.krow(k0);
+        const bf16_t* vb = kv.vrow(k0);
+        static_assert(kInstr == 1 || kInstr == 2, "full-tile copy");
+        const int g0 = wave * kInstr;
+        dma16_s(kb, k_off0, stage + 64 * g0 * 8);
+        dma16_s(vb, v_off0, stage + kPfBN * D + 64 * g0 * 8);
+        if constexpr (kInstr == 2) {
+          dma16_s(kb + 32, k_off0, stage + 64 * (g0 + 1) * 8);    // 64 bytes on
+          dma16_s(vb + (size_t)16 * kv.stride, v_off0, stage + kPfBN * D + 64 * (g0 + 1) * 8);
+        }
+        return;
+      }
+    }
     const int ln = opaque_lane();
 #pragma unroll
     for (int i = 0; i < kInstr; ++i) {
