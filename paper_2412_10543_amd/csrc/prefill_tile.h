@@ -555,29 +555,52 @@ __device__ __forceinline__ void prefill_items(const PfGroup& g, const KV& kv, co
   // folded into the scalar base.  (The pattern holds for D = 64 and
   // 128 with eight waves: the chunks of instruction i are those of
   // instruction 0 moved by four chunks of the same rows (K) or by 16 rows (V).)
+  // For a paged cache the rows of one instruction are the 16 slots of one
+  // page, so the per-lane offset is within the page (slot r % 16) and the
+  // page's base is the scalar part.
+  static_assert(kInstr == 1 || kInstr == 2, "full-tile copy");
   uint32_t k_off0 = 0, v_off0 = 0;
-  if constexpr (!KV::kPaged) {
+  {
     int kr, kc, vr, vc;
     Lay::k_src(64 * wave * kInstr + lane, kr, kc);
     Lay::v_src(64 * wave * kInstr + lane, vr, vc);
-    k_off0 = (uint32_t)((kr * kv.stride + kc * 8) * sizeof(bf16_t));
-    v_off0 = (uint32_t)((vr * kv.stride + vc * 8) * sizeof(bf16_t));
+    if constexpr (KV::kPaged) {
+      k_off0 = (uint32_t)(((kr & 15) * D + kc * 8) * sizeof(bf16_t));
+      v_off0 = (uint32_t)(((vr & 15) * D + vc * 8) * sizeof(bf16_t));
+    } else {
+      k_off0 = (uint32_t)((kr * kv.stride + kc * 8) * sizeof(bf16_t));
+      v_off0 = (uint32_t)((vr * kv.stride + vc * 8) * sizeof(bf16_t));
+    }
   }
   auto issue_tile = [&](bf16_t* stage, int k0) {
-    if constexpr (!KV::kPaged) {
-      if (k0 + kPfBN <= nk) {
+    if (k0 + kPfBN <= nk) {
+      const int g0 = wave * kInstr;
+      if constexpr (KV::kPaged) {
+        // K rows of instruction 1 are those of instruction 0 (64 bytes on);
+        // V rows of instruction i are rows 16*i on (the next page).
+        int kr0, vr0, unused;
+        Lay::k_src(64 * g0, kr0, unused);
+        Lay::v_src(64 * g0, vr0, unused);
+        const bf16_t* kb = kv.k + kv.at(pick(kr0 >> 4), 0);
+        dma16_s(kb, k_off0, stage + 64 * g0 * 8);
+        dma16_s(kv.v + kv.at(pick(vr0 >> 4), 0), v_off0, stage + kPfBN * D + 64 * g0 * 8);
+        if constexpr (kInstr == 2) {
+          dma16_s(kb + 32, k_off0, stage + 64 * (g0 + 1) * 8);
+          dma16_s(kv.v + kv.at(pick((vr0 >> 4) + 1), 0), v_off0,
+                  stage + kPfBN * D + 64 * (g0 + 1) * 8);
+        }
+        load_ids(k0 + kPfBN);
+      } else {
         const bf16_t* kb = kv.krow(k0);
         const bf16_t* vb = kv.vrow(k0);
-        static_assert(kInstr == 1 || kInstr == 2, "full-tile copy");
-        const int g0 = wave * kInstr;
         dma16_s(kb, k_off0, stage + 64 * g0 * 8);
         dma16_s(vb, v_off0, stage + kPfBN * D + 64 * g0 * 8);
         if constexpr (kInstr == 2) {
           dma16_s(kb + 32, k_off0, stage + 64 * (g0 + 1) * 8);    // 64 bytes on
           dma16_s(vb + (size_t)16 * kv.stride, v_off0, stage + kPfBN * D + 64 * (g0 + 1) * 8);
         }
-        return;
       }
+      return;
     }
     const int ln = opaque_lane();
 #pragma unroll
