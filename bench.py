@@ -410,7 +410,7 @@ def main():
                      kernel="prefill_varlen_kernel<128>")
     rl_dec = roofline("hbm", dec_gbs, PEAK_HBM_GBS, "GB/s",
                       traffic=stored_traffic("paged_kernel"),
-                      kernel="paged_kernel<128,false> (rag_attn_decode_paged)")
+                      kernel="paged_decode_kernel<128> (rag_attn_decode_paged)")
     dominant = rl_dec if dec_total > pf_avg else rl_pf
 
     res = {
