@@ -281,6 +281,46 @@ def bench_phase_mixed(torch, dev, reps):
     return out
 
 
+def bench_phase_kv_write(torch, dev, reps):
+    """Paged KV-cache write of the stuff7b prompt tokens (what a prefill hands
+    to decode) and of one decode step (one token per sequence), into a pool of
+    randomly permuted pages.  HBM-bound copy: bytes = K and V read once and
+    written once, plus the slot mapping."""
+    import numpy as np
+
+    from paper_2412_10543_amd import binding
+    from paper_2412_10543_amd.workloads import normal_bf16, stuff7b
+    w = stuff7b()
+    cu, _ = binding.rag_plan_prompts(w.method, w.query_lens, w.num_chunks, w.chunk_len,
+                                     w.intermediate_length, w.answer_len)
+    T = cu[-1]
+    nblocks = int(math.ceil(T / 16 * 1.25))
+    out = {}
+    for name, ntok in (("prompt_tokens", T), ("decode_step", len(cu) - 1)):
+        rng = np.random.Generator(np.random.PCG64(17))
+        slots = torch.tensor(rng.permutation(nblocks * 16)[:ntok].astype(np.int32), device=dev)
+        k = normal_bf16((ntok, w.hkv, w.d), 31, dev)
+        v = normal_bf16((ntok, w.hkv, w.d), 32, dev)
+        kc = torch.empty((nblocks, w.hkv, 16, w.d), dtype=torch.bfloat16, device=dev)
+        vc = torch.empty_like(kc)
+        binding.rag_kv_cache_write(k, v, kc, vc, slots)
+        torch.cuda.synchronize()
+        timer = Timer(torch)
+        for _ in range(reps):
+            timer.start("w")
+            binding.rag_kv_cache_write(k, v, kc, vc, slots)
+            timer.stop("w")
+        torch.cuda.synchronize()
+        ms = median(timer.ms("w"))
+        nbytes = 2.0 * 2 * ntok * w.hkv * w.d * 2 + 4 * ntok
+        gbs = nbytes / ms / 1e6
+        out[name] = {"tokens": ntok, "us": round(ms * 1e3, 2), "gbs": round(gbs, 1),
+                     "frac_hbm": round(gbs / PEAK_HBM_GBS, 4)}
+        del k, v, kc, vc
+    torch.cuda.empty_cache()
+    return out
+
+
 # ---------------------------------------------------------------------------
 # CPU baseline: the oracle on a bounded sample of the same workload
 # ---------------------------------------------------------------------------
@@ -438,6 +478,7 @@ def main():
         for fn in (mapred7b, long70b):
             phases[fn.__name__] = bench_phase_stuff(torch, fn(), dev, args.extra_reps)
         phases["mixed"] = bench_phase_mixed(torch, dev, args.extra_reps)
+        phases["kv_write"] = bench_phase_kv_write(torch, dev, max(args.extra_reps, 10))
         res["phases"] = phases
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(torch, st)

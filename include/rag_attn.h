@@ -178,6 +178,37 @@ rag_status rag_attn_decode_paged(const void *q, const void *k_cache,
                                  void *workspace, size_t workspace_bytes,
                                  hipStream_t stream);
 
+/*
+ * Paged KV-cache write: store the keys and values of a batch of new tokens in
+ * the paged cache that rag_attn_decode_paged reads.  The serving engine the
+ * paper builds on (Sec. "Implementation": vLLM, with its paged KV cache) keeps
+ * each token's K/V in 16-token pages; a token's slot is page * 16 + offset.
+ * A prefill writes its prompt tokens this way, so that decode can start on
+ * the pages with no host-side re-layout; each decode step writes one token
+ * per sequence.
+ *
+ *   k, v     device [num_tokens, num_kv_heads, head_dim]: the new tokens
+ *            (for a prefill, the packed K and V given to
+ *            rag_attn_prefill_varlen).
+ *   k_cache, v_cache  device [num_blocks, num_kv_heads, block_size,
+ *            head_dim]: token t's row of kv head h is written to
+ *            cache[slot / 16][h][slot % 16][:]; nothing else changes.
+ *   slot_mapping  device int32 [num_tokens]: slot of each token; a negative
+ *            slot skips the token (padding).  Precondition: slots are below
+ *            num_blocks * block_size and no two tokens share a slot (both
+ *            checked when RAG_ATTN_CHECK=1).
+ *   block_size  must be 16; head_dim 64 or 128.
+ *
+ * Returns RAG_OK (num_tokens == 0 is a no-op), RAG_ERR_INVALID_ARG (null or
+ * misaligned pointer, negative size, num_kv_heads <= 0, violated precondition
+ * in debug mode), RAG_ERR_UNSUPPORTED (head_dim, block_size) or RAG_ERR_HIP.
+ */
+rag_status rag_kv_cache_write(const void *k, const void *v, void *k_cache,
+                              void *v_cache, const int32_t *slot_mapping,
+                              int32_t num_tokens, int32_t num_kv_heads,
+                              int32_t head_dim, int32_t block_size,
+                              int32_t num_blocks, hipStream_t stream);
+
 /* Synthesis methods (Sec. "RAG systems and configurations"). */
 typedef enum {
   RAG_STUFF = 0,             /* one prompt: all chunks, then the query       */

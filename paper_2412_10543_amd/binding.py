@@ -46,7 +46,7 @@ _lib = None
 def exported_symbols():
     return ["rag_abi_version", "rag_last_error", "rag_attn_prefill_varlen",
             "rag_attn_decode_num_splits", "rag_attn_decode_workspace_size",
-            "rag_attn_decode_paged", "rag_plan_prompts"]
+            "rag_attn_decode_paged", "rag_kv_cache_write", "rag_plan_prompts"]
 
 
 def lib():
@@ -71,6 +71,8 @@ def lib():
     L.rag_attn_decode_paged.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _i32, _i32, _i32,
                                         _i32, _i32, _i32, _i32, _i32, _i32, ctypes.c_float,
                                         _i32, _vp, ctypes.c_size_t, _vp]
+    L.rag_kv_cache_write.restype = ctypes.c_int
+    L.rag_kv_cache_write.argtypes = [_vp, _vp, _vp, _vp, _vp, _i32, _i32, _i32, _i32, _i32, _vp]
     L.rag_plan_prompts.restype = ctypes.c_int
     L.rag_plan_prompts.argtypes = [ctypes.c_int, _i32, _i32p, _i32p, _i32, _i32, _i32, _i32p,
                                    _i32, _i32p, _i32p]
@@ -172,6 +174,19 @@ def rag_attn_decode_paged(q, k_cache, v_cache, o, block_tables, kv_lens, softmax
         int(max_seqlen_q), k_cache.shape[0], q.shape[1], k_cache.shape[1], q.shape[2],
         k_cache.shape[2], float(softmax_scale), int(num_splits), _ptr(workspace), ws_bytes,
         _stream(stream)))
+
+
+def rag_kv_cache_write(k, v, k_cache, v_cache, slot_mapping, stream=None) -> None:
+    """k, v [T, Hkv, d] bf16; caches [num_blocks, Hkv, 16, d] bf16; slot_mapping
+    int32 [T] on the GPU (negative = skip)."""
+    for t, n in ((k, "k"), (v, "v")):
+        _need(t, torch.bfloat16, n, 3)
+    for t, n in ((k_cache, "k_cache"), (v_cache, "v_cache")):
+        _need(t, torch.bfloat16, n, 4)
+    _need(slot_mapping, torch.int32, "slot_mapping", 1)
+    _check(lib().rag_kv_cache_write(
+        _ptr(k), _ptr(v), _ptr(k_cache), _ptr(v_cache), _ptr(slot_mapping), k.shape[0],
+        k.shape[1], k.shape[2], k_cache.shape[2], k_cache.shape[0], _stream(stream)))
 
 
 def rag_plan_prompts(method, query_len, num_chunks, chunk_len, intermediate_length=0,

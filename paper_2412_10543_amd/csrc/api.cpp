@@ -293,6 +293,46 @@ rag_status rag_attn_decode_paged(const void* q, const void* k_cache, const void*
   return ok();
 }
 
+rag_status rag_kv_cache_write(const void* k, const void* v, void* k_cache, void* v_cache,
+                              const int32_t* slot_mapping, int32_t num_tokens,
+                              int32_t num_kv_heads, int32_t head_dim, int32_t block_size,
+                              int32_t num_blocks, hipStream_t stream) {
+  if (num_tokens < 0 || num_blocks < 0)
+    return fail(RAG_ERR_INVALID_ARG, "kv write: negative size");
+  if (num_kv_heads <= 0) return fail(RAG_ERR_INVALID_ARG, "kv write: num_kv_heads must be > 0");
+  if (head_dim != 64 && head_dim != 128)
+    return fail(RAG_ERR_UNSUPPORTED, "kv write: head_dim %d (supported: 64, 128)", head_dim);
+  if (block_size != kBlock)
+    return fail(RAG_ERR_UNSUPPORTED, "kv write: block_size %d (supported: 16)", block_size);
+  if (num_tokens == 0) return ok();
+  if (!k || !v || !k_cache || !v_cache || !slot_mapping)
+    return fail(RAG_ERR_INVALID_ARG, "kv write: null pointer argument");
+  if (!aligned16(k) || !aligned16(v) || !aligned16(k_cache) || !aligned16(v_cache))
+    return fail(RAG_ERR_INVALID_ARG, "kv write: k/v/k_cache/v_cache must be 16-byte aligned");
+  if (rag::kv_cache_write_grid(num_tokens, num_kv_heads, head_dim) > INT_MAX)
+    return fail(RAG_ERR_UNSUPPORTED, "kv write: batch too large for one grid");
+  if (check_mode()) {
+    std::vector<int32_t> sl;
+    if (!fetch(sl, slot_mapping, (size_t)num_tokens, stream))
+      return fail(RAG_ERR_HIP, "kv write: debug copy of slot_mapping failed");
+    const int64_t slots = (int64_t)num_blocks * kBlock;
+    std::vector<char> seen((size_t)slots, 0);
+    for (int32_t t = 0; t < num_tokens; ++t) {
+      const int32_t s = sl[t];
+      if (s < 0) continue;
+      if (s >= slots)
+        return fail(RAG_ERR_INVALID_ARG, "kv write: slot_mapping[%d] = %d outside [0, %lld)", t, s,
+                    (long long)slots);
+      if (seen[(size_t)s]++)
+        return fail(RAG_ERR_INVALID_ARG, "kv write: slot %d is written by two tokens", s);
+    }
+  }
+  rag::KvWriteArgs a{k, v, k_cache, v_cache, slot_mapping, num_tokens, num_kv_heads, head_dim};
+  const hipError_t e = rag::launch_kv_cache_write(a, stream);
+  if (e != hipSuccess) return fail(RAG_ERR_HIP, "kv write launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
 rag_status rag_plan_prompts(rag_synthesis method, int32_t num_queries, const int32_t* query_len,
                             const int32_t* num_chunks, int32_t chunk_len,
                             int32_t intermediate_length, int32_t answer_len,

@@ -1,0 +1,55 @@
+// Paged KV-cache write for gfx950: the K and V rows of a batch of new tokens
+// (a prefill's prompt tokens, or one decode token per sequence) are copied to
+// their slots in the paged cache, slot = page * 16 + offset, so that prefill
+// output reaches the cache without any host-side re-layout.
+//
+// HBM-bound copy.  Thread i moves one 16-byte chunk of one (token, kv head)
+// row of K and the same chunk of V: the D/8 threads of a row read it
+// contiguously from the packed [T, Hkv, D] input and write it contiguously
+// into the 16-slot page of that kv head (a row of D bf16 values is the unit
+// the cache stores contiguously).
+#include "common.h"
+#include "launch.h"
+
+namespace rag {
+
+template <int D>
+__global__ __launch_bounds__(256) void kv_cache_write_kernel(
+    const bf16_t* __restrict__ k, const bf16_t* __restrict__ v, bf16_t* __restrict__ kc,
+    bf16_t* __restrict__ vc, const int32_t* __restrict__ slots, int64_t num_tokens, int hkv) {
+  constexpr int kCh = D / 8;                       // 16-byte chunks per row
+  const int64_t per_token = (int64_t)hkv * kCh;
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= num_tokens * per_token) return;
+  const int64_t t = i / per_token;
+  const int rem = (int)(i - t * per_token);
+  const int h = rem / kCh, c = rem % kCh;
+  const int slot = slots[t];
+  if (slot < 0) return;                            // padding token
+  const size_t src = ((size_t)t * hkv + h) * D + c * 8;
+  const size_t dst = (((size_t)(slot >> 4) * hkv + h) * 16 + (slot & 15)) * D + c * 8;
+  const u32x4 kx = load16(k + src);
+  const u32x4 vx = load16(v + src);
+  *reinterpret_cast<u32x4*>(kc + dst) = kx;
+  *reinterpret_cast<u32x4*>(vc + dst) = vx;
+}
+
+int64_t kv_cache_write_grid(int64_t num_tokens, int hkv, int d) {
+  return (num_tokens * hkv * (d / 8) + 255) / 256;
+}
+
+hipError_t launch_kv_cache_write(const KvWriteArgs& a, hipStream_t stream) {
+  const int64_t grid = kv_cache_write_grid(a.num_tokens, a.hkv, a.d);
+  if (grid == 0) return hipSuccess;
+  if (a.d == 64)
+    hipLaunchKernelGGL(kv_cache_write_kernel<64>, dim3((unsigned)grid), dim3(256), 0, stream,
+                       (const bf16_t*)a.k, (const bf16_t*)a.v, (bf16_t*)a.k_cache,
+                       (bf16_t*)a.v_cache, a.slots, a.num_tokens, a.hkv);
+  else
+    hipLaunchKernelGGL(kv_cache_write_kernel<128>, dim3((unsigned)grid), dim3(256), 0, stream,
+                       (const bf16_t*)a.k, (const bf16_t*)a.v, (bf16_t*)a.k_cache,
+                       (bf16_t*)a.v_cache, a.slots, a.num_tokens, a.hkv);
+  return hipGetLastError();
+}
+
+}  // namespace rag

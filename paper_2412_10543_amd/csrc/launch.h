@@ -35,6 +35,16 @@ struct PagedArgs {
   int* arrivals;
 };
 
+struct KvWriteArgs {
+  const void* k;                // [num_tokens, hkv, d]
+  const void* v;
+  void* k_cache;                // [num_blocks, hkv, 16, d]
+  void* v_cache;
+  const int32_t* slots;         // [num_tokens]
+  int64_t num_tokens;
+  int hkv, d;
+};
+
 // Launch-grid sizes, exposed so the host can check them before launching.
 int64_t prefill_grid(int num_seqs, int hkv, int group, int max_seqlen_q);
 int64_t paged_prefill_grid(int num_pieces, int hkv, int group, int max_seqlen_q);
@@ -42,5 +52,7 @@ int64_t paged_decode_grid(int num_decode, int hkv, int num_splits);
 
 hipError_t launch_prefill_varlen(const PrefillArgs& a, hipStream_t stream);
 hipError_t launch_paged(const PagedArgs& a, hipStream_t stream);
+int64_t kv_cache_write_grid(int64_t num_tokens, int hkv, int d);
+hipError_t launch_kv_cache_write(const KvWriteArgs& a, hipStream_t stream);
 
 }  // namespace rag

@@ -106,6 +106,31 @@ def test_decode_validation(kw, status):
     assert _decode(**kw) == status
 
 
+def _kv_write(**kw):
+    a = dict(k=FAKE, v=FAKE, kc=FAKE, vc=FAKE, slots=FAKE, T=16, hkv=8, d=128, bs=16,
+             num_blocks=100)
+    a.update(kw)
+    return binding.lib().rag_kv_cache_write(a["k"], a["v"], a["kc"], a["vc"], a["slots"], a["T"],
+                                            a["hkv"], a["d"], a["bs"], a["num_blocks"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(k=None), binding.RAG_ERR_INVALID_ARG),
+    (dict(slots=None), binding.RAG_ERR_INVALID_ARG),
+    (dict(vc=FAKE + 8), binding.RAG_ERR_INVALID_ARG),
+    (dict(T=-1), binding.RAG_ERR_INVALID_ARG),
+    (dict(num_blocks=-1), binding.RAG_ERR_INVALID_ARG),
+    (dict(hkv=0), binding.RAG_ERR_INVALID_ARG),
+    (dict(d=96), binding.RAG_ERR_UNSUPPORTED),
+    (dict(bs=8), binding.RAG_ERR_UNSUPPORTED),
+    (dict(T=0, k=None, slots=None), binding.RAG_OK),          # nothing to write
+])
+def test_kv_write_validation(kw, status):
+    assert _kv_write(**kw) == status
+    if status != binding.RAG_OK:
+        assert binding.rag_last_error().startswith("kv write")
+
+
 def test_split_policy():
     ns = binding.rag_attn_decode_num_splits
     # one split never needs a workspace
