@@ -54,6 +54,8 @@ extern "C" {
 #define RAG_ATTN_ABI_VERSION 1
 
 typedef enum {
+  RAG_NO_FIT = 1,           /* rag_choose_config: no configuration fits in the
+                               available memory; the request waits            */
   RAG_OK = 0,
   RAG_ERR_INVALID_ARG = -1, /* null pointer, negative size, bad enum, bad alignment,
                                violated precondition (debug mode)              */
@@ -245,6 +247,90 @@ rag_status rag_plan_prompts(rag_synthesis method, int32_t num_queries,
                             int32_t answer_len, int32_t *cu_seqlens_out,
                             int32_t capacity, int32_t *num_seqs_out,
                             int32_t *decode_len_out);
+
+/*
+ * Configuration planner (host only).  A query's profile -- estimated by an LLM
+ * in the paper, given here -- is pruned to a space of configurations
+ * (Algorithm 1, Sec. "Mapping query profiles to RAG configurations"); one
+ * configuration of that space is then chosen from the GPU memory available
+ * for the current batch (Sec. "Joint configuration-scheduling adaptation").
+ */
+typedef struct {
+  int32_t complexity_high;   /* query complexity: 1 = "High", 0 = "Low"          */
+  int32_t joint_reasoning;   /* joint reasoning required: 1 = "Yes", 0 = "No"    */
+  int32_t pieces;            /* pieces of information required (paper: 1-10)    */
+  int32_t summary_len_min;   /* length range of the summaries, tokens           */
+  int32_t summary_len_max;   /*   (paper: 30-200)                               */
+} rag_query_profile;
+
+typedef struct {
+  uint32_t methods;          /* bit (1u << m) for each allowed method m: RAG_STUFF,
+                                RAG_MAP_REDUCE_MAP (a map_reduce configuration)
+                                or RAG_MAP_RERANK                               */
+  int32_t num_chunks_min, num_chunks_max;
+  int32_t intermediate_length_min, intermediate_length_max;
+} rag_config_space;
+
+typedef struct {
+  int32_t query_len;         /* tokens of the query                             */
+  int32_t chunk_len;         /* tokens per retrieved chunk                      */
+  int32_t answer_len;        /* tokens an answer-producing call generates       */
+  int64_t kv_bytes_per_token;/* K and V of one token over all layers, as held
+                                by this GPU (model shape x bytes per element)   */
+} rag_request_shape;
+
+typedef struct {
+  int32_t method;            /* RAG_STUFF, RAG_MAP_REDUCE_MAP or RAG_MAP_RERANK; -1
+                                when nothing fits                                */
+  int32_t num_chunks;
+  int32_t intermediate_length;  /* 0 unless map_reduce                          */
+  int32_t fallback;          /* 1: chosen outside the pruned space (none fitted) */
+  int64_t kv_bytes;          /* memory requirement, 2% buffer included          */
+} rag_config;
+
+/*
+ * Algorithm 1: no joint reasoning -> {map_rerank}; joint reasoning with low
+ * complexity -> {stuff}; with high complexity -> {stuff, map_reduce};
+ * num_chunks in [pieces, 3 * pieces]; intermediate_length in the summary range.
+ * Returns RAG_OK or RAG_ERR_INVALID_ARG (null pointer; flags not 0/1; pieces
+ * < 1; empty or non-positive summary range).
+ */
+rag_status rag_prune_config_space(const rag_query_profile *profile,
+                                  rag_config_space *space);
+
+/*
+ * KV-cache memory requirement of one configuration, in bytes, with the
+ * paper's 2% buffer: tokens * kv_bytes_per_token * 1.02, rounded up.  A call
+ * holds its prompt and the tokens it generates.  stuff: one call of
+ * num_chunks * chunk_len + query_len prompt tokens; map_rerank: num_chunks
+ * calls of chunk_len + query_len, run together; map_reduce: the larger of its
+ * num_chunks mappers (chunk_len + query_len prompt, intermediate_length
+ * summary tokens each) and its reduce call (num_chunks * intermediate_length
+ * + query_len).  -1 for an invalid argument.
+ */
+int64_t rag_config_kv_bytes(int32_t method, int32_t num_chunks,
+                            int32_t intermediate_length,
+                            const rag_request_shape *shape);
+
+/*
+ * Best-fit choice: among the configurations of the pruned space that can
+ * start in available_bytes -- stuff and map_rerank when their whole
+ * requirement fits, map_reduce when its largest single call fits (its mappers
+ * enter the running batch as memory allows) -- the one with the highest
+ * requirement; ties go to more chunks, then a longer intermediate length,
+ * then stuff, map_reduce, map_rerank in that order.  If none fits, a cheaper
+ * configuration just outside the space: stuff (joint reasoning) or
+ * map_rerank (otherwise) with as many chunks as fit (fallback = 1).  Returns
+ * RAG_OK, RAG_NO_FIT (not even one chunk fits: the request waits; *out has
+ * method -1) or RAG_ERR_INVALID_ARG.
+ */
+rag_status rag_choose_config(const rag_query_profile *profile,
+                             const rag_request_shape *shape,
+                             int64_t available_bytes, rag_config *out);
+
+/* Free and total memory of the current HIP device (hipMemGetInfo), the input
+ * of rag_choose_config's available_bytes.  RAG_OK or RAG_ERR_HIP. */
+rag_status rag_device_free_memory(size_t *free_bytes, size_t *total_bytes);
 
 #ifdef __cplusplus
 }

@@ -17,6 +17,7 @@ import torch
 
 LIBRARY = os.path.join(os.path.dirname(os.path.abspath(__file__)), "librag_attn.so")
 
+RAG_NO_FIT = 1
 RAG_OK = 0
 RAG_ERR_INVALID_ARG = -1
 RAG_ERR_UNSUPPORTED = -2
@@ -46,7 +47,32 @@ _lib = None
 def exported_symbols():
     return ["rag_abi_version", "rag_last_error", "rag_attn_prefill_varlen",
             "rag_attn_decode_num_splits", "rag_attn_decode_workspace_size",
-            "rag_attn_decode_paged", "rag_kv_cache_write", "rag_plan_prompts"]
+            "rag_attn_decode_paged", "rag_kv_cache_write", "rag_plan_prompts",
+            "rag_prune_config_space", "rag_config_kv_bytes", "rag_choose_config",
+            "rag_device_free_memory"]
+
+
+class QueryProfile(ctypes.Structure):
+    _fields_ = [("complexity_high", ctypes.c_int32), ("joint_reasoning", ctypes.c_int32),
+                ("pieces", ctypes.c_int32), ("summary_len_min", ctypes.c_int32),
+                ("summary_len_max", ctypes.c_int32)]
+
+
+class ConfigSpace(ctypes.Structure):
+    _fields_ = [("methods", ctypes.c_uint32), ("num_chunks_min", ctypes.c_int32),
+                ("num_chunks_max", ctypes.c_int32), ("intermediate_length_min", ctypes.c_int32),
+                ("intermediate_length_max", ctypes.c_int32)]
+
+
+class RequestShape(ctypes.Structure):
+    _fields_ = [("query_len", ctypes.c_int32), ("chunk_len", ctypes.c_int32),
+                ("answer_len", ctypes.c_int32), ("kv_bytes_per_token", ctypes.c_int64)]
+
+
+class Config(ctypes.Structure):
+    _fields_ = [("method", ctypes.c_int32), ("num_chunks", ctypes.c_int32),
+                ("intermediate_length", ctypes.c_int32), ("fallback", ctypes.c_int32),
+                ("kv_bytes", ctypes.c_int64)]
 
 
 def lib():
@@ -73,6 +99,16 @@ def lib():
                                         _i32, _vp, ctypes.c_size_t, _vp]
     L.rag_kv_cache_write.restype = ctypes.c_int
     L.rag_kv_cache_write.argtypes = [_vp, _vp, _vp, _vp, _vp, _i32, _i32, _i32, _i32, _i32, _vp]
+    L.rag_prune_config_space.restype = ctypes.c_int
+    L.rag_prune_config_space.argtypes = [ctypes.POINTER(QueryProfile), ctypes.POINTER(ConfigSpace)]
+    L.rag_config_kv_bytes.restype = ctypes.c_int64
+    L.rag_config_kv_bytes.argtypes = [_i32, _i32, _i32, ctypes.POINTER(RequestShape)]
+    L.rag_choose_config.restype = ctypes.c_int
+    L.rag_choose_config.argtypes = [ctypes.POINTER(QueryProfile), ctypes.POINTER(RequestShape),
+                                    ctypes.c_int64, ctypes.POINTER(Config)]
+    L.rag_device_free_memory.restype = ctypes.c_int
+    L.rag_device_free_memory.argtypes = [ctypes.POINTER(ctypes.c_size_t),
+                                         ctypes.POINTER(ctypes.c_size_t)]
     L.rag_plan_prompts.restype = ctypes.c_int
     L.rag_plan_prompts.argtypes = [ctypes.c_int, _i32, _i32p, _i32p, _i32, _i32, _i32, _i32p,
                                    _i32, _i32p, _i32p]
@@ -208,3 +244,64 @@ def rag_plan_prompts(method, query_len, num_chunks, chunk_len, intermediate_leng
     _check(L.rag_plan_prompts(code, n, ql, nc, chunk_len, intermediate_length, answer_len, cu,
                               cap, ctypes.byref(count), dec))
     return list(cu), list(dec)[:count.value]
+
+
+# ---------------------------------------------------------------------------
+# configuration planner (host only)
+# ---------------------------------------------------------------------------
+CONFIG_METHOD_NAMES = {RAG_STUFF: "stuff", RAG_MAP_REDUCE_MAP: "map_reduce",
+                       RAG_MAP_RERANK: "map_rerank"}
+
+
+def _profile(complexity_high, joint_reasoning, pieces, summary_range):
+    return QueryProfile(int(bool(complexity_high)), int(bool(joint_reasoning)), int(pieces),
+                        int(summary_range[0]), int(summary_range[1]))
+
+
+def rag_prune_config_space(complexity_high, joint_reasoning, pieces, summary_range):
+    """Algorithm 1.  Returns (method names, (chunks_min, chunks_max),
+    (il_min, il_max))."""
+    sp = ConfigSpace()
+    _check(lib().rag_prune_config_space(
+        ctypes.byref(_profile(complexity_high, joint_reasoning, pieces, summary_range)),
+        ctypes.byref(sp)))
+    methods = tuple(n for m, n in CONFIG_METHOD_NAMES.items() if sp.methods & (1 << m))
+    return methods, (sp.num_chunks_min, sp.num_chunks_max), \
+        (sp.intermediate_length_min, sp.intermediate_length_max)
+
+
+def _shape(query_len, chunk_len, answer_len, bytes_per_token):
+    return RequestShape(int(query_len), int(chunk_len), int(answer_len), int(bytes_per_token))
+
+
+def rag_config_kv_bytes(method, num_chunks, intermediate_length, query_len, chunk_len,
+                        answer_len, bytes_per_token) -> int:
+    code = {v: k for k, v in CONFIG_METHOD_NAMES.items()}[method] if isinstance(method, str) \
+        else int(method)
+    return lib().rag_config_kv_bytes(code, int(num_chunks), int(intermediate_length),
+                                     ctypes.byref(_shape(query_len, chunk_len, answer_len,
+                                                         bytes_per_token)))
+
+
+def rag_choose_config(complexity_high, joint_reasoning, pieces, summary_range, query_len,
+                      chunk_len, answer_len, bytes_per_token, available_bytes):
+    """Best-fit choice.  Returns a dict (method name, num_chunks,
+    intermediate_length, kv_bytes, fallback) or None when nothing fits."""
+    out = Config()
+    st = lib().rag_choose_config(
+        ctypes.byref(_profile(complexity_high, joint_reasoning, pieces, summary_range)),
+        ctypes.byref(_shape(query_len, chunk_len, answer_len, bytes_per_token)),
+        int(available_bytes), ctypes.byref(out))
+    if st == RAG_NO_FIT:
+        return None
+    _check(st)
+    return dict(method=CONFIG_METHOD_NAMES[out.method], num_chunks=out.num_chunks,
+                intermediate_length=out.intermediate_length, kv_bytes=out.kv_bytes,
+                fallback=bool(out.fallback))
+
+
+def rag_device_free_memory():
+    """(free bytes, total bytes) of the current HIP device."""
+    f, t = ctypes.c_size_t(0), ctypes.c_size_t(0)
+    _check(lib().rag_device_free_memory(ctypes.byref(f), ctypes.byref(t)))
+    return f.value, t.value

@@ -10,12 +10,15 @@
 #include <string>
 #include <vector>
 
+#include "errors.h"
 #include "launch.h"
 #include "rag_attn.h"
 
 namespace {
-
 thread_local std::string g_last_error;
+}  // namespace
+
+namespace rag {
 
 rag_status fail(rag_status st, const char* fmt, ...) {
   char buf[512];
@@ -31,6 +34,13 @@ rag_status ok() {
   g_last_error.clear();
   return RAG_OK;
 }
+
+}  // namespace rag
+
+namespace {
+
+using rag::fail;
+using rag::ok;
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
