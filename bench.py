@@ -321,6 +321,21 @@ def bench_phase_kv_write(torch, dev, reps):
     return out
 
 
+def bench_phase_stream(torch, n=32, rate=100.0, budget_gb=16):
+    """A synthetic query stream (Poisson arrivals, random profiles) through the
+    configuration planner and the kernels: 7B-class shape (Hq 32, Hkv 8, d 128,
+    32 layers for the KV budget), 512-token chunks, `budget_gb` GB of KV."""
+    from paper_2412_10543_amd import stream
+    eng = stream.Engine(kv_budget_bytes=int(budget_gb * (1 << 30)), chunk_len=512, answer_len=32,
+                        layers=32, seed=5)
+    res = stream.run_stream(stream.synthetic_queries(n, rate, seed=2024), eng)
+    res["rate_per_s"] = rate
+    res["kv_budget_gb"] = budget_gb
+    del eng
+    torch.cuda.empty_cache()
+    return res
+
+
 # ---------------------------------------------------------------------------
 # CPU baseline: the oracle on a bounded sample of the same workload
 # ---------------------------------------------------------------------------
@@ -479,6 +494,8 @@ def main():
             phases[fn.__name__] = bench_phase_stuff(torch, fn(), dev, args.extra_reps)
         phases["mixed"] = bench_phase_mixed(torch, dev, args.extra_reps)
         phases["kv_write"] = bench_phase_kv_write(torch, dev, max(args.extra_reps, 10))
+        phases["query_stream"] = bench_phase_stream(torch)
+        phases["query_stream_tight"] = bench_phase_stream(torch, n=32, rate=2000.0, budget_gb=1)
         res["phases"] = phases
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(torch, st)
