@@ -16,6 +16,8 @@ Contents
   planner.py     prompt lengths per synthesis method (Sec. "RAG systems and
                  configurations")
   kvcache.py     paged KV-cache write (token -> page, offset by its slot)
+  scheduler.py   configuration pruning (Algorithm 1) and memory-aware choice
+  awq.py         group-quantized int4-weight GEMM (dequantize, multiply)
 
 Pins: ``tests/test_oracle_pins.py`` checks the oracle against brute force on
 tiny inputs, closed forms and invariants; ``tests/test_oracle_mutants.py``
@@ -23,5 +25,6 @@ plants mistakes in a copy of the C source and checks that the pins catch each
 one.
 """
 from .attention import Oracle, bf16_bits_to_f64, build, default  # noqa: F401
+from .awq import awq_gemm, dequantize  # noqa: F401
 from .kvcache import slots_from_block_table, write_kv_cache  # noqa: F401
 from .planner import plan_prompts  # noqa: F401
