@@ -321,6 +321,46 @@ def bench_phase_kv_write(torch, dev, reps):
     return out
 
 
+def bench_phase_awq(torch, dev, reps, batches=(16, 8192)):
+    """Group-quantized int4-weight GEMMs of the 7B model's linear layers
+    (qkv, o, gate_up, down) at a decode batch of 16 rows (HBM-bound: the packed
+    weights dominate) and a chunked-prefill batch of 8192 rows (MFMA-bound).
+    Algorithmic bytes: x and y in bf16, codes at 4 bits, one bf16 scale and one
+    uint8 zero point per group of 128 k; flops 2 M N K."""
+    from paper_2412_10543_amd import binding
+    from paper_2412_10543_amd.workloads import AWQ_LAYERS_7B, awq_problem
+    out = {}
+    for name, K, N in AWQ_LAYERS_7B:
+        p = awq_problem(max(batches), N, K, seed=K + N, device=dev)
+        qw = torch.from_numpy(binding.rag_awq_pack_weights(p.codes)).to(dev)
+        sc, z = p.scales.to(dev), torch.from_numpy(p.zeros).to(dev)
+        for M in batches:
+            x = p.x[:M]
+            y = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
+            ws = torch.empty(max(binding.rag_awq_workspace_size(M, N, K), 1), dtype=torch.uint8,
+                             device=dev)
+            binding.rag_awq_gemm(x, qw, sc, z, y, ws)
+            torch.cuda.synchronize()
+            timer = Timer(torch)
+            for _ in range(reps):
+                timer.start("g")
+                binding.rag_awq_gemm(x, qw, sc, z, y, ws)
+                timer.stop("g")
+            torch.cuda.synchronize()
+            ms = median(timer.ms("g"))
+            nbytes = 2.0 * M * K + K * N / 2 + (K // 128) * N * 3 + 2.0 * M * N
+            tflops = 2.0 * M * N * K / ms / 1e9
+            gbs = nbytes / ms / 1e6
+            out[f"{name}_m{M}"] = {"M": M, "N": N, "K": K, "us": round(ms * 1e3, 2),
+                                   "tflops": round(tflops, 1), "gbs": round(gbs, 1),
+                                   "frac_mfma": round(tflops / PEAK_BF16_TFLOPS, 4),
+                                   "frac_hbm": round(gbs / PEAK_HBM_GBS, 4)}
+            del x, y, ws
+        del p, qw, sc, z
+    torch.cuda.empty_cache()
+    return out
+
+
 def bench_phase_stream(torch, n=32, rate=100.0, budget_gb=16):
     """A synthetic query stream (Poisson arrivals, random profiles) through the
     configuration planner and the kernels: 7B-class shape (Hq 32, Hkv 8, d 128,
@@ -494,6 +534,7 @@ def main():
             phases[fn.__name__] = bench_phase_stuff(torch, fn(), dev, args.extra_reps)
         phases["mixed"] = bench_phase_mixed(torch, dev, args.extra_reps)
         phases["kv_write"] = bench_phase_kv_write(torch, dev, max(args.extra_reps, 10))
+        phases["awq_gemm_7b"] = bench_phase_awq(torch, dev, max(args.extra_reps, 10))
         phases["query_stream"] = bench_phase_stream(torch)
         phases["query_stream_tight"] = bench_phase_stream(torch, n=32, rate=2000.0, budget_gb=1)
         res["phases"] = phases

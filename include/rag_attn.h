@@ -332,6 +332,57 @@ rag_status rag_choose_config(const rag_query_profile *profile,
  * of rag_choose_config's available_bytes.  RAG_OK or RAG_ERR_HIP. */
 rag_status rag_device_free_memory(size_t *free_bytes, size_t *total_bytes);
 
+/*
+ * Group-quantized int4-weight GEMM, the weight format of the served models
+ * (Sec. "Setup": both are AWQ-quantized), for the projections and MLP around
+ * the attention calls:
+ *
+ *   y[m, n] = sum_k x[m, k] * (q[k, n] - zeros[g, n]) * scales[g, n],
+ *   g = k / group_size.
+ *
+ * Codes q and zero points are 4-bit unsigned (0..15), one scale and one zero
+ * point per group of 128 consecutive k and output column n.  Products and sums
+ * run in fp32, y is rounded to bf16 (nearest even).
+ *
+ * rag_awq_pack_weights (host only) packs codes for the kernel:
+ *   q       host uint8 [K, N], each 0..15
+ *   packed  host int32 [K / 128, N, 16] (K * N / 8 words), library-defined
+ *           order: 32 contiguous bytes per (group, column, half of the group)
+ * Returns RAG_OK, RAG_ERR_INVALID_ARG (null pointer, a code above 15, N or K
+ * not positive) or RAG_ERR_UNSUPPORTED (group_size not 128, K or N not a
+ * multiple of 128).
+ */
+rag_status rag_awq_pack_weights(const uint8_t *q, int32_t K, int32_t N,
+                                int32_t group_size, int32_t *packed);
+
+/* Bytes of workspace rag_awq_gemm needs (0 for M == 0 or invalid shapes).
+ * Library-internal layout: fp32 group sums of x [K / 128, M], then, for a
+ * small M whose tiles cannot fill the GPU, fp32 partial outputs
+ * [splits, M, N] of a split over the groups (reduced in a fixed order, so
+ * results do not depend on timing). */
+size_t rag_awq_workspace_size(int32_t M, int32_t N, int32_t K,
+                              int32_t group_size);
+
+/*
+ *   x        device bf16 [M, K], row-major
+ *   qweight  device int32 [K / 128, N, 16] from rag_awq_pack_weights
+ *   scales   device bf16 [K / 128, N]
+ *   zeros    device uint8 [K / 128, N], each 0..15
+ *   y        device bf16 [M, N]; output, written in full
+ *   workspace  device, >= rag_awq_workspace_size(M, N, K, group_size) bytes,
+ *            256-byte aligned; no state is kept in it between calls.
+ *            Overlapping calls must not share it.
+ * Returns RAG_OK (M == 0 is a no-op; x and y may then be NULL),
+ * RAG_ERR_INVALID_ARG (null or misaligned pointer: x, qweight, y 16-byte,
+ * scales 2-byte; negative M; N or K not positive), RAG_ERR_UNSUPPORTED (group_size not 128, K or N not a multiple of
+ * 128, M over 4,194,240), RAG_ERR_WORKSPACE or RAG_ERR_HIP.
+ */
+rag_status rag_awq_gemm(const void *x, const int32_t *qweight,
+                        const void *scales, const uint8_t *zeros, void *y,
+                        int32_t M, int32_t N, int32_t K, int32_t group_size,
+                        void *workspace, size_t workspace_bytes,
+                        hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -49,7 +49,8 @@ def exported_symbols():
             "rag_attn_decode_num_splits", "rag_attn_decode_workspace_size",
             "rag_attn_decode_paged", "rag_kv_cache_write", "rag_plan_prompts",
             "rag_prune_config_space", "rag_config_kv_bytes", "rag_choose_config",
-            "rag_device_free_memory"]
+            "rag_device_free_memory", "rag_awq_pack_weights", "rag_awq_workspace_size",
+            "rag_awq_gemm"]
 
 
 class QueryProfile(ctypes.Structure):
@@ -109,6 +110,13 @@ def lib():
     L.rag_device_free_memory.restype = ctypes.c_int
     L.rag_device_free_memory.argtypes = [ctypes.POINTER(ctypes.c_size_t),
                                          ctypes.POINTER(ctypes.c_size_t)]
+    L.rag_awq_pack_weights.restype = ctypes.c_int
+    L.rag_awq_pack_weights.argtypes = [_vp, _i32, _i32, _i32, _vp]
+    L.rag_awq_workspace_size.restype = ctypes.c_size_t
+    L.rag_awq_workspace_size.argtypes = [_i32, _i32, _i32, _i32]
+    L.rag_awq_gemm.restype = ctypes.c_int
+    L.rag_awq_gemm.argtypes = [_vp, _vp, _vp, _vp, _vp, _i32, _i32, _i32, _i32, _vp,
+                               ctypes.c_size_t, _vp]
     L.rag_plan_prompts.restype = ctypes.c_int
     L.rag_plan_prompts.argtypes = [ctypes.c_int, _i32, _i32p, _i32p, _i32, _i32, _i32, _i32p,
                                    _i32, _i32p, _i32p]
@@ -305,3 +313,45 @@ def rag_device_free_memory():
     f, t = ctypes.c_size_t(0), ctypes.c_size_t(0)
     _check(lib().rag_device_free_memory(ctypes.byref(f), ctypes.byref(t)))
     return f.value, t.value
+
+
+def rag_awq_pack_weights(q, group_size: int = 128):
+    """Host packer: q a numpy uint8 array [K, N] of 4-bit codes -> numpy int32
+    [K // group_size, N, 16] in the kernel's order."""
+    import numpy as np
+    q = np.ascontiguousarray(q, dtype=np.uint8)
+    if q.ndim != 2:
+        raise ValueError("q must be [K, N]")
+    K, N = q.shape
+    out = np.empty((max(K // 128, 0), N, 16), dtype=np.int32)
+    _check(lib().rag_awq_pack_weights(q.ctypes.data, K, N, int(group_size), out.ctypes.data))
+    return out
+
+
+def rag_awq_workspace_size(M: int, N: int, K: int, group_size: int = 128) -> int:
+    return int(lib().rag_awq_workspace_size(int(M), int(N), int(K), int(group_size)))
+
+
+def rag_awq_gemm(x, qweight, scales, zeros, y, workspace, group_size: int = 128,
+                 stream=None) -> None:
+    """x [M, K] bf16; qweight int32 [K/128, N, 16] (rag_awq_pack_weights);
+    scales bf16 [K/128, N]; zeros uint8 [K/128, N]; y [M, N] bf16 output;
+    workspace a GPU uint8 tensor of rag_awq_workspace_size bytes (no
+    initialisation needed)."""
+    _need(x, torch.bfloat16, "x", 2)
+    _need(qweight, torch.int32, "qweight", 3)
+    _need(scales, torch.bfloat16, "scales", 2)
+    _need(zeros, torch.uint8, "zeros", 2)
+    _need(y, torch.bfloat16, "y", 2)
+    M, K = x.shape
+    N = y.shape[1]
+    if y.shape[0] != M or qweight.shape != (K // 128, N, 16) or \
+            scales.shape != (K // 128, N) or zeros.shape != (K // 128, N):
+        raise ValueError("awq gemm: inconsistent shapes")
+    ws_bytes = 0
+    if workspace is not None:
+        if not workspace.is_cuda or not workspace.is_contiguous():
+            raise ValueError("workspace must be a contiguous GPU tensor")
+        ws_bytes = workspace.numel() * workspace.element_size()
+    _check(lib().rag_awq_gemm(_ptr(x), _ptr(qweight), _ptr(scales), _ptr(zeros), _ptr(y), M, N,
+                              K, int(group_size), _ptr(workspace), ws_bytes, _stream(stream)))

@@ -22,7 +22,7 @@ DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-I", INCLUDE, "-I", CSRC,
           "-Wall", "-Wno-unused-result"]
 
-SOURCES = ["kernels.hip", "kv_cache.hip", "api.cpp", "planner.cpp"]
+SOURCES = ["kernels.hip", "kv_cache.hip", "awq_gemm.hip", "api.cpp", "awq_api.cpp", "planner.cpp"]
 HEADERS = ["common.h", "prefill_tile.h", "decode_unit.h", "launch.h", "errors.h"]
 
 

@@ -179,3 +179,36 @@ def paged_pool(kv_lens, hkv: int, d: int, seed: int, block_size: int = BLOCK_SIZ
         v = torch.where(mask, nan, v)
     return PagedPool(k.contiguous(), v.contiguous(),
                      torch.from_numpy(table).to(device), list(kv_lens), num_blocks)
+
+
+# --------------------------------------------------------------------------
+# group-quantized int4 weights
+# --------------------------------------------------------------------------
+AWQ_GROUP = 128
+# Linear layers of the 7B model (hidden 4096, MLP 14336, 32 q / 8 kv heads of
+# 128): (name, K, N) with y[M, N] = x[M, K] W[K, N].
+AWQ_LAYERS_7B = (("qkv_proj", 4096, 6144), ("o_proj", 4096, 4096),
+                 ("gate_up_proj", 4096, 28672), ("down_proj", 14336, 4096))
+
+
+@dataclasses.dataclass
+class AwqProblem:
+    x: torch.Tensor        # [M, K] bf16 on the requested device
+    codes: np.ndarray      # uint8 [K, N], 0..15
+    zeros: np.ndarray      # uint8 [K / 128, N], 0..15
+    scales: torch.Tensor   # bf16 [K / 128, N] (host)
+
+
+def awq_problem(M: int, N: int, K: int, seed: int, device="cpu") -> AwqProblem:
+    """x ~ N(0, 1) in bf16; codes and zero points uniform on 0..15; scales
+    uniform in [0.5, 1.5] / (6.5 sqrt(K)) rounded to bf16, so that the weights
+    have a spread near 1 / sqrt(K) (the code minus zero point has standard
+    deviation about 6.5) and outputs stay of order 1."""
+    rng = _rng(seed)
+    codes = rng.integers(0, 16, size=(K, N), dtype=np.uint8)
+    groups = K // AWQ_GROUP
+    zeros = rng.integers(0, 16, size=(groups, N), dtype=np.uint8)
+    s = rng.uniform(0.5, 1.5, size=(groups, N)) / (6.5 * np.sqrt(K))
+    scales = torch.from_numpy(s.astype(np.float32)).to(torch.bfloat16)
+    x = normal_bf16((M, K), seed + 1, device)
+    return AwqProblem(x, codes, zeros, scales)

@@ -183,3 +183,76 @@ def test_planner_errors():
     cu2 = (ctypes.c_int32 * 2)()
     assert L.rag_plan_prompts(0, 1, big, many, 1_000_000_000, 0, 0, cu2, 2, ctypes.byref(n),
                               None) == binding.RAG_ERR_INVALID_ARG
+
+
+# ---- group-quantized int4-weight GEMM --------------------------------------
+def _awq(**kw):
+    a = dict(x=FAKE, qw=FAKE, s=FAKE, z=FAKE, y=FAKE, M=64, N=256, K=512, G=128, ws=FAKE,
+             ws_bytes=1 << 30)
+    a.update(kw)
+    return binding.lib().rag_awq_gemm(a["x"], a["qw"], a["s"], a["z"], a["y"], a["M"], a["N"],
+                                      a["K"], a["G"], a["ws"], a["ws_bytes"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(x=None), binding.RAG_ERR_INVALID_ARG),
+    (dict(z=None), binding.RAG_ERR_INVALID_ARG),
+    (dict(x=FAKE + 8), binding.RAG_ERR_INVALID_ARG),
+    (dict(s=FAKE + 1), binding.RAG_ERR_INVALID_ARG),
+    (dict(M=-1), binding.RAG_ERR_INVALID_ARG),
+    (dict(N=0), binding.RAG_ERR_INVALID_ARG),
+    (dict(G=64), binding.RAG_ERR_UNSUPPORTED),
+    (dict(K=500), binding.RAG_ERR_UNSUPPORTED),
+    (dict(N=200), binding.RAG_ERR_UNSUPPORTED),
+    (dict(M=5_000_000), binding.RAG_ERR_UNSUPPORTED),
+    (dict(ws=None), binding.RAG_ERR_WORKSPACE),
+    (dict(ws_bytes=100), binding.RAG_ERR_WORKSPACE),
+    (dict(ws=FAKE + 16), binding.RAG_ERR_INVALID_ARG),
+    (dict(M=0, x=None, y=None, ws=None, ws_bytes=0), binding.RAG_OK),  # nothing to compute
+    (dict(M=0, qw=None), binding.RAG_ERR_INVALID_ARG),
+])
+def test_awq_validation(kw, status):
+    assert _awq(**kw) == status
+    if status != binding.RAG_OK:
+        assert binding.rag_last_error().startswith("awq gemm")
+
+
+def test_awq_workspace_size():
+    ws = binding.rag_awq_workspace_size
+    assert ws(0, 256, 512) == 0
+    assert ws(64, 256, 500) == 0 and ws(64, 256, 512, 64) == 0
+    # enough tiles to fill the GPU: only the per-group row sums, 256-byte rounded
+    M, N, K = 4096, 4096, 4096
+    assert ws(M, N, K) == (K // 128) * M * 4
+    # one tile row of a wide decode batch: group sums plus fp32 split partials
+    small = ws(16, 4096, 4096)
+    assert small > (4096 // 128) * 16 * 4
+    assert (small - 2048) % (16 * 4096 * 4) == 0
+
+
+def test_awq_pack_layout():
+    """Every code lands at the documented position: word 8h + t of (group g,
+    column n) holds k = 128g + 16t + 8h + j at bits 4(j/2) + 16(j%2)."""
+    r = np.random.Generator(np.random.PCG64(3))
+    K, N = 384, 256
+    q = r.integers(0, 16, size=(K, N), dtype=np.uint8)
+    packed = binding.rag_awq_pack_weights(q).view(np.uint32)
+    assert packed.shape == (K // 128, N, 16)
+    back = np.zeros_like(q)
+    for w in range(16):
+        h, t = divmod(w, 8)
+        for j in range(8):
+            k = np.arange(K // 128) * 128 + 16 * t + 8 * h + j
+            back[k, :] = (packed[:, :, w] >> (4 * (j // 2) + 16 * (j % 2))) & 15
+    assert np.array_equal(back, q)
+
+
+def test_awq_pack_errors():
+    q = np.zeros((256, 128), dtype=np.uint8)
+    q[200, 5] = 16
+    with pytest.raises(binding.RagError, match="not 4-bit"):
+        binding.rag_awq_pack_weights(q)
+    with pytest.raises(binding.RagError, match="group_size"):
+        binding.rag_awq_pack_weights(np.zeros((256, 128), np.uint8), group_size=64)
+    with pytest.raises(binding.RagError, match="multiple of 128"):
+        binding.rag_awq_pack_weights(np.zeros((256, 100), np.uint8))

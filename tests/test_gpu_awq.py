@@ -1,0 +1,113 @@
+"""GPU parity of the group-quantized int4-weight GEMM (rag_awq_gemm) against
+the fp64 oracle (dequantize per group, then multiply).
+
+Tolerance, from the arithmetic: the kernel's products are exact and its sums
+run in fp32 over 128-term group sums, so its error before the final rounding
+is at most about 128 * 2^-24 = 2^-17 times A = sum_k |x| (|q| + 128 + |z| +
+128) |s| (the magnitudes entering those sums); y is then rounded to bf16
+(half an ulp, 2^-9 relative).  Each element must satisfy
+|y - ref| <= 2^-8 |ref| + 2^-17 A, and with these inputs (outputs of order
+1) the attention path's max-abs 2e-2 / mean-abs 2e-3 bar as well.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2412_10543_amd import binding
+from paper_2412_10543_amd.workloads import AWQ_LAYERS_7B, awq_problem
+
+import gpu_support as G
+
+pytestmark = pytest.mark.gpu
+
+
+def _device(p):
+    qw = torch.from_numpy(binding.rag_awq_pack_weights(p.codes)).cuda()
+    return qw, p.scales.cuda(), torch.from_numpy(p.zeros).cuda()
+
+
+def _run(p, qw, sc, z):
+    M, K = p.x.shape
+    N = p.codes.shape[1]
+    y = torch.full((M, N), float("nan"), dtype=torch.bfloat16, device="cuda")
+    ws = torch.empty(max(binding.rag_awq_workspace_size(M, N, K), 1), dtype=torch.uint8,
+                     device="cuda")
+    binding.rag_awq_gemm(p.x, qw, sc, z, y, ws)
+    torch.cuda.synchronize()
+    return y
+
+
+def _check(p, y, rows=None, cols=None):
+    x = p.x.float().cpu().numpy().astype(np.float64)
+    s = p.scales.float().numpy().astype(np.float64)
+    rows = np.arange(x.shape[0]) if rows is None else rows
+    cols = np.arange(p.codes.shape[1]) if cols is None else cols
+    xr = x[rows]
+    ref = oracle.awq_gemm(xr, p.codes[:, cols], p.zeros[:, cols], s[:, cols], 128)
+    g = np.arange(p.codes.shape[0]) // 128
+    mag = (p.codes[:, cols].astype(np.float64) + p.zeros[g][:, cols] + 256) * s[g][:, cols]
+    bound = 2.0 ** -8 * np.abs(ref) + 2.0 ** -17 * (np.abs(xr) @ mag)
+    got = y.float().cpu().numpy().astype(np.float64)[np.ix_(rows, cols)]
+    assert np.all(np.isfinite(got)), "non-finite output"
+    err = np.abs(got - ref)
+    worst = np.unravel_index(np.argmax(err - bound), err.shape)
+    assert np.all(err <= bound), f"err {err[worst]:.3e} > bound {bound[worst]:.3e} at {worst}"
+    G.assert_parity(got, ref, "awq")
+
+
+@pytest.mark.parametrize("M,N,K", [
+    (1, 128, 128), (7, 256, 384), (64, 128, 256), (77, 384, 1024), (130, 512, 512),
+    (16, 4096, 4096), (256, 1024, 2048), (333, 256, 14336 // 4), (1000, 640, 256)])
+def test_awq_parity(M, N, K):
+    p = awq_problem(M, N, K, seed=M * 7 + N + K, device="cuda")
+    _check(p, _run(p, *_device(p)))
+
+
+@pytest.mark.parametrize("name,K,N", AWQ_LAYERS_7B)
+@pytest.mark.parametrize("M", [16, 8192])
+def test_awq_7b_layers_sampled(name, K, N, M):
+    """The 7B model's linear layers at a decode batch and a chunked-prefill
+    batch, the shapes the bench times; sampled rows and columns (first, last,
+    random) against the oracle."""
+    p = awq_problem(M, N, K, seed=K + N + M, device="cuda")
+    y = _run(p, *_device(p))
+    r = np.random.Generator(np.random.PCG64(M + N))
+    rows = np.unique(np.concatenate([[0, M - 1], r.integers(0, M, 14)]))
+    cols = np.unique(np.concatenate([[0, 127, 128, N - 1], r.integers(0, N, 60)]))
+    _check(p, y, rows, cols)
+
+
+def test_awq_deterministic_and_extremes():
+    """Two runs give identical bits (fixed-order split reduction); codes and
+    zero points at 0 and 15 and zero scales are handled exactly."""
+    M, N, K = 24, 1024, 2048
+    p = awq_problem(M, N, K, seed=5, device="cuda")
+    p.codes[:128] = 15
+    p.zeros[0] = 0
+    p.codes[128:256] = 0
+    p.zeros[1] = 15
+    p.scales[2] = 0.0
+    dev = _device(p)
+    a, b = _run(p, *dev), _run(p, *dev)
+    assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+    _check(p, a)
+
+
+def test_awq_zero_weights():
+    """q == z everywhere: every weight is zero; y is zero up to the fp32
+    cancellation between the code sums and the zero-point term (the bound's
+    2^-17 A part, as ref is 0)."""
+    M, N, K = 40, 256, 512
+    p = awq_problem(M, N, K, seed=9, device="cuda")
+    p.codes[:] = 6
+    p.zeros[:] = 6
+    _check(p, _run(p, *_device(p)))
+
+
+def test_awq_empty_batch():
+    p = awq_problem(0, 256, 256, seed=1, device="cuda")
+    qw, sc, z = _device(p)
+    y = torch.empty((0, 256), dtype=torch.bfloat16, device="cuda")
+    binding.rag_awq_gemm(p.x, qw, sc, z, y, None)
+    torch.cuda.synchronize()
