@@ -356,10 +356,10 @@ rag_status rag_awq_pack_weights(const uint8_t *q, int32_t K, int32_t N,
                                 int32_t group_size, int32_t *packed);
 
 /* Bytes of workspace rag_awq_gemm needs (0 for M == 0 or invalid shapes).
- * Library-internal layout: fp32 group sums of x [K / 128, M], then, for a
- * small M whose tiles cannot fill the GPU, fp32 partial outputs
- * [splits, M, N] of a split over the groups (reduced in a fixed order, so
- * results do not depend on timing). */
+ * Library-internal layout: the group sums of x [K / 128, M] (each as three
+ * bf16 pieces in 16 bytes), then, when the output tiles are too few to fill
+ * the GPU, fp32 partial outputs [splits, M, N] of a split over the groups
+ * (reduced in a fixed order, so results do not depend on timing). */
 size_t rag_awq_workspace_size(int32_t M, int32_t N, int32_t K,
                               int32_t group_size);
 
@@ -373,8 +373,8 @@ size_t rag_awq_workspace_size(int32_t M, int32_t N, int32_t K,
  *            256-byte aligned; no state is kept in it between calls.
  *            Overlapping calls must not share it.
  * Returns RAG_OK (M == 0 is a no-op; x and y may then be NULL),
- * RAG_ERR_INVALID_ARG (null or misaligned pointer: x, qweight, y 16-byte,
- * scales 2-byte; negative M; N or K not positive), RAG_ERR_UNSUPPORTED (group_size not 128, K or N not a multiple of
+ * RAG_ERR_INVALID_ARG (null pointer, a pointer not 16-byte aligned, negative
+ * M, N or K not positive), RAG_ERR_UNSUPPORTED (group_size not 128, K or N not a multiple of
  * 128, M over 4,194,240), RAG_ERR_WORKSPACE or RAG_ERR_HIP.
  */
 rag_status rag_awq_gemm(const void *x, const int32_t *qweight,

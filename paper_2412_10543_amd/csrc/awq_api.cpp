@@ -39,7 +39,7 @@ extern "C" {
 size_t rag_awq_workspace_size(int32_t M, int32_t N, int32_t K, int32_t group_size) {
   if (check_shape("awq workspace", M, N, K, group_size) != RAG_OK || M == 0) return 0;
   const rag::AwqPlan p = rag::awq_plan(M, N, K);
-  return p.rsum_bytes + p.part_bytes;
+  return p.sp_bytes + p.part_bytes;
 }
 
 rag_status rag_awq_pack_weights(const uint8_t* q, int32_t K, int32_t N, int32_t group_size,
@@ -78,9 +78,10 @@ rag_status rag_awq_gemm(const void* x, const int32_t* qweight, const void* scale
   if (rag_status st = check_shape("awq gemm", M, N, K, group_size); st != RAG_OK) return st;
   if (M == 0) return rag::ok();
   if (!x || !y) return fail(RAG_ERR_INVALID_ARG, "awq gemm: null x/y");
-  if (!aligned(x, 16) || !aligned(qweight, 16) || !aligned(y, 16))
-    return fail(RAG_ERR_INVALID_ARG, "awq gemm: x/qweight/y must be 16-byte aligned");
-  if (!aligned(scales, 2)) return fail(RAG_ERR_INVALID_ARG, "awq gemm: scales must be 2-byte aligned");
+  if (!aligned(x, 16) || !aligned(qweight, 16) || !aligned(y, 16) || !aligned(scales, 16) ||
+      !aligned(zeros, 16))
+    return fail(RAG_ERR_INVALID_ARG,
+                "awq gemm: x/qweight/scales/zeros/y must be 16-byte aligned");
   const size_t need = rag_awq_workspace_size(M, N, K, group_size);
   if (!workspace || workspace_bytes < need)
     return fail(RAG_ERR_WORKSPACE, "awq gemm: workspace of %zu bytes needed, %zu given", need,

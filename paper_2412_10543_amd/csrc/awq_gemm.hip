@@ -5,36 +5,33 @@
 // Method.  The 4-bit codes become MFMA operands without any floating-point
 // dequantization: a code q placed in the low mantissa bits of the bf16 value
 // 128.0 (bits 0x4300 | q) is exactly 128 + q, so two codes become a pair of
-// bf16 operands with one shift and one and-or.  Per group g the matrix cores
-// accumulate P'[m, n] = sum_k X[m, k] (128 + q[k, n]) in fp32 (exact products,
-// fp32 sums), and since
-//     sum_k X[m, k] W[k, n] = s[g, n] * (P'[m, n] - (128 + z[g, n]) * S[g, m])
-// with S[g, m] = sum of X[m, k] over the group, a short fp32 epilogue per group
-// applies zero point and scale.  S comes from a small pre-pass over X.
+// bf16 operands with one shift and one and-or.  For group g,
+//     sum_k X[m, k] W[k, n] = s[g, n] * (P[m, n] - (128 + z[g, n]) * S[g, m]),
+//     P = sum_k X[m, k] (128 + q[k, n]),   S[g, m] = sum of X[m, k] over g.
+// A pre-pass computes S in fp32 and stores it as three bf16 pieces
+// S1 + S2 + S3 = S (exact: 24 bits in 3 x 8).  The large-batch kernel folds
+// the zero-point term into the matrix cores as a ninth MFMA per group (A =
+// the pieces, B = -(128 + z), which bf16 holds exactly as bits 0xC300 | z),
+// so the per-group scale is one fp32 FMA per output element.
 //
 // Packed weight layout (rag_awq_pack_weights): int32 [K/128][N][16].  Word
 // 8h + t of column n in group g holds the codes of k = 128g + 16t + 8h + j,
-// j = 0..7, code j in bits 4(j/2) + 16(j%2) .. +4.  Lane (column c, half h)
-// of the MFMA B operand for k-step t then needs word 8h + t of its column: a
-// lane's 8 words are 32 contiguous bytes, and the words of 32 consecutive
-// columns of a group are 2 KB contiguous.
-//
-// Tiling: a workgroup of 4 waves computes a 64 x 128 tile of Y (wave w: all 64
-// rows, columns 32w .. 32w+31, two 32x32 MFMA blocks); small batches split the
-// groups over workgroups (partial sums in the workspace, reduced in fixed
-// order by a second kernel, so results are deterministic).
+// j = 0..7, code j in bits 4(j/2) + 16(j%2) .. +4.  MFMA B-operand lane
+// (column c, half h) at k-step t needs word 8h + t of its column; a column's
+// 16 words of one group are 64 contiguous bytes.
 #include "common.h"
 #include "launch.h"
 
 namespace rag {
 
 constexpr int kAwqGroup = 128;
-constexpr int kAwqBM = 64;
-constexpr int kAwqBN = 128;
+constexpr int kAwqCus = 256;     // MI355X compute units
 
-// S[g, m] = sum over the group of X[m, k], fp32 in k order.
-__global__ __launch_bounds__(256) void awq_row_sums_kernel(const bf16_t* __restrict__ x,
-                                                           float* __restrict__ s, int M, int K) {
+// S[g, m] = sum over the group of X[m, k] (fp32, k order), stored as bf16
+// pieces [S1, S2, S3, 0, 0, 0, 0, 0] (16 bytes per (g, m)).
+__global__ __launch_bounds__(256) void awq_group_sums_kernel(const bf16_t* __restrict__ x,
+                                                             bf16_t* __restrict__ sp, int M,
+                                                             int K) {
   const int groups = K / kAwqGroup;
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= (int64_t)groups * M) return;
@@ -47,31 +44,282 @@ __global__ __launch_bounds__(256) void awq_row_sums_kernel(const bf16_t* __restr
 #pragma unroll
     for (int e = 0; e < 8; ++e) acc += (float)v[e];
   }
-  s[(size_t)g * M + m] = acc;
+  const __bf16 s1 = (__bf16)acc;
+  const float r1 = acc - (float)s1;
+  const __bf16 s2 = (__bf16)r1;
+  const __bf16 s3 = (__bf16)(r1 - (float)s2);
+  u32x4 out;
+  out[0] = (uint32_t)__builtin_bit_cast(uint16_t, s1) |
+           ((uint32_t)__builtin_bit_cast(uint16_t, s2) << 16);
+  out[1] = (uint32_t)__builtin_bit_cast(uint16_t, s3);
+  out[2] = 0;
+  out[3] = 0;
+  *reinterpret_cast<u32x4*>(sp + (size_t)i * 8) = out;
 }
 
-// Four bf16 pairs (128 + code) from one packed word.
-__device__ __forceinline__ bf16x8 codes_to_bf16(uint32_t w) {
+// A value the compiler must keep in a VGPR (no constant folding).
+__device__ __forceinline__ uint32_t in_vgpr(uint32_t v) {
+  asm volatile("" : "+v"(v));
+  return v;
+}
+
+// Four bf16 pairs (128 + code) from one packed word.  mask = 0x000F000F and
+// magic = 0x43004300 come in registers: gfx9 VOP3 instructions take no
+// literal operand, and with both constants in VGPRs each pair is one
+// v_and_or_b32 (after a shift).
+__device__ __forceinline__ bf16x8 codes_to_bf16(uint32_t w, uint32_t mask, uint32_t magic) {
   u32x4 r;
-  r[0] = (w & 0x000F000Fu) | 0x43004300u;
-  r[1] = ((w >> 4) & 0x000F000Fu) | 0x43004300u;
-  r[2] = ((w >> 8) & 0x000F000Fu) | 0x43004300u;
-  r[3] = ((w >> 12) & 0x000F000Fu) | 0x43004300u;
+  r[0] = (w & mask) | magic;
+  r[1] = ((w >> 4) & mask) | magic;
+  r[2] = ((w >> 8) & mask) | magic;
+  r[3] = ((w >> 12) & mask) | magic;
   return as_bf16x8(r);
 }
 
+__device__ __forceinline__ float bf16_to_f32(uint32_t bits16) {
+  return __builtin_bit_cast(float, bits16 << 16);
+}
+
+// ---------------------------------------------------------------------------
+// Large batches: 8-wave workgroups own 128 x 256 tiles of Y; wave (wm, wn)
+// computes rows 64 wm .. +64 and columns 64 wn .. +64 as 2 x 2 MFMA blocks of
+// 32 x 32.  Per group the workgroup stages in LDS, by direct global -> LDS
+// copies issued two groups ahead into a 3-stage ring:
+//   X   128 rows x 128 k bf16, row r's 16-byte chunk c at position c ^ (r & 15)
+//       (the MFMA A reads of 16 rows then hit 16 distinct bank groups)
+//   W   256 columns x 64 bytes of codes, the 16-byte chunk j of column c at
+//       position j ^ ((c >> 2) & 3) within its 1 KB copy block
+//   SP  128 rows x 16 bytes of group-sum pieces
+//   SZ  256 bf16 scales then 256 uint8 zero points
+// ---------------------------------------------------------------------------
+namespace awq_lg {
+constexpr int kThreads = 512;
+constexpr int kBM = 128;
+constexpr int kBN = 256;
+constexpr int kStages = 3;
+constexpr int kX = kBM * kAwqGroup * 2;          // 32768
+constexpr int kW = kBN * kAwqGroup / 2;          // 16384
+constexpr int kSP = kBM * 16;                    // 2048
+constexpr int kSZ = kBN * 3;                     // 768
+constexpr int kStage = kX + kW + kSP + kSZ;      // 51968
+constexpr int kGroupM = 8;                       // M tiles per raster group
+constexpr int kOutStride = 160;                  // bytes per row of the output transpose
+static_assert(kStage % 16 == 0, "stage alignment");
+static_assert(8 * 64 * kOutStride <= kStages * kStage, "output transpose fits");
+}  // namespace awq_lg
+
+// vmcnt <= n (n < 64), expcnt and lgkmcnt unconstrained.
+template <int n>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(n >= 0 && n < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt(0x0F70 | (n & 15) | ((n >> 4) << 14));
+}
+
 template <bool kSplit>
-__global__ __launch_bounds__(256, 2) void awq_gemm_kernel(
+__global__ __launch_bounds__(awq_lg::kThreads) void awq_gemm_lg_kernel(
+    const bf16_t* __restrict__ x, const uint32_t* __restrict__ qw,
+    const bf16_t* __restrict__ scales, const uint8_t* __restrict__ zeros,
+    const bf16_t* __restrict__ sp, bf16_t* __restrict__ y, float* __restrict__ part, int M,
+    int N, int K, int groups_per_split, int tiles_m, int tiles_n, int tiles_per_xcd) {
+  using namespace awq_lg;
+  __shared__ __attribute__((aligned(16))) char lds[kStages * kStage];
+  const int lane = threadIdx.x & 63, w = wave_id();
+  // tile: XCD-contiguous ranges of a grouped raster order (kGroupM M-tiles
+  // per group, N fastest within it), so the workgroups resident on one XCD
+  // share X rows and code columns in its L2
+  int xcd, local;
+  xcd_slot(blockIdx.x, xcd, local);
+  const int pid = xcd * tiles_per_xcd + local;
+  if (local >= tiles_per_xcd || pid >= tiles_m * tiles_n) return;
+  const int per_group = kGroupM * tiles_n;
+  const int first_m = (pid / per_group) * kGroupM;
+  const int gm = min(tiles_m - first_m, kGroupM);
+  const int mt = first_m + (pid % per_group) % gm;
+  const int nt = (pid % per_group) / gm;
+  const int m0 = mt * kBM, n0 = nt * kBN;
+  const int groups = K / kAwqGroup;
+  const int g_begin = blockIdx.y * groups_per_split;
+  const int n_groups = min(groups, g_begin + groups_per_split) - g_begin;
+
+  // ---- copies of one group into one stage (each wave its share) ----
+  auto issue = [&](int g, int st) {
+    char* S = lds + st * kStage;
+    const bf16_t* xb = x + (size_t)m0 * K + (size_t)g * kAwqGroup;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int i = 4 * w + j;
+      const int row = 4 * i + (lane >> 4);
+      const int c = (lane & 15) ^ (row & 15);
+      const int rr = min(m0 + row, M - 1) - m0;
+      dma16_s(xb, (uint32_t)(rr * K * 2 + c * 16), (bf16_t*)(S + i * 1024));
+    }
+    const uint32_t* wb = qw + ((size_t)g * N + n0) * 16;
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int i = 2 * w + j;
+      const int cl = lane >> 2;
+      const int ch = (lane & 3) ^ ((cl >> 2) & 3);
+      const int col = min(16 * i + cl, N - 1 - n0);
+      dma16_s(wb, (uint32_t)((col * 16 + ch * 4) * 4), (bf16_t*)(S + kX + i * 1024));
+    }
+    if (w < 2) {
+      const int rr = min(m0 + 64 * w + lane, M - 1);
+      dma16(sp + ((size_t)g * M + rr) * 8, (bf16_t*)(S + kX + kW + w * 1024));
+    } else if (w == 2) {
+      const void* src = lane < 32
+          ? (const void*)(scales + (size_t)g * N + min(n0 + 8 * lane, N - 8))
+          : (const void*)(zeros + (size_t)g * N + min(n0 + 16 * (lane - 32), N - 16));
+      if (lane < 48) dma16(src, (bf16_t*)(S + kX + kW + kSP));
+    }
+  };
+  // copies per wave per group: 7 for waves 0-2, 6 for the others
+  auto wait_group = [&](bool one_more_in_flight) {
+    if (!one_more_in_flight) {
+      wait_vm<0>();
+    } else if (w < 3) {
+      wait_vm<7>();
+    } else {
+      wait_vm<6>();
+    }
+  };
+
+  const int wm = w >> 2, wn = w & 3;
+  const int r = lane & 31, h = lane >> 5;
+  const uint32_t kMask = in_vgpr(0x000F000Fu), kMagic = in_vgpr(0x43004300u);
+  f32x16 yacc[2][2];
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int j = 0; j < 16; ++j) yacc[a][b][j] = 0.f;
+
+  if (n_groups > 0) issue(g_begin, 0);
+  if (n_groups > 1) issue(g_begin + 1, 1);
+  for (int it = 0; it < n_groups; ++it) {
+    wait_group(it + 1 < n_groups);
+    __syncthreads();
+    if (it + 2 < n_groups) issue(g_begin + it + 2, (it + 2) % kStages);
+    const char* S = lds + (it % kStages) * kStage;
+    const char* SX = S;
+    const char* SW = S + kX;
+    const char* SPc = S + kX + kW;
+    const char* SZ = S + kX + kW + kSP;
+
+    float sc[2];
+    bf16x8 bz[2];
+    u32x4 words[2][2];
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb) {
+      const int cl = 64 * wn + 32 * nb + r;
+      sc[nb] = bf16_to_f32(*reinterpret_cast<const uint16_t*>(SZ + 2 * cl));
+      const uint32_t nz = 0xC300u | SZ[512 + cl];   // bf16 -(128 + z)
+      u32x4 b;
+      b[0] = nz | (nz << 16);
+      b[1] = nz;
+      b[2] = 0;
+      b[3] = 0;
+      bz[nb] = as_bf16x8(b);
+      const int blk = cl >> 4, ci = cl & 15;
+#pragma unroll
+      for (int q = 0; q < 2; ++q) {
+        const int ch = (2 * h + q) ^ ((ci >> 2) & 3);
+        words[nb][q] = *reinterpret_cast<const u32x4*>(SW + blk * 1024 + ci * 64 + ch * 16);
+      }
+    }
+    f32x16 p[2][2];
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb) {
+      const int row = 64 * wm + 32 * mb + r;
+      u32x4 az = *reinterpret_cast<const u32x4*>(SPc + row * 16);
+      if (h) az = u32x4{0, 0, 0, 0};
+      const f32x16 zero = {};
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb) p[mb][nb] = mfma32(as_bf16x8(az), bz[nb], zero);
+    }
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+      bf16x8 a[2], b[2];
+#pragma unroll
+      for (int mb = 0; mb < 2; ++mb) {
+        const int row = 64 * wm + 32 * mb + r;
+        a[mb] = as_bf16x8(*reinterpret_cast<const u32x4*>(SX + row * 256 +
+                                                          (((2 * t + h) ^ (r & 15)) * 16)));
+      }
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb) b[nb] = codes_to_bf16(words[nb][t >> 2][t & 3], kMask, kMagic);
+#pragma unroll
+      for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+        for (int nb = 0; nb < 2; ++nb) p[mb][nb] = mfma32(a[mb], b[nb], p[mb][nb]);
+    }
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+        for (int j = 0; j < 16; ++j) yacc[mb][nb][j] = fmaf(sc[nb], p[mb][nb][j], yacc[mb][nb][j]);
+  }
+
+  // ---- output ----
+  const bool cols_in = n0 + 64 * wn < N;
+  if constexpr (kSplit) {
+    if (!cols_in) return;
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+          const int row = m0 + 64 * wm + 32 * mb + 8 * (j >> 2) + 4 * h + (j & 3);
+          if (row < M)
+            part[((size_t)blockIdx.y * M + row) * N + n0 + 64 * wn + 32 * nb + r] = yacc[mb][nb][j];
+        }
+  } else {
+    // transpose through LDS so that each lane stores 16 contiguous bytes
+    __syncthreads();
+    char* T = lds + w * 64 * kOutStride;
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+          const int row = 32 * mb + 8 * (j >> 2) + 4 * h + (j & 3);
+          const __bf16 v = (__bf16)yacc[mb][nb][j];
+          *reinterpret_cast<__bf16*>(T + row * kOutStride + 2 * (32 * nb + r)) = v;
+        }
+    wave_lds_sync();
+    if (!cols_in) return;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int idx = 64 * i + lane;
+      const int row = idx >> 3, ch = idx & 7;
+      const int grow = m0 + 64 * wm + row;
+      const u32x4 v = *reinterpret_cast<const u32x4*>(T + row * kOutStride + ch * 16);
+      if (grow < M)
+        *reinterpret_cast<u32x4*>(y + (size_t)grow * N + n0 + 64 * wn + 8 * ch) = v;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Small batches (M <= 64): 4-wave workgroups own 64 x 128 tiles; wave w
+// computes columns 32 w .. +32 of all 64 rows, operands straight from global
+// memory; the zero-point term is applied in fp32 from S = S1 + S2 + S3.
+// ---------------------------------------------------------------------------
+template <bool kSplit>
+__global__ __launch_bounds__(256, 2) void awq_gemm_sm_kernel(
     const bf16_t* __restrict__ x, const uint32_t* __restrict__ qw, const bf16_t* __restrict__ scales,
-    const uint8_t* __restrict__ zeros, const float* __restrict__ rsum, bf16_t* __restrict__ y,
+    const uint8_t* __restrict__ zeros, const bf16_t* __restrict__ sp, bf16_t* __restrict__ y,
     float* __restrict__ part, int M, int N, int K, int groups_per_split) {
   const int lane = threadIdx.x & 63, wave = wave_id();
   const int l32 = lane & 31, h = lane >> 5;
-  const int nt = blockIdx.x, mt = blockIdx.y, sp = blockIdx.z;
-  const int m0 = mt * kAwqBM;
-  const int n = nt * kAwqBN + 32 * wave + l32;     // this lane's column
+  const int nt = blockIdx.x, mt = blockIdx.y, spl = blockIdx.z;
+  const int m0 = mt * 64;
+  const int n = nt * 128 + 32 * wave + l32;     // this lane's column
   const int groups = K / kAwqGroup;
-  const int g_begin = sp * groups_per_split;
+  const int g_begin = spl * groups_per_split;
   const int g_end = min(groups, g_begin + groups_per_split);
 
   f32x16 yacc[2];
@@ -79,11 +327,11 @@ __global__ __launch_bounds__(256, 2) void awq_gemm_kernel(
   for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
     for (int j = 0; j < 16; ++j) yacc[mb][j] = 0.f;
-  // A-operand rows of this lane (row l32 of each 32-row block), zero past M
   const int ra0 = m0 + l32, ra1 = m0 + 32 + l32;
   const bf16_t* xa0 = x + (size_t)min(ra0, M - 1) * K + 8 * h;
   const bf16_t* xa1 = x + (size_t)min(ra1, M - 1) * K + 8 * h;
   const bool va0 = ra0 < M, va1 = ra1 < M;
+  const uint32_t kMask = in_vgpr(0x000F000Fu), kMagic = in_vgpr(0x43004300u);
 
   for (int g = g_begin; g < g_end; ++g) {
     const uint32_t* wp = qw + ((size_t)g * N + n) * 16 + 8 * h;
@@ -96,27 +344,33 @@ __global__ __launch_bounds__(256, 2) void awq_gemm_kernel(
 #pragma unroll
     for (int t = 0; t < 8; ++t) {
       const uint32_t word = t < 4 ? w0[t] : w1[t - 4];
-      const bf16x8 b = codes_to_bf16(word);
+      const bf16x8 b = codes_to_bf16(word, kMask, kMagic);
       u32x4 z4 = {0, 0, 0, 0};
       const bf16x8 a0 = as_bf16x8(va0 ? load16(xa0 + kg + 16 * t) : z4);
       const bf16x8 a1 = as_bf16x8(va1 ? load16(xa1 + kg + 16 * t) : z4);
       p0 = mfma32(a0, b, p0);
       p1 = mfma32(a1, b, p1);
     }
-    // epilogue: rows 8(j/4) + 4h + j%4 of each block
-    const float* sg = rsum + (size_t)g * M;
+    const bf16_t* sg = sp + (size_t)g * M * 8;
 #pragma unroll
     for (int mb = 0; mb < 2; ++mb) {
-      const f32x16& p = mb ? p1 : p0;
+      const f32x16& pv = mb ? p1 : p0;
 #pragma unroll
       for (int a = 0; a < 4; ++a) {
-        const int r = m0 + 32 * mb + 8 * a + 4 * h;
+        const int rw = m0 + 32 * mb + 8 * a + 4 * h;
         float sv[4];
 #pragma unroll
-        for (int b = 0; b < 4; ++b) sv[b] = r + b < M ? sg[r + b] : 0.f;
+        for (int b = 0; b < 4; ++b) {
+          sv[b] = 0.f;
+          if (rw + b < M) {
+            const u32x2 pc = *reinterpret_cast<const u32x2*>(sg + (size_t)(rw + b) * 8);
+            sv[b] = (bf16_to_f32(pc[0] & 0xFFFFu) + bf16_to_f32(pc[0] >> 16)) +
+                    bf16_to_f32(pc[1] & 0xFFFFu);
+          }
+        }
 #pragma unroll
         for (int b = 0; b < 4; ++b)
-          yacc[mb][4 * a + b] = fmaf(sc, fmaf(-zz, sv[b], p[4 * a + b]), yacc[mb][4 * a + b]);
+          yacc[mb][4 * a + b] = fmaf(sc, fmaf(-zz, sv[b], pv[4 * a + b]), yacc[mb][4 * a + b]);
       }
     }
   }
@@ -124,13 +378,13 @@ __global__ __launch_bounds__(256, 2) void awq_gemm_kernel(
   for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
     for (int j = 0; j < 16; ++j) {
-      const int r = m0 + 32 * mb + 8 * (j >> 2) + 4 * h + (j & 3);
-      if (r >= M) continue;
+      const int rw = m0 + 32 * mb + 8 * (j >> 2) + 4 * h + (j & 3);
+      if (rw >= M) continue;
       if constexpr (kSplit) {
-        part[((size_t)sp * M + r) * N + n] = yacc[mb][j];
+        part[((size_t)spl * M + rw) * N + n] = yacc[mb][j];
       } else {
         const __bf16 v = (__bf16)yacc[mb][j];
-        y[(size_t)r * N + n] = __builtin_bit_cast(bf16_t, v);
+        y[(size_t)rw * N + n] = __builtin_bit_cast(bf16_t, v);
       }
     }
 }
@@ -148,40 +402,66 @@ __global__ __launch_bounds__(256) void awq_reduce_kernel(const float* __restrict
 }
 
 AwqPlan awq_plan(int M, int N, int K) {
-  AwqPlan p;
+  AwqPlan p{};
   p.groups = K / kAwqGroup;
-  p.tiles = (int64_t)((M + kAwqBM - 1) / kAwqBM) * (N / kAwqBN);
-  // Fewer tiles than about two per CU: split the groups.
+  p.large = M > 64 && N % awq_lg::kBN == 0;
+  if (p.large) {
+    p.tiles_m = (M + awq_lg::kBM - 1) / awq_lg::kBM;
+    p.tiles_n = N / awq_lg::kBN;
+  } else {
+    p.tiles_m = (M + 63) / 64;
+    p.tiles_n = N / 128;
+  }
+  p.tiles = (int64_t)p.tiles_m * p.tiles_n;
+  p.tiles_per_xcd = (int)((p.tiles + kNumXcd - 1) / kNumXcd);
+  // Fewer tiles than resident workgroups: split the groups.
+  const int64_t resident = p.large ? kAwqCus : 2 * kAwqCus;
   int splits = 1;
-  if (p.tiles > 0 && p.tiles < 512) splits = (int)std::min<int64_t>(p.groups, 512 / p.tiles);
-  p.groups_per_split = (p.groups + splits - 1) / std::max(splits, 1);
-  p.splits = std::max(1, (p.groups + p.groups_per_split - 1) / std::max(p.groups_per_split, 1));
+  if (p.tiles > 0 && p.tiles < resident)
+    splits = (int)std::min<int64_t>(p.groups, (2 * resident) / p.tiles);
+  p.groups_per_split = (p.groups + std::max(splits, 1) - 1) / std::max(splits, 1);
+  p.splits = (p.groups + p.groups_per_split - 1) / p.groups_per_split;
   const size_t up = 255;
-  p.rsum_bytes = ((size_t)p.groups * M * sizeof(float) + up) & ~up;
+  p.sp_bytes = ((size_t)p.groups * M * 16 + up) & ~up;
   p.part_bytes = p.splits > 1 ? (size_t)p.splits * M * N * sizeof(float) : 0;
   return p;
 }
 
 hipError_t launch_awq_gemm(const AwqArgs& a, hipStream_t stream) {
   const AwqPlan p = awq_plan(a.M, a.N, a.K);
-  float* rsum = reinterpret_cast<float*>(a.workspace);
-  float* part = reinterpret_cast<float*>(static_cast<char*>(a.workspace) + p.rsum_bytes);
+  bf16_t* sp = reinterpret_cast<bf16_t*>(a.workspace);
+  float* part = reinterpret_cast<float*>(static_cast<char*>(a.workspace) + p.sp_bytes);
   const int64_t nsum = (int64_t)p.groups * a.M;
-  hipLaunchKernelGGL(awq_row_sums_kernel, dim3((unsigned)((nsum + 255) / 256)), dim3(256), 0,
-                     stream, (const bf16_t*)a.x, rsum, a.M, a.K);
-  const dim3 grid((unsigned)(a.N / kAwqBN), (unsigned)((a.M + kAwqBM - 1) / kAwqBM),
-                  (unsigned)p.splits);
-  if (p.splits > 1) {
-    hipLaunchKernelGGL(awq_gemm_kernel<true>, grid, dim3(256), 0, stream, (const bf16_t*)a.x,
-                       (const uint32_t*)a.qweight, (const bf16_t*)a.scales, a.zeros, rsum,
-                       (bf16_t*)a.y, part, a.M, a.N, a.K, p.groups_per_split);
+  hipLaunchKernelGGL(awq_group_sums_kernel, dim3((unsigned)((nsum + 255) / 256)), dim3(256), 0,
+                     stream, (const bf16_t*)a.x, sp, a.M, a.K);
+  const bf16_t* x = (const bf16_t*)a.x;
+  const uint32_t* qw = (const uint32_t*)a.qweight;
+  const bf16_t* sc = (const bf16_t*)a.scales;
+  bf16_t* y = (bf16_t*)a.y;
+  const bool split = p.splits > 1;
+  if (p.large) {
+    const dim3 grid((unsigned)(p.tiles_per_xcd * kNumXcd), (unsigned)p.splits);
+    if (split)
+      hipLaunchKernelGGL(awq_gemm_lg_kernel<true>, grid, dim3(awq_lg::kThreads), 0, stream, x, qw,
+                         sc, a.zeros, sp, y, part, a.M, a.N, a.K, p.groups_per_split, p.tiles_m,
+                         p.tiles_n, p.tiles_per_xcd);
+    else
+      hipLaunchKernelGGL(awq_gemm_lg_kernel<false>, grid, dim3(awq_lg::kThreads), 0, stream, x,
+                         qw, sc, a.zeros, sp, y, part, a.M, a.N, a.K, p.groups_per_split,
+                         p.tiles_m, p.tiles_n, p.tiles_per_xcd);
+  } else {
+    const dim3 grid((unsigned)p.tiles_n, (unsigned)p.tiles_m, (unsigned)p.splits);
+    if (split)
+      hipLaunchKernelGGL(awq_gemm_sm_kernel<true>, grid, dim3(256), 0, stream, x, qw, sc, a.zeros,
+                         sp, y, part, a.M, a.N, a.K, p.groups_per_split);
+    else
+      hipLaunchKernelGGL(awq_gemm_sm_kernel<false>, grid, dim3(256), 0, stream, x, qw, sc,
+                         a.zeros, sp, y, part, a.M, a.N, a.K, p.groups_per_split);
+  }
+  if (split) {
     const int64_t mn = (int64_t)a.M * a.N;
     hipLaunchKernelGGL(awq_reduce_kernel, dim3((unsigned)((mn + 255) / 256)), dim3(256), 0,
-                       stream, part, (bf16_t*)a.y, mn, p.splits);
-  } else {
-    hipLaunchKernelGGL(awq_gemm_kernel<false>, grid, dim3(256), 0, stream, (const bf16_t*)a.x,
-                       (const uint32_t*)a.qweight, (const bf16_t*)a.scales, a.zeros, rsum,
-                       (bf16_t*)a.y, part, a.M, a.N, a.K, p.groups_per_split);
+                       stream, part, y, mn, p.splits);
   }
   return hipGetLastError();
 }

@@ -58,9 +58,11 @@ struct AwqArgs {
 };
 
 struct AwqPlan {
+  bool large;                   // 128 x 256 tiles, LDS-staged (else 64 x 128 direct)
   int groups, splits, groups_per_split;
+  int tiles_m, tiles_n, tiles_per_xcd;
   int64_t tiles;
-  size_t rsum_bytes, part_bytes;
+  size_t sp_bytes, part_bytes;  // group-sum pieces, split partials
 };
 
 // Launch-grid sizes, exposed so the host can check them before launching.

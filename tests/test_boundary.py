@@ -198,7 +198,8 @@ def _awq(**kw):
     (dict(x=None), binding.RAG_ERR_INVALID_ARG),
     (dict(z=None), binding.RAG_ERR_INVALID_ARG),
     (dict(x=FAKE + 8), binding.RAG_ERR_INVALID_ARG),
-    (dict(s=FAKE + 1), binding.RAG_ERR_INVALID_ARG),
+    (dict(s=FAKE + 2), binding.RAG_ERR_INVALID_ARG),
+    (dict(z=FAKE + 8), binding.RAG_ERR_INVALID_ARG),
     (dict(M=-1), binding.RAG_ERR_INVALID_ARG),
     (dict(N=0), binding.RAG_ERR_INVALID_ARG),
     (dict(G=64), binding.RAG_ERR_UNSUPPORTED),
@@ -221,13 +222,15 @@ def test_awq_workspace_size():
     ws = binding.rag_awq_workspace_size
     assert ws(0, 256, 512) == 0
     assert ws(64, 256, 500) == 0 and ws(64, 256, 512, 64) == 0
-    # enough tiles to fill the GPU: only the per-group row sums, 256-byte rounded
+    # enough tiles to fill the GPU: only the group-sum pieces, 16 bytes per
+    # (group, row), 256-byte rounded
     M, N, K = 4096, 4096, 4096
-    assert ws(M, N, K) == (K // 128) * M * 4
+    assert ws(M, N, K) == (K // 128) * M * 16
     # one tile row of a wide decode batch: group sums plus fp32 split partials
-    small = ws(16, 4096, 4096)
-    assert small > (4096 // 128) * 16 * 4
-    assert (small - 2048) % (16 * 4096 * 4) == 0
+    for M, N, K in ((16, 4096, 4096), (200, 1024, 2048)):
+        pieces = -(-(K // 128) * M * 16 // 256) * 256
+        small = ws(M, N, K)
+        assert small > pieces and (small - pieces) % (M * N * 4) == 0
 
 
 def test_awq_pack_layout():
