@@ -22,6 +22,10 @@ DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-I", INCLUDE, "-I", CSRC,
           "-Wall", "-Wno-unused-result"]
 
+# Per-source device flags.  The int4 GEMM keeps its MFMA accumulators in
+# ordinary VGPRs, where the per-group rescaling (a VALU multiply) can reach
+# them without AGPR copies.
+SOURCE_FLAGS = {"awq_gemm.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]}
 SOURCES = ["kernels.hip", "kv_cache.hip", "awq_gemm.hip", "api.cpp", "awq_api.cpp", "planner.cpp"]
 HEADERS = ["common.h", "prefill_tile.h", "decode_unit.h", "launch.h", "errors.h"]
 
@@ -32,7 +36,8 @@ def build(verbose: bool = False) -> str:
     for src in SOURCES:
         obj = os.path.join(OBJDIR, os.path.splitext(src)[0] + ".o")
         lang = ["-x", "hip"] if src.endswith(".hip") else ["-x", "hip"]
-        cmd = [HIPCC, *COMMON, *DEVICE_FLAGS, *lang, "-c", os.path.join(CSRC, src), "-o", obj]
+        cmd = [HIPCC, *COMMON, *DEVICE_FLAGS, *SOURCE_FLAGS.get(src, []), *lang, "-c",
+               os.path.join(CSRC, src), "-o", obj]
         if verbose:
             print(" ".join(cmd), flush=True)
         subprocess.run(cmd, check=True, stderr=None if verbose else subprocess.PIPE)

@@ -81,29 +81,42 @@ __device__ __forceinline__ float bf16_to_f32(uint32_t bits16) {
 }
 
 // ---------------------------------------------------------------------------
-// Large batches: 8-wave workgroups own 128 x 256 tiles of Y; wave (wm, wn)
-// computes rows 64 wm .. +64 and columns 64 wn .. +64 as 2 x 2 MFMA blocks of
-// 32 x 32.  Per group the workgroup stages in LDS, by direct global -> LDS
-// copies issued two groups ahead into a 3-stage ring:
+// Large batches: 8-wave workgroups (two waves per SIMD) own 128 x 512 tiles
+// of Y; wave w computes all 128 rows and columns 64 w .. +64 as 4 x 2 MFMA
+// blocks of 32 x 32.  Per group the workgroup stages in LDS, by direct
+// global -> LDS copies issued one group ahead into a 2-stage ring:
 //   X   128 rows x 128 k bf16, row r's 16-byte chunk c at position c ^ (r & 15)
 //       (the MFMA A reads of 16 rows then hit 16 distinct bank groups)
-//   W   256 columns x 64 bytes of codes, the 16-byte chunk j of column c at
+//   W   512 columns x 64 bytes of codes, the 16-byte chunk j of column c at
 //       position j ^ ((c >> 2) & 3) within its 1 KB copy block
 //   SP  128 rows x 16 bytes of group-sum pieces
-//   SZ  256 bf16 scales then 256 uint8 zero points
+//   SZ  512 bf16 scales then 512 uint8 zero points
+//
+// Scale handling.  Each scale is split exactly as s = m * 2^e with |m| in
+// [1, 2).  The power of two goes into the B operands: the magic constant's
+// exponent field becomes 134 + e, so a code turns into (128 + q) 2^e, still
+// exact in bf16 (likewise -(128 + z) 2^e for the zero-point term).  The
+// accumulators hold u = y / c with c the m of the column's last group: before
+// group g they are multiplied by c / m[g, n] (one fp32 multiply per element;
+// the ratio lies in (1/2, 2), so u never leaves the range of y), then every
+// MFMA of group g (the zero-point term and the 8 k-steps) accumulates
+// straight into them, and y = u * c at the end.  There is no separate
+// per-group accumulator, which is what lets a wave hold a 128 x 64 tile and
+// convert each code word once for 4 row blocks.  A zero scale turns the
+// column's operands to zero (mask and magic 0) and leaves c as it was.
 // ---------------------------------------------------------------------------
 namespace awq_lg {
 constexpr int kThreads = 512;
 constexpr int kBM = 128;
-constexpr int kBN = 256;
-constexpr int kStages = 3;
+constexpr int kBN = 512;
+constexpr int kStages = 2;
 constexpr int kX = kBM * kAwqGroup * 2;          // 32768
 constexpr int kW = kBN * kAwqGroup / 2;          // 16384
 constexpr int kSP = kBM * 16;                    // 2048
-constexpr int kSZ = kBN * 3;                     // 768
-constexpr int kStage = kX + kW + kSP + kSZ;      // 51968
+constexpr int kSZ = kBN * 3;                     // 1536
+constexpr int kStage = kX + kW + kSP + kSZ;      // 69120
 constexpr int kGroupM = 8;                       // M tiles per raster group
-constexpr int kOutStride = 160;                  // bytes per row of the output transpose
+constexpr int kOutStride = 144;                  // bytes per row of the output transpose
 static_assert(kStage % 16 == 0, "stage alignment");
 static_assert(8 * 64 * kOutStride <= kStages * kStage, "output transpose fits");
 }  // namespace awq_lg
@@ -113,6 +126,41 @@ template <int n>
 __device__ __forceinline__ void wait_vm() {
   static_assert(n >= 0 && n < 64, "vmcnt range");
   __builtin_amdgcn_s_waitcnt(0x0F70 | (n & 15) | ((n >> 4) << 14));
+}
+
+// Per-column constants of one group from its bf16 scale bits: c = sign * m,
+// the conversion mask and magic (exponent field 134 + e), and the bf16 bits of
+// -(128 + z) 2^e.  Scales of 2^121 and above keep the excess power of two in
+// c; a zero scale gives mask = magic = nz = 0 and c = 0 (the caller keeps its
+// reference); inf or NaN gives c = NaN.
+struct ColScale {
+  float c;
+  uint32_t mask, magic, nz;
+};
+__device__ __forceinline__ ColScale col_scale(uint32_t sb, uint32_t z) {
+  const uint32_t E = (sb >> 7) & 0xFFu, mt = sb & 0x7Fu;
+  int e;
+  uint32_t mbits;
+  if (E == 0) {                                   // bf16 subnormal: mt * 2^-133
+    const int k = 31 - __builtin_clz(mt | 1u);
+    mbits = (mt << (7 - k)) & 0x7Fu;
+    e = k - 133;
+  } else {
+    mbits = mt;
+    e = (int)E - 127;
+  }
+  const int eb = min(e, 120);
+  float c = bf16_to_f32((sb & 0x8000u) | 0x3F80u | mbits);
+  if (e > eb) c = ldexpf(c, e - eb);
+  if (E == 0xFFu) c = __builtin_nanf("");
+  const bool zero = (sb & 0x7FFFu) == 0;
+  const uint32_t ex = (uint32_t)(134 + eb) << 7;
+  ColScale r;
+  r.c = zero ? 0.f : c;
+  r.mask = zero ? 0u : 0x000F000Fu;
+  r.magic = zero ? 0u : ex | (ex << 16);
+  r.nz = zero ? 0u : 0x8000u | ex | z;
+  return r;
 }
 
 template <bool kSplit>
@@ -142,81 +190,81 @@ __global__ __launch_bounds__(awq_lg::kThreads) void awq_gemm_lg_kernel(
   const int n_groups = min(groups, g_begin + groups_per_split) - g_begin;
 
   // ---- copies of one group into one stage (each wave its share) ----
+  // Per-lane byte offsets do not depend on the group: computed once.
+  uint32_t xoff[4], woff[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int row = 4 * (4 * w + j) + (lane >> 4);
+    const int c = (lane & 15) ^ (row & 15);
+    const int rr = min(m0 + row, M - 1) - m0;
+    xoff[j] = (uint32_t)(rr * K * 2 + c * 16);
+  }
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int cl = lane >> 2;
+    const int ch = (lane & 3) ^ ((cl >> 2) & 3);
+    const int col = min(16 * (4 * w + j) + cl, N - 1 - n0);
+    woff[j] = (uint32_t)((col * 16 + ch * 4) * 4);
+  }
+  const uint32_t spoff = (uint32_t)(min(m0 + 64 * (w & 1) + lane, M - 1) * 16);
+  const uint32_t szoff = w == 2 ? (uint32_t)(2 * min(n0 + 8 * lane, N - 8))
+                                : (uint32_t)min(n0 + 16 * lane, N - 16);
   auto issue = [&](int g, int st) {
     char* S = lds + st * kStage;
     const bf16_t* xb = x + (size_t)m0 * K + (size_t)g * kAwqGroup;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int i = 4 * w + j;
-      const int row = 4 * i + (lane >> 4);
-      const int c = (lane & 15) ^ (row & 15);
-      const int rr = min(m0 + row, M - 1) - m0;
-      dma16_s(xb, (uint32_t)(rr * K * 2 + c * 16), (bf16_t*)(S + i * 1024));
-    }
+    for (int j = 0; j < 4; ++j) dma16_s(xb, xoff[j], (bf16_t*)(S + (4 * w + j) * 1024));
     const uint32_t* wb = qw + ((size_t)g * N + n0) * 16;
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int i = 2 * w + j;
-      const int cl = lane >> 2;
-      const int ch = (lane & 3) ^ ((cl >> 2) & 3);
-      const int col = min(16 * i + cl, N - 1 - n0);
-      dma16_s(wb, (uint32_t)((col * 16 + ch * 4) * 4), (bf16_t*)(S + kX + i * 1024));
-    }
+    for (int j = 0; j < 4; ++j) dma16_s(wb, woff[j], (bf16_t*)(S + kX + (4 * w + j) * 1024));
     if (w < 2) {
-      const int rr = min(m0 + 64 * w + lane, M - 1);
-      dma16(sp + ((size_t)g * M + rr) * 8, (bf16_t*)(S + kX + kW + w * 1024));
+      dma16_s(sp + (size_t)g * M * 8, spoff, (bf16_t*)(S + kX + kW + w * 1024));
     } else if (w == 2) {
-      const void* src = lane < 32
-          ? (const void*)(scales + (size_t)g * N + min(n0 + 8 * lane, N - 8))
-          : (const void*)(zeros + (size_t)g * N + min(n0 + 16 * (lane - 32), N - 16));
-      if (lane < 48) dma16(src, (bf16_t*)(S + kX + kW + kSP));
+      dma16((const char*)(scales + (size_t)g * N) + szoff, (bf16_t*)(S + kX + kW + kSP));
+    } else if (w == 3) {
+      if (lane < 32) dma16(zeros + (size_t)g * N + szoff, (bf16_t*)(S + kX + kW + kSP + 1024));
     }
   };
-  // copies per wave per group: 7 for waves 0-2, 6 for the others
-  auto wait_group = [&](bool one_more_in_flight) {
-    if (!one_more_in_flight) {
-      wait_vm<0>();
-    } else if (w < 3) {
-      wait_vm<7>();
-    } else {
-      wait_vm<6>();
-    }
-  };
-
-  const int wm = w >> 2, wn = w & 3;
   const int r = lane & 31, h = lane >> 5;
-  const uint32_t kMask = in_vgpr(0x000F000Fu), kMagic = in_vgpr(0x43004300u);
-  f32x16 yacc[2][2];
+  f32x16 u[4][2];
 #pragma unroll
-  for (int a = 0; a < 2; ++a)
+  for (int a = 0; a < 4; ++a)
 #pragma unroll
     for (int b = 0; b < 2; ++b)
 #pragma unroll
-      for (int j = 0; j < 16; ++j) yacc[a][b][j] = 0.f;
+      for (int j = 0; j < 16; ++j) u[a][b][j] = 0.f;
+  float cref[2] = {1.f, 1.f};
 
   if (n_groups > 0) issue(g_begin, 0);
-  if (n_groups > 1) issue(g_begin + 1, 1);
   for (int it = 0; it < n_groups; ++it) {
-    wait_group(it + 1 < n_groups);
+    // this group's copies have landed (the only ones in flight) and every
+    // wave is done with the stage the next group's copies overwrite
+    wait_vm<0>();
     __syncthreads();
-    if (it + 2 < n_groups) issue(g_begin + it + 2, (it + 2) % kStages);
+    if (it + 1 < n_groups) issue(g_begin + it + 1, (it + 1) % kStages);
     const char* S = lds + (it % kStages) * kStage;
     const char* SX = S;
     const char* SW = S + kX;
     const char* SPc = S + kX + kW;
     const char* SZ = S + kX + kW + kSP;
 
-    float sc[2];
+    float rho[2];
+    uint32_t mask[2], magic[2];
     bf16x8 bz[2];
     u32x4 words[2][2];
 #pragma unroll
     for (int nb = 0; nb < 2; ++nb) {
-      const int cl = 64 * wn + 32 * nb + r;
-      sc[nb] = bf16_to_f32(*reinterpret_cast<const uint16_t*>(SZ + 2 * cl));
-      const uint32_t nz = 0xC300u | SZ[512 + cl];   // bf16 -(128 + z)
+      const int cl = 64 * w + 32 * nb + r;
+      const ColScale cs = col_scale(*reinterpret_cast<const uint16_t*>(SZ + 2 * cl),
+                                    (uint8_t)SZ[1024 + cl]);
+      const bool zero = cs.mask == 0u;
+      rho[nb] = zero ? 1.f : cref[nb] * __builtin_amdgcn_rcpf(cs.c);
+      cref[nb] = zero ? cref[nb] : cs.c;
+      mask[nb] = in_vgpr(cs.mask);
+      magic[nb] = in_vgpr(cs.magic);
       u32x4 b;
-      b[0] = nz | (nz << 16);
-      b[1] = nz;
+      b[0] = cs.nz | (cs.nz << 16);
+      b[1] = cs.nz;
       b[2] = 0;
       b[3] = 0;
       bz[nb] = as_bf16x8(b);
@@ -227,78 +275,100 @@ __global__ __launch_bounds__(awq_lg::kThreads) void awq_gemm_lg_kernel(
         words[nb][q] = *reinterpret_cast<const u32x4*>(SW + blk * 1024 + ci * 64 + ch * 16);
       }
     }
-    f32x16 p[2][2];
+    auto a_op = [&](int mb, int t) {
+      return as_bf16x8(*reinterpret_cast<const u32x4*>(
+          SX + (32 * mb + r) * 256 + (((2 * t + h) ^ (r & 15)) * 16)));
+    };
+    bf16x8 acur[4];
 #pragma unroll
-    for (int mb = 0; mb < 2; ++mb) {
-      const int row = 64 * wm + 32 * mb + r;
-      u32x4 az = *reinterpret_cast<const u32x4*>(SPc + row * 16);
-      if (h) az = u32x4{0, 0, 0, 0};
-      const f32x16 zero = {};
+    for (int mb = 0; mb < 4; ++mb) acur[mb] = a_op(mb, 0);
+    // u <- u * c / m, then the group's MFMAs accumulate into u
 #pragma unroll
-      for (int nb = 0; nb < 2; ++nb) p[mb][nb] = mfma32(as_bf16x8(az), bz[nb], zero);
+    for (int mb = 0; mb < 4; ++mb) {
+      u32x4 v = *reinterpret_cast<const u32x4*>(SPc + (32 * mb + r) * 16);
+      if (h) v = u32x4{0, 0, 0, 0};
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb) {
+#pragma unroll
+        for (int j = 0; j < 16; ++j) u[mb][nb][j] *= rho[nb];
+        u[mb][nb] = mfma32(as_bf16x8(v), bz[nb], u[mb][nb]);
+      }
     }
 #pragma unroll
     for (int t = 0; t < 8; ++t) {
-      bf16x8 a[2], b[2];
+      // one k-step at a time (the A operands of step t + 1 are loaded during
+      // step t, no earlier: the accumulators need the registers)
+      __builtin_amdgcn_sched_barrier(0);
+      bf16x8 anxt[4];
+      if (t < 7) {
 #pragma unroll
-      for (int mb = 0; mb < 2; ++mb) {
-        const int row = 64 * wm + 32 * mb + r;
-        a[mb] = as_bf16x8(*reinterpret_cast<const u32x4*>(SX + row * 256 +
-                                                          (((2 * t + h) ^ (r & 15)) * 16)));
+        for (int mb = 0; mb < 4; ++mb) anxt[mb] = a_op(mb, t + 1);
       }
-#pragma unroll
-      for (int nb = 0; nb < 2; ++nb) b[nb] = codes_to_bf16(words[nb][t >> 2][t & 3], kMask, kMagic);
-#pragma unroll
-      for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-        for (int nb = 0; nb < 2; ++nb) p[mb][nb] = mfma32(a[mb], b[nb], p[mb][nb]);
-    }
-#pragma unroll
-    for (int mb = 0; mb < 2; ++mb)
+      bf16x8 b[2];
 #pragma unroll
       for (int nb = 0; nb < 2; ++nb)
+        b[nb] = codes_to_bf16(words[nb][t >> 2][t & 3], mask[nb], magic[nb]);
 #pragma unroll
-        for (int j = 0; j < 16; ++j) yacc[mb][nb][j] = fmaf(sc[nb], p[mb][nb][j], yacc[mb][nb][j]);
+      for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+        for (int nb = 0; nb < 2; ++nb) u[mb][nb] = mfma32(acur[mb], b[nb], u[mb][nb]);
+      if (t < 7) {
+#pragma unroll
+        for (int mb = 0; mb < 4; ++mb) acur[mb] = anxt[mb];
+      }
+    }
   }
+#pragma unroll
+  for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+      for (int j = 0; j < 16; ++j) u[mb][nb][j] *= cref[nb];
 
   // ---- output ----
-  const bool cols_in = n0 + 64 * wn < N;
+  const bool cols_in = n0 + 64 * w < N;
   if constexpr (kSplit) {
     if (!cols_in) return;
 #pragma unroll
-    for (int mb = 0; mb < 2; ++mb)
+    for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
       for (int nb = 0; nb < 2; ++nb)
 #pragma unroll
         for (int j = 0; j < 16; ++j) {
-          const int row = m0 + 64 * wm + 32 * mb + 8 * (j >> 2) + 4 * h + (j & 3);
+          const int row = m0 + 32 * mb + 8 * (j >> 2) + 4 * h + (j & 3);
           if (row < M)
-            part[((size_t)blockIdx.y * M + row) * N + n0 + 64 * wn + 32 * nb + r] = yacc[mb][nb][j];
+            part[((size_t)blockIdx.y * M + row) * N + n0 + 64 * w + 32 * nb + r] = u[mb][nb][j];
         }
   } else {
-    // transpose through LDS so that each lane stores 16 contiguous bytes
+    // transpose through LDS so that each lane stores 16 contiguous bytes,
+    // 64 rows at a time
     __syncthreads();
     char* T = lds + w * 64 * kOutStride;
 #pragma unroll
-    for (int mb = 0; mb < 2; ++mb)
+    for (int half = 0; half < 2; ++half) {
 #pragma unroll
-      for (int nb = 0; nb < 2; ++nb)
+      for (int mh = 0; mh < 2; ++mh)
 #pragma unroll
-        for (int j = 0; j < 16; ++j) {
-          const int row = 32 * mb + 8 * (j >> 2) + 4 * h + (j & 3);
-          const __bf16 v = (__bf16)yacc[mb][nb][j];
-          *reinterpret_cast<__bf16*>(T + row * kOutStride + 2 * (32 * nb + r)) = v;
+        for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+          for (int j = 0; j < 16; ++j) {
+            const int row = 32 * mh + 8 * (j >> 2) + 4 * h + (j & 3);
+            const __bf16 v = (__bf16)u[2 * half + mh][nb][j];
+            *reinterpret_cast<__bf16*>(T + row * kOutStride + 2 * (32 * nb + r)) = v;
+          }
+      wave_lds_sync();
+      if (cols_in) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          const int idx = 64 * i + lane;
+          const int row = idx >> 3, ch = idx & 7;
+          const int grow = m0 + 64 * half + row;
+          const u32x4 v = *reinterpret_cast<const u32x4*>(T + row * kOutStride + ch * 16);
+          if (grow < M)
+            *reinterpret_cast<u32x4*>(y + (size_t)grow * N + n0 + 64 * w + 8 * ch) = v;
         }
-    wave_lds_sync();
-    if (!cols_in) return;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int idx = 64 * i + lane;
-      const int row = idx >> 3, ch = idx & 7;
-      const int grow = m0 + 64 * wm + row;
-      const u32x4 v = *reinterpret_cast<const u32x4*>(T + row * kOutStride + ch * 16);
-      if (grow < M)
-        *reinterpret_cast<u32x4*>(y + (size_t)grow * N + n0 + 64 * wn + 8 * ch) = v;
+      }
+      wave_lds_sync();
     }
   }
 }
@@ -404,10 +474,10 @@ __global__ __launch_bounds__(256) void awq_reduce_kernel(const float* __restrict
 AwqPlan awq_plan(int M, int N, int K) {
   AwqPlan p{};
   p.groups = K / kAwqGroup;
-  p.large = M > 64 && N % awq_lg::kBN == 0;
+  p.large = M > 64;
   if (p.large) {
     p.tiles_m = (M + awq_lg::kBM - 1) / awq_lg::kBM;
-    p.tiles_n = N / awq_lg::kBN;
+    p.tiles_n = (N + awq_lg::kBN - 1) / awq_lg::kBN;
   } else {
     p.tiles_m = (M + 63) / 64;
     p.tiles_n = N / 128;
