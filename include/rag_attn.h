@@ -346,8 +346,10 @@ rag_status rag_device_free_memory(size_t *free_bytes, size_t *total_bytes);
  *
  * rag_awq_pack_weights (host only) packs codes for the kernel:
  *   q       host uint8 [K, N], each 0..15
- *   packed  host int32 [K / 128, N, 16] (K * N / 8 words), library-defined
- *           order: 32 contiguous bytes per (group, column, half of the group)
+ *   packed  host int32 [K / 128, N, 16] (K * N / 8 words): the 64 bytes of
+ *           (group g, column n) are contiguous; word 8a + 4b + c holds the
+ *           codes of k = 128 g + 8 (4c + 2b + a) + j, j = 0..7, code j in
+ *           bits 4 (j / 2) + 16 (j % 2) .. +4
  * Returns RAG_OK, RAG_ERR_INVALID_ARG (null pointer, a code above 15, N or K
  * not positive) or RAG_ERR_UNSUPPORTED (group_size not 128, K or N not a
  * multiple of 128).
@@ -357,9 +359,10 @@ rag_status rag_awq_pack_weights(const uint8_t *q, int32_t K, int32_t N,
 
 /* Bytes of workspace rag_awq_gemm needs (0 for M == 0 or invalid shapes).
  * Library-internal layout: the group sums of x [K / 128, M] (each as three
- * bf16 pieces in 16 bytes), then, when the output tiles are too few to fill
- * the GPU, fp32 partial outputs [splits, M, N] of a split over the groups
- * (reduced in a fixed order, so results do not depend on timing). */
+ * bf16 pieces in 16 bytes), then, for M > 64 with too few output tiles to
+ * fill the GPU, fp32 partial outputs [splits, M, N] of a split over the
+ * groups (added in a fixed order, so results do not depend on timing), or,
+ * for M <= 64, a group-major copy of x with M padded to 16, 32 or 64 rows. */
 size_t rag_awq_workspace_size(int32_t M, int32_t N, int32_t K,
                               int32_t group_size);
 

@@ -39,7 +39,7 @@ extern "C" {
 size_t rag_awq_workspace_size(int32_t M, int32_t N, int32_t K, int32_t group_size) {
   if (check_shape("awq workspace", M, N, K, group_size) != RAG_OK || M == 0) return 0;
   const rag::AwqPlan p = rag::awq_plan(M, N, K);
-  return p.sp_bytes + p.part_bytes;
+  return p.sp_bytes + p.part_bytes + p.xr_bytes;
 }
 
 rag_status rag_awq_pack_weights(const uint8_t* q, int32_t K, int32_t N, int32_t group_size,
@@ -51,12 +51,12 @@ rag_status rag_awq_pack_weights(const uint8_t* q, int32_t K, int32_t N, int32_t 
   for (int32_t g = 0; g < groups; ++g)
     for (int32_t n = 0; n < N; ++n)
       for (int32_t w = 0; w < 16; ++w) {
-        // word 8h + t holds k = 128g + 16t + 8h + j, code j at bits
-        // 4(j/2) + 16(j%2)
-        const int32_t h = w / 8, t = w % 8;
+        // word 8a + 4b + c holds the 8 codes of k = 128g + 8o + j with
+        // o = 4c + 2b + a, code j at bits 4(j/2) + 16(j%2)
+        const int32_t o = 4 * (w & 3) + 2 * ((w >> 2) & 1) + (w >> 3);
         uint32_t word = 0;
         for (int32_t j = 0; j < 8; ++j) {
-          const int64_t k = (int64_t)g * kGroup + 16 * t + 8 * h + j;
+          const int64_t k = (int64_t)g * kGroup + 8 * o + j;
           const uint8_t c = q[k * N + n];
           if (c > 15)
             return fail(RAG_ERR_INVALID_ARG, "awq pack: code %u at (k=%lld, n=%d) is not 4-bit",

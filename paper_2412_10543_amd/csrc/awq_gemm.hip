@@ -14,11 +14,15 @@
 // the pieces, B = -(128 + z), which bf16 holds exactly as bits 0xC300 | z),
 // so the per-group scale is one fp32 FMA per output element.
 //
-// Packed weight layout (rag_awq_pack_weights): int32 [K/128][N][16].  Word
-// 8h + t of column n in group g holds the codes of k = 128g + 16t + 8h + j,
-// j = 0..7, code j in bits 4(j/2) + 16(j%2) .. +4.  MFMA B-operand lane
-// (column c, half h) at k-step t needs word 8h + t of its column; a column's
-// 16 words of one group are 64 contiguous bytes.
+// Packed weight layout (rag_awq_pack_weights): int32 [K/128][N][16].  The
+// 16 words of (group g, column n) are 64 contiguous bytes; word
+// 8a + 4b + c holds the codes of the k-octet o = 4c + 2b + a, i.e. of
+// k = 128g + 8o + j, j = 0..7, code j in bits 4(j/2) + 16(j%2) .. +4.  This
+// order serves both MFMA shapes with contiguous reads: a 32x32x16 B-operand
+// lane (column, half h) needs the octets 2t + h of k-steps t = 0..7, which
+// are words 8h .. 8h+7 (step t at 8h + 4(t&1) + t/2); a 16x16x32 lane
+// (column, quarter qq) needs the octets 4t + qq of k-steps t = 0..3, words
+// 8(qq&1) + 4(qq>>1) .. +3.
 #include "common.h"
 #include "launch.h"
 
@@ -28,21 +32,42 @@ constexpr int kAwqGroup = 128;
 constexpr int kAwqCus = 256;     // MI355X compute units
 
 // S[g, m] = sum over the group of X[m, k] (fp32, k order), stored as bf16
-// pieces [S1, S2, S3, 0, 0, 0, 0, 0] (16 bytes per (g, m)).
+// pieces [S1, S2, S3, 0, 0, 0, 0, 0] (16 bytes per (g, m)).  For small
+// batches (xr non-null) the same pass also writes X group-major in the order
+// the small-batch kernel's 16x16x32 A operands are read, xr[g][b][t][q][r]
+// = the 8 values X[16 b + r][128 g + 32 t + 8 q ..], rows past M as zeros:
+// each of that kernel's activation loads is then 1 KB contiguous instead of
+// 16 rows K apart (which all fall into the same cache sets).
 __global__ __launch_bounds__(256) void awq_group_sums_kernel(const bf16_t* __restrict__ x,
-                                                             bf16_t* __restrict__ sp, int M,
-                                                             int K) {
+                                                             bf16_t* __restrict__ sp,
+                                                             bf16_t* __restrict__ xr, int M,
+                                                             int m_pad, int K) {
   const int groups = K / kAwqGroup;
+  const int rows = xr ? m_pad : M;
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= (int64_t)groups * M) return;
-  const int g = (int)(i / M), m = (int)(i % M);
+  if (i >= (int64_t)groups * rows) return;
+  const int g = (int)(i / rows), m = (int)(i % rows);
+  if (m >= M) {                                    // padding rows of xr
+    bf16_t* dst = xr + ((size_t)(g * (m_pad / 16) + m / 16) * 4 * 64 + (m % 16)) * 8;
+#pragma unroll
+    for (int c = 0; c < kAwqGroup / 8; ++c)
+      *reinterpret_cast<u32x4*>(dst + (size_t)((c >> 2) * 64 + (c & 3) * 16) * 8) = u32x4{0, 0, 0, 0};
+    return;
+  }
   const bf16_t* row = x + (size_t)m * K + (size_t)g * kAwqGroup;
   float acc = 0.f;
 #pragma unroll 4
   for (int c = 0; c < kAwqGroup / 8; ++c) {
-    const bf16x8 v = as_bf16x8(load16(row + 8 * c));
+    const u32x4 raw = load16(row + 8 * c);
+    const bf16x8 v = as_bf16x8(raw);
 #pragma unroll
     for (int e = 0; e < 8; ++e) acc += (float)v[e];
+    if (xr) {
+      // chunk c = 4 t + q of the row
+      bf16_t* dst = xr + ((size_t)(g * (m_pad / 16) + m / 16) * 4 * 64 +
+                          (size_t)((c >> 2) * 64 + (c & 3) * 16 + (m % 16))) * 8;
+      *reinterpret_cast<u32x4*>(dst) = raw;
+    }
   }
   const __bf16 s1 = (__bf16)acc;
   const float r1 = acc - (float)s1;
@@ -54,7 +79,7 @@ __global__ __launch_bounds__(256) void awq_group_sums_kernel(const bf16_t* __res
   out[1] = (uint32_t)__builtin_bit_cast(uint16_t, s3);
   out[2] = 0;
   out[3] = 0;
-  *reinterpret_cast<u32x4*>(sp + (size_t)i * 8) = out;
+  *reinterpret_cast<u32x4*>(sp + ((size_t)g * M + m) * 8) = out;
 }
 
 // A value the compiler must keep in a VGPR (no constant folding).
@@ -307,7 +332,7 @@ __global__ __launch_bounds__(awq_lg::kThreads) void awq_gemm_lg_kernel(
       bf16x8 b[2];
 #pragma unroll
       for (int nb = 0; nb < 2; ++nb)
-        b[nb] = codes_to_bf16(words[nb][t >> 2][t & 3], mask[nb], magic[nb]);
+        b[nb] = codes_to_bf16(words[nb][t & 1][t >> 1], mask[nb], magic[nb]);
 #pragma unroll
       for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
@@ -374,89 +399,146 @@ __global__ __launch_bounds__(awq_lg::kThreads) void awq_gemm_lg_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// Small batches (M <= 64): 4-wave workgroups own 64 x 128 tiles; wave w
-// computes columns 32 w .. +32 of all 64 rows, operands straight from global
-// memory; the zero-point term is applied in fp32 from S = S1 + S2 + S3.
+// Small batches (M <= 64), where streaming the codes from HBM is the cost.
+// 16x16x32 MFMAs (16 rows per block: no padding rows for a decode batch of
+// 16), one 4-wave workgroup per 32 output columns (two 16-column blocks);
+// wave w takes the groups [w R, w R + R), R = ceil(G / 4), and streams them
+// through a ring of 4 / (M / 16) register slots: the code words (16 contiguous
+// bytes per lane and column block), activations, scales, zero points and
+// group-sum pieces of group i + kDepth are requested as soon as group i has
+// taken its slot.  Per group and
+// block: the zero-point MFMA (group-sum pieces times -(128 + z), bf16 exact)
+// opens the chain, 4 k-steps follow, and y += s * P in fp32.  The waves'
+// sums are added in LDS in wave order.
 // ---------------------------------------------------------------------------
-template <bool kSplit>
-__global__ __launch_bounds__(256, 2) void awq_gemm_sm_kernel(
-    const bf16_t* __restrict__ x, const uint32_t* __restrict__ qw, const bf16_t* __restrict__ scales,
-    const uint8_t* __restrict__ zeros, const bf16_t* __restrict__ sp, bf16_t* __restrict__ y,
-    float* __restrict__ part, int M, int N, int K, int groups_per_split) {
-  const int lane = threadIdx.x & 63, wave = wave_id();
-  const int l32 = lane & 31, h = lane >> 5;
-  const int nt = blockIdx.x, mt = blockIdx.y, spl = blockIdx.z;
-  const int m0 = mt * 64;
-  const int n = nt * 128 + 32 * wave + l32;     // this lane's column
+namespace awq_sm {
+constexpr int kWaves = 4;
+constexpr int kThreads = kWaves * 64;
+constexpr int kCols = 32;          // output columns per workgroup
+}  // namespace awq_sm
+
+template <int MB>   // 16-row blocks: M <= 16 MB
+__global__ __launch_bounds__(awq_sm::kThreads) void awq_gemm_sm_kernel(
+    const bf16_t* __restrict__ xr, const uint32_t* __restrict__ qw,
+    const bf16_t* __restrict__ scales, const uint8_t* __restrict__ zeros,
+    const bf16_t* __restrict__ sp, bf16_t* __restrict__ y, int M, int N, int K) {
+  using namespace awq_sm;
+  constexpr int kDepth = 4 / MB;                   // ring slots (registers)
+  constexpr int kOut = MB * 2 * 4;                 // accumulator values per lane
+  __shared__ float red[kWaves * kOut * 64];
+  const int lane = threadIdx.x & 63, w = wave_id();
+  const int c = lane & 15, qq = lane >> 4;
+  const int n0 = kCols * blockIdx.x + c;           // columns n0 and n0 + 16
   const int groups = K / kAwqGroup;
-  const int g_begin = spl * groups_per_split;
-  const int g_end = min(groups, g_begin + groups_per_split);
-
-  f32x16 yacc[2];
-#pragma unroll
-  for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-    for (int j = 0; j < 16; ++j) yacc[mb][j] = 0.f;
-  const int ra0 = m0 + l32, ra1 = m0 + 32 + l32;
-  const bf16_t* xa0 = x + (size_t)min(ra0, M - 1) * K + 8 * h;
-  const bf16_t* xa1 = x + (size_t)min(ra1, M - 1) * K + 8 * h;
-  const bool va0 = ra0 < M, va1 = ra1 < M;
+  const int per_wave = (groups + kWaves - 1) / kWaves;
+  const int g0 = w * per_wave;
+  const int ng = max(0, min(per_wave, groups - g0));
   const uint32_t kMask = in_vgpr(0x000F000Fu), kMagic = in_vgpr(0x43004300u);
+  const int wpos = 8 * (qq & 1) + 4 * (qq >> 1);   // this lane's 4 words
+  int rows[MB];
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) rows[mb] = min(16 * mb + c, M - 1);
 
-  for (int g = g_begin; g < g_end; ++g) {
-    const uint32_t* wp = qw + ((size_t)g * N + n) * 16 + 8 * h;
-    const u32x4 w0 = *reinterpret_cast<const u32x4*>(wp);
-    const u32x4 w1 = *reinterpret_cast<const u32x4*>(wp + 4);
-    const float sc = (float)__builtin_bit_cast(__bf16, scales[(size_t)g * N + n]);
-    const float zz = 128.f + (float)zeros[(size_t)g * N + n];
-    f32x16 p0 = {}, p1 = {};
-    const size_t kg = (size_t)g * kAwqGroup;
+  struct Slot {
+    u32x4 wd[2];
+    u32x4 xa[4][MB];
+    u32x4 az[MB];
+    uint32_t sbits[2], z[2];
+  };
+  // everything one group needs; raw values only (arithmetic on a loaded
+  // value here would wait for the load)
+  auto fetch = [&](int g, Slot& sl) {
 #pragma unroll
-    for (int t = 0; t < 8; ++t) {
-      const uint32_t word = t < 4 ? w0[t] : w1[t - 4];
-      const bf16x8 b = codes_to_bf16(word, kMask, kMagic);
-      u32x4 z4 = {0, 0, 0, 0};
-      const bf16x8 a0 = as_bf16x8(va0 ? load16(xa0 + kg + 16 * t) : z4);
-      const bf16x8 a1 = as_bf16x8(va1 ? load16(xa1 + kg + 16 * t) : z4);
-      p0 = mfma32(a0, b, p0);
-      p1 = mfma32(a1, b, p1);
+    for (int nb = 0; nb < 2; ++nb) {
+      const size_t col = (size_t)g * N + n0 + 16 * nb;
+      sl.wd[nb] = *reinterpret_cast<const u32x4*>(qw + col * 16 + wpos);
+      sl.sbits[nb] = scales[col];
+      sl.z[nb] = zeros[col];
     }
-    const bf16_t* sg = sp + (size_t)g * M * 8;
 #pragma unroll
-    for (int mb = 0; mb < 2; ++mb) {
-      const f32x16& pv = mb ? p1 : p0;
+    for (int t = 0; t < 4; ++t)
 #pragma unroll
-      for (int a = 0; a < 4; ++a) {
-        const int rw = m0 + 32 * mb + 8 * a + 4 * h;
-        float sv[4];
+      for (int mb = 0; mb < MB; ++mb)
+        sl.xa[t][mb] = load16(xr + ((((size_t)g * MB + mb) * 4 + t) * 64 + lane) * 8);
 #pragma unroll
-        for (int b = 0; b < 4; ++b) {
-          sv[b] = 0.f;
-          if (rw + b < M) {
-            const u32x2 pc = *reinterpret_cast<const u32x2*>(sg + (size_t)(rw + b) * 8);
-            sv[b] = (bf16_to_f32(pc[0] & 0xFFFFu) + bf16_to_f32(pc[0] >> 16)) +
-                    bf16_to_f32(pc[1] & 0xFFFFu);
+    for (int mb = 0; mb < MB; ++mb) sl.az[mb] = load16(sp + ((size_t)g * M + rows[mb]) * 8);
+  };
+
+  f32x4 yv[MB][2];
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb) yv[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  if (ng > 0) {
+    Slot ring[kDepth];
+#pragma unroll
+    for (int d = 0; d < kDepth; ++d) fetch(g0 + min(d, ng - 1), ring[d]);
+    const int g_last = g0 + ng - 1;
+    for (int i0 = 0; i0 < ng; i0 += kDepth) {
+#pragma unroll
+      for (int d = 0; d < kDepth; ++d) {
+        const int i = i0 + d;
+        if (i >= ng) break;
+        const int g = g0 + i;
+        // take the slot, refill it (unconditionally: a load issued on one
+        // path only makes the compiler's waits fall back to waiting for all)
+        __builtin_amdgcn_sched_barrier(0);
+        const Slot sl = ring[d];
+        fetch(min(g + kDepth, g_last), ring[d]);
+        __builtin_amdgcn_sched_barrier(0);
+        f32x4 p[MB][2];
+#pragma unroll
+        for (int nb = 0; nb < 2; ++nb) {
+          const uint32_t nz = 0xC300u | sl.z[nb];              // bf16 -(128 + z)
+          const u32x4 bzv = {nz | (nz << 16), nz, 0u, 0u};
+#pragma unroll
+          for (int mb = 0; mb < MB; ++mb) {
+            const u32x4 az = qq ? u32x4{0, 0, 0, 0} : sl.az[mb];
+            p[mb][nb] = mfma16(as_bf16x8(az), as_bf16x8(bzv), f32x4{0.f, 0.f, 0.f, 0.f});
           }
         }
 #pragma unroll
-        for (int b = 0; b < 4; ++b)
-          yacc[mb][4 * a + b] = fmaf(sc, fmaf(-zz, sv[b], pv[4 * a + b]), yacc[mb][4 * a + b]);
+        for (int t = 0; t < 4; ++t)
+#pragma unroll
+          for (int nb = 0; nb < 2; ++nb) {
+            const bf16x8 b = codes_to_bf16(sl.wd[nb][t], kMask, kMagic);
+#pragma unroll
+            for (int mb = 0; mb < MB; ++mb) p[mb][nb] = mfma16(as_bf16x8(sl.xa[t][mb]), b, p[mb][nb]);
+          }
+#pragma unroll
+        for (int nb = 0; nb < 2; ++nb) {
+          const float sc = bf16_to_f32(sl.sbits[nb]);
+#pragma unroll
+          for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) yv[mb][nb][j] = fmaf(sc, p[mb][nb][j], yv[mb][nb][j]);
+        }
       }
     }
   }
+
+  // ---- the waves' sums, added in wave order ----
 #pragma unroll
-  for (int mb = 0; mb < 2; ++mb)
+  for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-    for (int j = 0; j < 16; ++j) {
-      const int rw = m0 + 32 * mb + 8 * (j >> 2) + 4 * h + (j & 3);
-      if (rw >= M) continue;
-      if constexpr (kSplit) {
-        part[((size_t)spl * M + rw) * N + n] = yacc[mb][j];
-      } else {
-        const __bf16 v = (__bf16)yacc[mb][j];
-        y[(size_t)rw * N + n] = __builtin_bit_cast(bf16_t, v);
-      }
+    for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) red[(w * kOut + (mb * 2 + nb) * 4 + j) * 64 + lane] = yv[mb][nb][j];
+  __syncthreads();
+  constexpr int kPer = kOut * 64 / kThreads;       // outputs per thread
+#pragma unroll
+  for (int e = 0; e < kPer; ++e) {
+    const int idx = threadIdx.x + e * kThreads;     // (mb, nb, j, lane') of the tile
+    const int l = idx & 63, j = (idx >> 6) & 3, nb = (idx >> 8) & 1, mb = idx >> 9;
+    const int row = 16 * mb + 4 * (l >> 4) + j;
+    float acc = 0.f;
+#pragma unroll
+    for (int v = 0; v < kWaves; ++v) acc += red[v * kOut * 64 + idx];
+    if (row < M) {
+      const __bf16 o = (__bf16)acc;
+      y[(size_t)row * N + kCols * blockIdx.x + 16 * nb + (l & 15)] = __builtin_bit_cast(bf16_t, o);
     }
+  }
 }
 
 // Y = sum of the split partials in split order, rounded to bf16.
@@ -475,63 +557,70 @@ AwqPlan awq_plan(int M, int N, int K) {
   AwqPlan p{};
   p.groups = K / kAwqGroup;
   p.large = M > 64;
+  const size_t up = 255;
+  p.sp_bytes = ((size_t)p.groups * M * 16 + up) & ~up;
+  p.splits = 1;
+  p.groups_per_split = p.groups;
   if (p.large) {
     p.tiles_m = (M + awq_lg::kBM - 1) / awq_lg::kBM;
     p.tiles_n = (N + awq_lg::kBN - 1) / awq_lg::kBN;
+    p.tiles = (int64_t)p.tiles_m * p.tiles_n;
+    p.tiles_per_xcd = (int)((p.tiles + kNumXcd - 1) / kNumXcd);
+    // fewer tiles than CUs: split the groups (partials + a reduce pass)
+    if (p.tiles < kAwqCus) {
+      const int splits = (int)std::min<int64_t>(p.groups, (2 * kAwqCus) / p.tiles);
+      p.groups_per_split = (p.groups + splits - 1) / splits;
+      p.splits = (p.groups + p.groups_per_split - 1) / p.groups_per_split;
+    }
+    p.part_bytes = p.splits > 1 ? (((size_t)p.splits * M * N * sizeof(float) + up) & ~up) : 0;
   } else {
-    p.tiles_m = (M + 63) / 64;
-    p.tiles_n = N / 128;
+    p.tiles_m = 1;
+    p.tiles_n = N / awq_sm::kCols;
+    p.tiles = p.tiles_n;
+    p.m_pad = M <= 16 ? 16 : (M <= 32 ? 32 : 64);
+    p.xr_bytes = (size_t)p.groups * p.m_pad * kAwqGroup * 2;
   }
-  p.tiles = (int64_t)p.tiles_m * p.tiles_n;
-  p.tiles_per_xcd = (int)((p.tiles + kNumXcd - 1) / kNumXcd);
-  // Fewer tiles than resident workgroups: split the groups.
-  const int64_t resident = p.large ? kAwqCus : 2 * kAwqCus;
-  int splits = 1;
-  if (p.tiles > 0 && p.tiles < resident)
-    splits = (int)std::min<int64_t>(p.groups, (2 * resident) / p.tiles);
-  p.groups_per_split = (p.groups + std::max(splits, 1) - 1) / std::max(splits, 1);
-  p.splits = (p.groups + p.groups_per_split - 1) / p.groups_per_split;
-  const size_t up = 255;
-  p.sp_bytes = ((size_t)p.groups * M * 16 + up) & ~up;
-  p.part_bytes = p.splits > 1 ? (size_t)p.splits * M * N * sizeof(float) : 0;
   return p;
 }
 
 hipError_t launch_awq_gemm(const AwqArgs& a, hipStream_t stream) {
   const AwqPlan p = awq_plan(a.M, a.N, a.K);
-  bf16_t* sp = reinterpret_cast<bf16_t*>(a.workspace);
-  float* part = reinterpret_cast<float*>(static_cast<char*>(a.workspace) + p.sp_bytes);
-  const int64_t nsum = (int64_t)p.groups * a.M;
+  char* ws = static_cast<char*>(a.workspace);
+  bf16_t* sp = reinterpret_cast<bf16_t*>(ws);
+  float* part = reinterpret_cast<float*>(ws + p.sp_bytes);
+  bf16_t* xr = p.large ? nullptr : reinterpret_cast<bf16_t*>(ws + p.sp_bytes + p.part_bytes);
+  const int64_t nsum = (int64_t)p.groups * (p.large ? a.M : p.m_pad);
   hipLaunchKernelGGL(awq_group_sums_kernel, dim3((unsigned)((nsum + 255) / 256)), dim3(256), 0,
-                     stream, (const bf16_t*)a.x, sp, a.M, a.K);
+                     stream, (const bf16_t*)a.x, sp, xr, a.M, p.m_pad, a.K);
   const bf16_t* x = (const bf16_t*)a.x;
   const uint32_t* qw = (const uint32_t*)a.qweight;
   const bf16_t* sc = (const bf16_t*)a.scales;
   bf16_t* y = (bf16_t*)a.y;
-  const bool split = p.splits > 1;
   if (p.large) {
     const dim3 grid((unsigned)(p.tiles_per_xcd * kNumXcd), (unsigned)p.splits);
-    if (split)
+    if (p.splits > 1) {
       hipLaunchKernelGGL(awq_gemm_lg_kernel<true>, grid, dim3(awq_lg::kThreads), 0, stream, x, qw,
                          sc, a.zeros, sp, y, part, a.M, a.N, a.K, p.groups_per_split, p.tiles_m,
                          p.tiles_n, p.tiles_per_xcd);
-    else
+      const int64_t mn = (int64_t)a.M * a.N;
+      hipLaunchKernelGGL(awq_reduce_kernel, dim3((unsigned)((mn + 255) / 256)), dim3(256), 0,
+                         stream, part, y, mn, p.splits);
+    } else {
       hipLaunchKernelGGL(awq_gemm_lg_kernel<false>, grid, dim3(awq_lg::kThreads), 0, stream, x,
                          qw, sc, a.zeros, sp, y, part, a.M, a.N, a.K, p.groups_per_split,
                          p.tiles_m, p.tiles_n, p.tiles_per_xcd);
+    }
   } else {
-    const dim3 grid((unsigned)p.tiles_n, (unsigned)p.tiles_m, (unsigned)p.splits);
-    if (split)
-      hipLaunchKernelGGL(awq_gemm_sm_kernel<true>, grid, dim3(256), 0, stream, x, qw, sc, a.zeros,
-                         sp, y, part, a.M, a.N, a.K, p.groups_per_split);
+    const dim3 grid((unsigned)p.tiles_n), block(awq_sm::kThreads);
+    if (a.M <= 16)
+      hipLaunchKernelGGL(awq_gemm_sm_kernel<1>, grid, block, 0, stream, xr, qw, sc, a.zeros, sp, y,
+                         a.M, a.N, a.K);
+    else if (a.M <= 32)
+      hipLaunchKernelGGL(awq_gemm_sm_kernel<2>, grid, block, 0, stream, xr, qw, sc, a.zeros, sp, y,
+                         a.M, a.N, a.K);
     else
-      hipLaunchKernelGGL(awq_gemm_sm_kernel<false>, grid, dim3(256), 0, stream, x, qw, sc,
-                         a.zeros, sp, y, part, a.M, a.N, a.K, p.groups_per_split);
-  }
-  if (split) {
-    const int64_t mn = (int64_t)a.M * a.N;
-    hipLaunchKernelGGL(awq_reduce_kernel, dim3((unsigned)((mn + 255) / 256)), dim3(256), 0,
-                       stream, part, y, mn, p.splits);
+      hipLaunchKernelGGL(awq_gemm_sm_kernel<4>, grid, block, 0, stream, xr, qw, sc, a.zeros, sp, y,
+                         a.M, a.N, a.K);
   }
   return hipGetLastError();
 }

@@ -58,11 +58,13 @@ struct AwqArgs {
 };
 
 struct AwqPlan {
-  bool large;                   // 128 x 256 tiles, LDS-staged (else 64 x 128 direct)
+  bool large;                   // M > 64: LDS-staged 128 x 512 tiles
   int groups, splits, groups_per_split;
   int tiles_m, tiles_n, tiles_per_xcd;
+  int m_pad;                    // small batches: rows padded to 16, 32 or 64
   int64_t tiles;
   size_t sp_bytes, part_bytes;  // group-sum pieces, split partials
+  size_t xr_bytes;              // small batches: group-major copy of X
 };
 
 // Launch-grid sizes, exposed so the host can check them before launching.

@@ -226,16 +226,22 @@ def test_awq_workspace_size():
     # (group, row), 256-byte rounded
     M, N, K = 4096, 4096, 4096
     assert ws(M, N, K) == (K // 128) * M * 16
-    # one tile row of a wide decode batch: group sums plus fp32 split partials
-    for M, N, K in ((16, 4096, 4096), (200, 1024, 2048)):
-        pieces = -(-(K // 128) * M * 16 // 256) * 256
-        small = ws(M, N, K)
-        assert small > pieces and (small - pieces) % (M * N * 4) == 0
+    # few 128-row output tiles: group sums plus a whole number of fp32
+    # [M, N] partial planes of a split over the groups
+    M, N, K = 200, 1024, 2048
+    pieces = -(-(K // 128) * M * 16 // 256) * 256
+    assert ws(M, N, K) > pieces and (ws(M, N, K) - pieces) % (M * N * 4) == 0
+    # small batches never split: group sums and the padded group-major x
+    M, N, K = 16, 4096, 4096
+    assert ws(M, N, K) == -(-(K // 128) * M * 16 // 256) * 256 + 16 * K * 2
+    M = 20
+    assert ws(M, N, K) == -(-(K // 128) * M * 16 // 256) * 256 + 32 * K * 2
 
 
 def test_awq_pack_layout():
-    """Every code lands at the documented position: word 8h + t of (group g,
-    column n) holds k = 128g + 16t + 8h + j at bits 4(j/2) + 16(j%2)."""
+    """Every code lands at the documented position: word 8a + 4b + c of
+    (group g, column n) holds k = 128g + 8(4c + 2b + a) + j at bits
+    4(j/2) + 16(j%2)."""
     r = np.random.Generator(np.random.PCG64(3))
     K, N = 384, 256
     q = r.integers(0, 16, size=(K, N), dtype=np.uint8)
@@ -243,9 +249,9 @@ def test_awq_pack_layout():
     assert packed.shape == (K // 128, N, 16)
     back = np.zeros_like(q)
     for w in range(16):
-        h, t = divmod(w, 8)
+        a, b, c = w >> 3, (w >> 2) & 1, w & 3
         for j in range(8):
-            k = np.arange(K // 128) * 128 + 16 * t + 8 * h + j
+            k = np.arange(K // 128) * 128 + 8 * (4 * c + 2 * b + a) + j
             back[k, :] = (packed[:, :, w] >> (4 * (j // 2) + 16 * (j % 2))) & 15
     assert np.array_equal(back, q)
 
