@@ -326,7 +326,12 @@ def bench_phase_awq(torch, dev, reps, batches=(16, 8192)):
     (qkv, o, gate_up, down) at a decode batch of 16 rows (HBM-bound: the packed
     weights dominate) and a chunked-prefill batch of 8192 rows (MFMA-bound).
     Algorithmic bytes: x and y in bf16, codes at 4 bits, one bf16 scale and one
-    uint8 zero point per group of 128 k; flops 2 M N K."""
+    uint8 zero point per group of 128 k; flops 2 M N K.
+
+    `us` is one call timed with HIP events around it, host launch included; at
+    16 rows that is mostly the launch path, so `us_gpu` times the same calls
+    captured in a HIP graph (10 per replay; every replay's output is checked
+    bit for bit against the eager result) and the rates use `us_gpu`."""
     from paper_2412_10543_amd import binding
     from paper_2412_10543_amd.workloads import AWQ_LAYERS_7B, awq_problem
     out = {}
@@ -341,6 +346,7 @@ def bench_phase_awq(torch, dev, reps, batches=(16, 8192)):
                              device=dev)
             binding.rag_awq_gemm(x, qw, sc, z, y, ws)
             torch.cuda.synchronize()
+            want = y.clone()
             timer = Timer(torch)
             for _ in range(reps):
                 timer.start("g")
@@ -348,10 +354,36 @@ def bench_phase_awq(torch, dev, reps, batches=(16, 8192)):
                 timer.stop("g")
             torch.cuda.synchronize()
             ms = median(timer.ms("g"))
+            ms_gpu = ms
+            if M <= 64:
+                side = torch.cuda.Stream()
+                side.wait_stream(torch.cuda.current_stream())
+                graph = torch.cuda.CUDAGraph()
+                with torch.cuda.stream(side):
+                    with torch.cuda.graph(graph, stream=side):
+                        for _ in range(10):
+                            binding.rag_awq_gemm(x, qw, sc, z, y, ws)
+                torch.cuda.current_stream().wait_stream(side)
+                torch.cuda.synchronize()
+                gms = []
+                for _ in range(5):
+                    y.zero_()
+                    torch.cuda.synchronize()
+                    timer = Timer(torch)
+                    timer.start("r")
+                    graph.replay()
+                    timer.stop("r")
+                    torch.cuda.synchronize()
+                    if not torch.equal(y.view(torch.int16), want.view(torch.int16)):
+                        raise RuntimeError(f"awq {name} M={M}: graph replay differs from eager")
+                    gms.append(timer.ms("r")[0] / 10)
+                ms_gpu = median(gms)
+                del graph
             nbytes = 2.0 * M * K + K * N / 2 + (K // 128) * N * 3 + 2.0 * M * N
-            tflops = 2.0 * M * N * K / ms / 1e9
-            gbs = nbytes / ms / 1e6
+            tflops = 2.0 * M * N * K / ms_gpu / 1e9
+            gbs = nbytes / ms_gpu / 1e6
             out[f"{name}_m{M}"] = {"M": M, "N": N, "K": K, "us": round(ms * 1e3, 2),
+                                   "us_gpu": round(ms_gpu * 1e3, 2),
                                    "tflops": round(tflops, 1), "gbs": round(gbs, 1),
                                    "frac_mfma": round(tflops / PEAK_BF16_TFLOPS, 4),
                                    "frac_hbm": round(gbs / PEAK_HBM_GBS, 4)}

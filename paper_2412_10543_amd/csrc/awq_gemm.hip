@@ -31,44 +31,42 @@ namespace rag {
 constexpr int kAwqGroup = 128;
 constexpr int kAwqCus = 256;     // MI355X compute units
 
-// S[g, m] = sum over the group of X[m, k] (fp32, k order), stored as bf16
-// pieces [S1, S2, S3, 0, 0, 0, 0, 0] (16 bytes per (g, m)).  For small
-// batches (xr non-null) the same pass also writes X group-major in the order
-// the small-batch kernel's 16x16x32 A operands are read, xr[g][b][t][q][r]
-// = the 8 values X[16 b + r][128 g + 32 t + 8 q ..], rows past M as zeros:
-// each of that kernel's activation loads is then 1 KB contiguous instead of
-// 16 rows K apart (which all fall into the same cache sets).
+// S[g, m] = sum over the group of X[m, k] (fp32), stored as bf16 pieces
+// [S1, S2, S3, 0, 0, 0, 0, 0] (16 bytes per (g, m)).  For small batches (xr
+// non-null) the same pass also writes X group-major in the order the
+// small-batch kernel's 16x16x32 A operands are read, xr[g][b][t][q][r] = the
+// 8 values X[16 b + r][128 g + 32 t + 8 q ..], rows past M as zeros: each of
+// that kernel's activation loads is then 1 KB contiguous instead of 16 rows K
+// apart (which all fall into the same cache sets).  16 lanes share one
+// (g, m): lane c loads the 16-byte chunk c of the group's row (consecutive
+// lanes, consecutive chunks) and the 16 partial sums are added with lane
+// shuffles in a fixed order.
 __global__ __launch_bounds__(256) void awq_group_sums_kernel(const bf16_t* __restrict__ x,
                                                              bf16_t* __restrict__ sp,
                                                              bf16_t* __restrict__ xr, int M,
                                                              int m_pad, int K) {
   const int groups = K / kAwqGroup;
   const int rows = xr ? m_pad : M;
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= (int64_t)groups * rows) return;
+  const int64_t i = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 4;
+  const int c = threadIdx.x & 15;
+  if (i >= (int64_t)groups * rows) return;        // whole 16-lane groups
   const int g = (int)(i / rows), m = (int)(i % rows);
-  if (m >= M) {                                    // padding rows of xr
-    bf16_t* dst = xr + ((size_t)(g * (m_pad / 16) + m / 16) * 4 * 64 + (m % 16)) * 8;
-#pragma unroll
-    for (int c = 0; c < kAwqGroup / 8; ++c)
-      *reinterpret_cast<u32x4*>(dst + (size_t)((c >> 2) * 64 + (c & 3) * 16) * 8) = u32x4{0, 0, 0, 0};
-    return;
+  u32x4 raw = {0, 0, 0, 0};
+  if (m < M) raw = load16(x + (size_t)m * K + (size_t)g * kAwqGroup + 8 * c);
+  if (xr) {
+    // chunk c = 4 t + q of row m
+    bf16_t* dst = xr + ((size_t)(g * (m_pad / 16) + m / 16) * 4 * 64 +
+                        (size_t)((c >> 2) * 64 + (c & 3) * 16 + (m % 16))) * 8;
+    *reinterpret_cast<u32x4*>(dst) = raw;
   }
-  const bf16_t* row = x + (size_t)m * K + (size_t)g * kAwqGroup;
+  if (m >= M) return;
+  const bf16x8 v = as_bf16x8(raw);
   float acc = 0.f;
-#pragma unroll 4
-  for (int c = 0; c < kAwqGroup / 8; ++c) {
-    const u32x4 raw = load16(row + 8 * c);
-    const bf16x8 v = as_bf16x8(raw);
 #pragma unroll
-    for (int e = 0; e < 8; ++e) acc += (float)v[e];
-    if (xr) {
-      // chunk c = 4 t + q of the row
-      bf16_t* dst = xr + ((size_t)(g * (m_pad / 16) + m / 16) * 4 * 64 +
-                          (size_t)((c >> 2) * 64 + (c & 3) * 16 + (m % 16))) * 8;
-      *reinterpret_cast<u32x4*>(dst) = raw;
-    }
-  }
+  for (int e = 0; e < 8; ++e) acc += (float)v[e];
+#pragma unroll
+  for (int o = 1; o < 16; o <<= 1) acc += __shfl_xor(acc, o, 16);
+  if (c != 0) return;
   const __bf16 s1 = (__bf16)acc;
   const float r1 = acc - (float)s1;
   const __bf16 s2 = (__bf16)r1;
@@ -401,8 +399,8 @@ __global__ __launch_bounds__(awq_lg::kThreads) void awq_gemm_lg_kernel(
 // ---------------------------------------------------------------------------
 // Small batches (M <= 64), where streaming the codes from HBM is the cost.
 // 16x16x32 MFMAs (16 rows per block: no padding rows for a decode batch of
-// 16), one 4-wave workgroup per 32 output columns (two 16-column blocks);
-// wave w takes the groups [w R, w R + R), R = ceil(G / 4), and streams them
+// 16), one workgroup of W waves per 32 output columns (two 16-column blocks);
+// wave w takes the groups [w R, w R + R), R = ceil(G / W), and streams them
 // through a ring of 4 / (M / 16) register slots: the code words (16 contiguous
 // bytes per lane and column block), activations, scales, zero points and
 // group-sum pieces of group i + kDepth are requested as soon as group i has
@@ -412,17 +410,19 @@ __global__ __launch_bounds__(awq_lg::kThreads) void awq_gemm_lg_kernel(
 // sums are added in LDS in wave order.
 // ---------------------------------------------------------------------------
 namespace awq_sm {
-constexpr int kWaves = 4;
-constexpr int kThreads = kWaves * 64;
 constexpr int kCols = 32;          // output columns per workgroup
 }  // namespace awq_sm
 
-template <int MB>   // 16-row blocks: M <= 16 MB
-__global__ __launch_bounds__(awq_sm::kThreads) void awq_gemm_sm_kernel(
+// MB: 16-row blocks (M <= 16 MB).  kWaves: 8 when the output has fewer than
+// 256 column blocks (fewer workgroups than CUs: more waves each keep enough
+// loads in flight), else 4.
+template <int MB, int kWaves>
+__global__ __launch_bounds__(kWaves * 64) void awq_gemm_sm_kernel(
     const bf16_t* __restrict__ xr, const uint32_t* __restrict__ qw,
     const bf16_t* __restrict__ scales, const uint8_t* __restrict__ zeros,
     const bf16_t* __restrict__ sp, bf16_t* __restrict__ y, int M, int N, int K) {
   using namespace awq_sm;
+  constexpr int kThreads = kWaves * 64;
   constexpr int kDepth = 4 / MB;                   // ring slots (registers)
   constexpr int kOut = MB * 2 * 4;                 // accumulator values per lane
   __shared__ float red[kWaves * kOut * 64];
@@ -589,7 +589,7 @@ hipError_t launch_awq_gemm(const AwqArgs& a, hipStream_t stream) {
   bf16_t* sp = reinterpret_cast<bf16_t*>(ws);
   float* part = reinterpret_cast<float*>(ws + p.sp_bytes);
   bf16_t* xr = p.large ? nullptr : reinterpret_cast<bf16_t*>(ws + p.sp_bytes + p.part_bytes);
-  const int64_t nsum = (int64_t)p.groups * (p.large ? a.M : p.m_pad);
+  const int64_t nsum = (int64_t)p.groups * (p.large ? a.M : p.m_pad) * 16;   // 16 lanes per row
   hipLaunchKernelGGL(awq_group_sums_kernel, dim3((unsigned)((nsum + 255) / 256)), dim3(256), 0,
                      stream, (const bf16_t*)a.x, sp, xr, a.M, p.m_pad, a.K);
   const bf16_t* x = (const bf16_t*)a.x;
@@ -611,16 +611,17 @@ hipError_t launch_awq_gemm(const AwqArgs& a, hipStream_t stream) {
                          p.tiles_m, p.tiles_n, p.tiles_per_xcd);
     }
   } else {
-    const dim3 grid((unsigned)p.tiles_n), block(awq_sm::kThreads);
+    const bool wide = p.tiles_n >= kAwqCus;
+    const dim3 grid((unsigned)p.tiles_n), block(wide ? 256 : 512);
+    auto go = [&](auto kernel) {
+      hipLaunchKernelGGL(kernel, grid, block, 0, stream, xr, qw, sc, a.zeros, sp, y, a.M, a.N, a.K);
+    };
     if (a.M <= 16)
-      hipLaunchKernelGGL(awq_gemm_sm_kernel<1>, grid, block, 0, stream, xr, qw, sc, a.zeros, sp, y,
-                         a.M, a.N, a.K);
+      wide ? go(awq_gemm_sm_kernel<1, 4>) : go(awq_gemm_sm_kernel<1, 8>);
     else if (a.M <= 32)
-      hipLaunchKernelGGL(awq_gemm_sm_kernel<2>, grid, block, 0, stream, xr, qw, sc, a.zeros, sp, y,
-                         a.M, a.N, a.K);
+      wide ? go(awq_gemm_sm_kernel<2, 4>) : go(awq_gemm_sm_kernel<2, 8>);
     else
-      hipLaunchKernelGGL(awq_gemm_sm_kernel<4>, grid, block, 0, stream, xr, qw, sc, a.zeros, sp, y,
-                         a.M, a.N, a.K);
+      wide ? go(awq_gemm_sm_kernel<4, 4>) : go(awq_gemm_sm_kernel<4, 8>);
   }
   return hipGetLastError();
 }
