@@ -59,10 +59,15 @@ def decode_bytes(kv_lens, hq, hkv, d, q_rows=None):
                      for n, r in zip(kv_lens, rows)))
 
 
+# The sources of the attention kernels the stored traffic counters measure:
+# their translation unit and the headers it includes.
+ATTN_SOURCES = ("kernels.hip", "common.h", "prefill_tile.h", "decode_unit.h", "launch.h")
+
+
 def kernel_source_hash():
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2412_10543_amd", "csrc")
-    for name in sorted(os.listdir(csrc)):
+    for name in ATTN_SOURCES:
         with open(os.path.join(csrc, name), "rb") as f:
             h.update(name.encode() + f.read())
     return h.hexdigest()[:16]
@@ -321,7 +326,7 @@ def bench_phase_kv_write(torch, dev, reps):
     return out
 
 
-def bench_phase_awq(torch, dev, reps, batches=(16, 8192)):
+def bench_phase_awq(torch, dev, reps, batches=(16, 8192), graph=True):
     """Group-quantized int4-weight GEMMs of the 7B model's linear layers
     (qkv, o, gate_up, down) at a decode batch of 16 rows (HBM-bound: the packed
     weights dominate) and a chunked-prefill batch of 8192 rows (MFMA-bound).
@@ -355,7 +360,7 @@ def bench_phase_awq(torch, dev, reps, batches=(16, 8192)):
             torch.cuda.synchronize()
             ms = median(timer.ms("g"))
             ms_gpu = ms
-            if M <= 64:
+            if graph and M <= 64:
                 side = torch.cuda.Stream()
                 side.wait_stream(torch.cuda.current_stream())
                 graph = torch.cuda.CUDAGraph()
@@ -488,6 +493,8 @@ def main():
     ap.add_argument("--extra-reps", type=int, default=5)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a 1 GiB device copy (counter calibration)")
+    ap.add_argument("--awq-only", action="store_true",
+                    help="only the int4-weight GEMM phase, eager calls (for profiling)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU: this build has no multi-GPU path "
@@ -501,6 +508,10 @@ def main():
         sys.exit(1)
     if args.copy_calibration:
         copy_calibration(torch)
+        return
+    if args.awq_only:
+        print(json.dumps({"awq_gemm_7b": bench_phase_awq(torch, torch.device("cuda:0"),
+                                                         max(args.extra_reps, 10), graph=False)}))
         return
     from paper_2412_10543_amd import binding
     from paper_2412_10543_amd.workloads import long70b, mapred7b, stuff7b

@@ -27,7 +27,7 @@ COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-I", INCLUDE,
 # them without AGPR copies.
 SOURCE_FLAGS = {"awq_gemm.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]}
 SOURCES = ["kernels.hip", "kv_cache.hip", "awq_gemm.hip", "api.cpp", "awq_api.cpp", "planner.cpp"]
-HEADERS = ["common.h", "prefill_tile.h", "decode_unit.h", "launch.h", "errors.h"]
+HEADERS = ["common.h", "prefill_tile.h", "decode_unit.h", "launch.h", "errors.h", "awq.h"]
 
 
 def build(verbose: bool = False) -> str:

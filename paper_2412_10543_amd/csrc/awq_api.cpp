@@ -6,7 +6,7 @@
 #include <cstdint>
 
 #include "errors.h"
-#include "launch.h"
+#include "awq.h"
 #include "rag_attn.h"
 
 namespace {

@@ -24,7 +24,7 @@
 // (column, quarter qq) needs the octets 4t + qq of k-steps t = 0..3, words
 // 8(qq&1) + 4(qq>>1) .. +3.
 #include "common.h"
-#include "launch.h"
+#include "awq.h"
 
 namespace rag {
 

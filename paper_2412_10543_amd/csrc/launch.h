@@ -47,26 +47,6 @@ struct KvWriteArgs {
   int hkv, d;
 };
 
-struct AwqArgs {
-  const void* x;                // bf16 [M, K]
-  const int32_t* qweight;       // packed codes [K/128][N][16]
-  const void* scales;           // bf16 [K/128, N]
-  const uint8_t* zeros;         // [K/128, N]
-  void* y;                      // bf16 [M, N]
-  void* workspace;
-  int M, N, K;
-};
-
-struct AwqPlan {
-  bool large;                   // M > 64: LDS-staged 128 x 512 tiles
-  int groups, splits, groups_per_split;
-  int tiles_m, tiles_n, tiles_per_xcd;
-  int m_pad;                    // small batches: rows padded to 16, 32 or 64
-  int64_t tiles;
-  size_t sp_bytes, part_bytes;  // group-sum pieces, split partials
-  size_t xr_bytes;              // small batches: group-major copy of X
-};
-
 // Launch-grid sizes, exposed so the host can check them before launching.
 int64_t prefill_grid(int num_seqs, int hkv, int group, int max_seqlen_q);
 int64_t paged_prefill_grid(int num_pieces, int hkv, int group, int max_seqlen_q);
@@ -76,7 +56,5 @@ hipError_t launch_prefill_varlen(const PrefillArgs& a, hipStream_t stream);
 hipError_t launch_paged(const PagedArgs& a, hipStream_t stream);
 int64_t kv_cache_write_grid(int64_t num_tokens, int hkv, int d);
 hipError_t launch_kv_cache_write(const KvWriteArgs& a, hipStream_t stream);
-AwqPlan awq_plan(int M, int N, int K);
-hipError_t launch_awq_gemm(const AwqArgs& a, hipStream_t stream);
 
 }  // namespace rag
