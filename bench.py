@@ -363,9 +363,9 @@ def bench_phase_awq(torch, dev, reps, batches=(16, 8192), graph=True):
             if graph and M <= 64:
                 side = torch.cuda.Stream()
                 side.wait_stream(torch.cuda.current_stream())
-                graph = torch.cuda.CUDAGraph()
+                cg = torch.cuda.CUDAGraph()
                 with torch.cuda.stream(side):
-                    with torch.cuda.graph(graph, stream=side):
+                    with torch.cuda.graph(cg, stream=side):
                         for _ in range(10):
                             binding.rag_awq_gemm(x, qw, sc, z, y, ws)
                 torch.cuda.current_stream().wait_stream(side)
@@ -376,14 +376,14 @@ def bench_phase_awq(torch, dev, reps, batches=(16, 8192), graph=True):
                     torch.cuda.synchronize()
                     timer = Timer(torch)
                     timer.start("r")
-                    graph.replay()
+                    cg.replay()
                     timer.stop("r")
                     torch.cuda.synchronize()
                     if not torch.equal(y.view(torch.int16), want.view(torch.int16)):
                         raise RuntimeError(f"awq {name} M={M}: graph replay differs from eager")
                     gms.append(timer.ms("r")[0] / 10)
                 ms_gpu = median(gms)
-                del graph
+                del cg
             nbytes = 2.0 * M * K + K * N / 2 + (K // 128) * N * 3 + 2.0 * M * N
             tflops = 2.0 * M * N * K / ms_gpu / 1e9
             gbs = nbytes / ms_gpu / 1e6
