@@ -80,7 +80,21 @@ def _mutant_last_group_scale(x, q, z, s, G):
     return x @ ((q - z[g]) * s[g])
 
 
-@pytest.mark.parametrize("mutant", [_mutant_zero_added, _mutant_last_group_scale])
+def _mutant_scale_by_k(x, q, z, s, G):
+    g = np.arange(q.shape[0]) // G
+    gk = np.arange(q.shape[0]) % z.shape[0]          # scale row picked by k, not by group
+    return x @ ((q - z[g]) * s[gk])
+
+
+def _mutant_codes_reversed_in_group(x, q, z, s, G):
+    k = np.arange(q.shape[0])
+    src = (k // G) * G + (G - 1 - k % G)              # an unpacking that reverses a group
+    g = k // G
+    return x @ ((q[src] - z[g]) * s[g])
+
+
+@pytest.mark.parametrize("mutant", [_mutant_zero_added, _mutant_last_group_scale,
+                                    _mutant_scale_by_k, _mutant_codes_reversed_in_group])
 def test_planted_mistakes_are_caught(mutant):
     x, q, z, s = _case(3, 64, 4, 16, 9)
     assert not np.allclose(mutant(x, q, z, s, 16), _brute(x, q, z, s, 16))
