@@ -359,10 +359,12 @@ rag_status rag_awq_pack_weights(const uint8_t *q, int32_t K, int32_t N,
 
 /* Bytes of workspace rag_awq_gemm needs (0 for M == 0 or invalid shapes).
  * Library-internal layout: the group sums of x [K / 128, M] (each as three
- * bf16 pieces in 16 bytes), then, for M > 64 with too few output tiles to
- * fill the GPU, fp32 partial outputs [splits, M, N] of a split over the
- * groups (added in a fixed order, so results do not depend on timing), or,
- * for M <= 64, a group-major copy of x with M padded to 16, 32 or 64 rows. */
+ * bf16 pieces in 16 bytes), then, when the output tiles are too few to fill
+ * the GPU, fp32 partial outputs [splits, M, N] of a split over the groups
+ * (added in a fixed order, so results do not depend on timing), then, for
+ * M <= 64, a group-major copy of x with M padded to 16, 32 or 64 rows and,
+ * with a split, one arrival counter per column block (the call zeroes them
+ * itself). */
 size_t rag_awq_workspace_size(int32_t M, int32_t N, int32_t K,
                               int32_t group_size);
 

@@ -24,9 +24,11 @@ struct AwqPlan {
   int groups, splits, groups_per_split;
   int tiles_m, tiles_n, tiles_per_xcd;
   int m_pad;                    // small batches: rows padded to 16, 32 or 64
+  int sm_nb;                    // small batches: 16-column blocks per workgroup
   int64_t tiles;
   size_t sp_bytes, part_bytes;  // group-sum pieces, split partials
   size_t xr_bytes;              // small batches: group-major copy of X
+  size_t counter_bytes;         // small batches split over groups: arrival counters
 };
 
 AwqPlan awq_plan(int M, int N, int K);

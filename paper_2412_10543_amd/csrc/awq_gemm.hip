@@ -37,17 +37,22 @@ constexpr int kAwqCus = 256;     // MI355X compute units
 // small-batch kernel's 16x16x32 A operands are read, xr[g][b][t][q][r] = the
 // 8 values X[16 b + r][128 g + 32 t + 8 q ..], rows past M as zeros: each of
 // that kernel's activation loads is then 1 KB contiguous instead of 16 rows K
-// apart (which all fall into the same cache sets).  16 lanes share one
+// apart (which all fall into the same cache sets).  It also zeroes the
+// arrival counters of the small-batch kernel of the same call.  16 lanes share one
 // (g, m): lane c loads the 16-byte chunk c of the group's row (consecutive
 // lanes, consecutive chunks) and the 16 partial sums are added with lane
 // shuffles in a fixed order.
 __global__ __launch_bounds__(256) void awq_group_sums_kernel(const bf16_t* __restrict__ x,
                                                              bf16_t* __restrict__ sp,
-                                                             bf16_t* __restrict__ xr, int M,
-                                                             int m_pad, int K) {
+                                                             bf16_t* __restrict__ xr,
+                                                             int* __restrict__ counters,
+                                                             int n_counters, int M, int m_pad,
+                                                             int K) {
   const int groups = K / kAwqGroup;
   const int rows = xr ? m_pad : M;
-  const int64_t i = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 4;
+  const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (tid < n_counters) counters[tid] = 0;        // the small-batch kernel's arrivals
+  const int64_t i = tid >> 4;
   const int c = threadIdx.x & 15;
   if (i >= (int64_t)groups * rows) return;        // whole 16-lane groups
   const int g = (int)(i / rows), m = (int)(i % rows);
@@ -399,40 +404,42 @@ __global__ __launch_bounds__(awq_lg::kThreads) void awq_gemm_lg_kernel(
 // ---------------------------------------------------------------------------
 // Small batches (M <= 64), where streaming the codes from HBM is the cost.
 // 16x16x32 MFMAs (16 rows per block: no padding rows for a decode batch of
-// 16), one workgroup of W waves per 32 output columns (two 16-column blocks);
-// wave w takes the groups [w R, w R + R), R = ceil(G / W), and streams them
-// through a ring of 4 / (M / 16) register slots: the code words (16 contiguous
-// bytes per lane and column block), activations, scales, zero points and
-// group-sum pieces of group i + kDepth are requested as soon as group i has
-// taken its slot.  Per group and
-// block: the zero-point MFMA (group-sum pieces times -(128 + z), bf16 exact)
-// opens the chain, 4 k-steps follow, and y += s * P in fp32.  The waves'
-// sums are added in LDS in wave order.
+// 16), one workgroup of W waves per 16 NB output columns (NB blocks of 16
+// columns, which share each activation load); wave w takes the groups
+// [w R, w R + R), R = ceil(G / W), and streams them through a ring of
+// register slots: the code words (16 contiguous bytes per lane and column
+// block), activations, scales, zero points and group-sum pieces of group
+// i + depth are requested as soon as group i has taken its slot.  Per group
+// and block: the zero-point MFMA (group-sum pieces times -(128 + z), bf16
+// exact) opens the chain, 4 k-steps follow, and y += s * P in fp32.  The
+// waves' sums are added in LDS in wave order.
 // ---------------------------------------------------------------------------
-namespace awq_sm {
-constexpr int kCols = 32;          // output columns per workgroup
-}  // namespace awq_sm
 
-// MB: 16-row blocks (M <= 16 MB).  kWaves: 8 when the output has fewer than
-// 256 column blocks (fewer workgroups than CUs: more waves each keep enough
-// loads in flight), else 4.
-template <int MB, int kWaves>
+// MB: 16-row blocks (M <= 16 MB).  NB: 16-column blocks per workgroup (4 for
+// M <= 16 when that still leaves one workgroup per CU, else 2).  kWaves: 8 when there are
+// fewer workgroups than CUs (more waves each keep enough loads in flight),
+// else 4.
+template <int MB, int NB, int kWaves>
 __global__ __launch_bounds__(kWaves * 64) void awq_gemm_sm_kernel(
     const bf16_t* __restrict__ xr, const uint32_t* __restrict__ qw,
     const bf16_t* __restrict__ scales, const uint8_t* __restrict__ zeros,
-    const bf16_t* __restrict__ sp, bf16_t* __restrict__ y, int M, int N, int K) {
-  using namespace awq_sm;
+    const bf16_t* __restrict__ sp, bf16_t* __restrict__ y, float* __restrict__ part,
+    int* __restrict__ arrivals, int M, int N, int K, int splits) {
+  constexpr int kCols = 16 * NB;
   constexpr int kThreads = kWaves * 64;
-  constexpr int kDepth = 4 / MB;                   // ring slots (registers)
-  constexpr int kOut = MB * 2 * 4;                 // accumulator values per lane
+  constexpr int kDepth = 8 / (MB * NB) > 1 ? 8 / (MB * NB) : 1;   // ring slots (registers)
+  constexpr int kOut = MB * NB * 4;                // accumulator values per lane
   __shared__ float red[kWaves * kOut * 64];
   const int lane = threadIdx.x & 63, w = wave_id();
   const int c = lane & 15, qq = lane >> 4;
-  const int n0 = kCols * blockIdx.x + c;           // columns n0 and n0 + 16
+  const int n0 = kCols * blockIdx.x + c;           // columns n0 + 16 nb
   const int groups = K / kAwqGroup;
-  const int per_wave = (groups + kWaves - 1) / kWaves;
-  const int g0 = w * per_wave;
-  const int ng = max(0, min(per_wave, groups - g0));
+  const int spl = blockIdx.y;
+  const int per_wg = (groups + splits - 1) / splits;
+  const int wg_end = min(groups, (spl + 1) * per_wg);
+  const int per_wave = (per_wg + kWaves - 1) / kWaves;
+  const int g0 = spl * per_wg + w * per_wave;
+  const int ng = max(0, min(per_wave, wg_end - g0));
   const uint32_t kMask = in_vgpr(0x000F000Fu), kMagic = in_vgpr(0x43004300u);
   const int wpos = 8 * (qq & 1) + 4 * (qq >> 1);   // this lane's 4 words
   int rows[MB];
@@ -440,16 +447,16 @@ __global__ __launch_bounds__(kWaves * 64) void awq_gemm_sm_kernel(
   for (int mb = 0; mb < MB; ++mb) rows[mb] = min(16 * mb + c, M - 1);
 
   struct Slot {
-    u32x4 wd[2];
+    u32x4 wd[NB];
     u32x4 xa[4][MB];
     u32x4 az[MB];
-    uint32_t sbits[2], z[2];
+    uint32_t sbits[NB], z[NB];
   };
   // everything one group needs; raw values only (arithmetic on a loaded
   // value here would wait for the load)
   auto fetch = [&](int g, Slot& sl) {
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb) {
+    for (int nb = 0; nb < NB; ++nb) {
       const size_t col = (size_t)g * N + n0 + 16 * nb;
       sl.wd[nb] = *reinterpret_cast<const u32x4*>(qw + col * 16 + wpos);
       sl.sbits[nb] = scales[col];
@@ -464,11 +471,11 @@ __global__ __launch_bounds__(kWaves * 64) void awq_gemm_sm_kernel(
     for (int mb = 0; mb < MB; ++mb) sl.az[mb] = load16(sp + ((size_t)g * M + rows[mb]) * 8);
   };
 
-  f32x4 yv[MB][2];
+  f32x4 yv[MB][NB];
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb) yv[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int nb = 0; nb < NB; ++nb) yv[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
   if (ng > 0) {
     Slot ring[kDepth];
 #pragma unroll
@@ -486,9 +493,9 @@ __global__ __launch_bounds__(kWaves * 64) void awq_gemm_sm_kernel(
         const Slot sl = ring[d];
         fetch(min(g + kDepth, g_last), ring[d]);
         __builtin_amdgcn_sched_barrier(0);
-        f32x4 p[MB][2];
+        f32x4 p[MB][NB];
 #pragma unroll
-        for (int nb = 0; nb < 2; ++nb) {
+        for (int nb = 0; nb < NB; ++nb) {
           const uint32_t nz = 0xC300u | sl.z[nb];              // bf16 -(128 + z)
           const u32x4 bzv = {nz | (nz << 16), nz, 0u, 0u};
 #pragma unroll
@@ -500,13 +507,13 @@ __global__ __launch_bounds__(kWaves * 64) void awq_gemm_sm_kernel(
 #pragma unroll
         for (int t = 0; t < 4; ++t)
 #pragma unroll
-          for (int nb = 0; nb < 2; ++nb) {
+          for (int nb = 0; nb < NB; ++nb) {
             const bf16x8 b = codes_to_bf16(sl.wd[nb][t], kMask, kMagic);
 #pragma unroll
             for (int mb = 0; mb < MB; ++mb) p[mb][nb] = mfma16(as_bf16x8(sl.xa[t][mb]), b, p[mb][nb]);
           }
 #pragma unroll
-        for (int nb = 0; nb < 2; ++nb) {
+        for (int nb = 0; nb < NB; ++nb) {
           const float sc = bf16_to_f32(sl.sbits[nb]);
 #pragma unroll
           for (int mb = 0; mb < MB; ++mb)
@@ -521,23 +528,55 @@ __global__ __launch_bounds__(kWaves * 64) void awq_gemm_sm_kernel(
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb)
+    for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) red[(w * kOut + (mb * 2 + nb) * 4 + j) * 64 + lane] = yv[mb][nb][j];
+      for (int j = 0; j < 4; ++j) red[(w * kOut + (mb * NB + nb) * 4 + j) * 64 + lane] = yv[mb][nb][j];
   __syncthreads();
   constexpr int kPer = kOut * 64 / kThreads;       // outputs per thread
+  float tot[kPer];
+  int orow[kPer], ocol[kPer];
 #pragma unroll
   for (int e = 0; e < kPer; ++e) {
     const int idx = threadIdx.x + e * kThreads;     // (mb, nb, j, lane') of the tile
-    const int l = idx & 63, j = (idx >> 6) & 3, nb = (idx >> 8) & 1, mb = idx >> 9;
-    const int row = 16 * mb + 4 * (l >> 4) + j;
+    const int l = idx & 63, j = (idx >> 6) & 3, nb = (idx >> 8) % NB, mb = (idx >> 8) / NB;
+    orow[e] = 16 * mb + 4 * (l >> 4) + j;
+    ocol[e] = kCols * blockIdx.x + 16 * nb + (l & 15);
     float acc = 0.f;
 #pragma unroll
     for (int v = 0; v < kWaves; ++v) acc += red[v * kOut * 64 + idx];
-    if (row < M) {
-      const __bf16 o = (__bf16)acc;
-      y[(size_t)row * N + kCols * blockIdx.x + 16 * nb + (l & 15)] = __builtin_bit_cast(bf16_t, o);
-    }
+    tot[e] = acc;
+  }
+  if (splits == 1) {
+#pragma unroll
+    for (int e = 0; e < kPer; ++e)
+      if (orow[e] < M) {
+        const __bf16 o = (__bf16)tot[e];
+        y[(size_t)orow[e] * N + ocol[e]] = __builtin_bit_cast(bf16_t, o);
+      }
+    return;
+  }
+  // ---- groups split over workgroups: fp32 partials (device-coherent stores,
+  // another XCD may add them), then the last workgroup of the column block to
+  // arrive adds them in split order ----
+  __shared__ int flag;
+#pragma unroll
+  for (int e = 0; e < kPer; ++e)
+    if (orow[e] < M) store_coherent(part + ((size_t)spl * M + orow[e]) * N + ocol[e], tot[e]);
+  wait_all_memory();
+  __syncthreads();
+  if (threadIdx.x == 0)
+    flag = __hip_atomic_fetch_add(arrivals + blockIdx.x, 1, __ATOMIC_RELAXED,
+                                  __HIP_MEMORY_SCOPE_AGENT);
+  __syncthreads();
+  if (flag != splits - 1) return;
+#pragma unroll
+  for (int e = 0; e < kPer; ++e) {
+    if (orow[e] >= M) continue;
+    float acc = 0.f;
+    for (int s2 = 0; s2 < splits; ++s2)
+      acc += load_coherent(part + ((size_t)s2 * M + orow[e]) * N + ocol[e]);
+    const __bf16 o = (__bf16)acc;
+    y[(size_t)orow[e] * N + ocol[e]] = __builtin_bit_cast(bf16_t, o);
   }
 }
 
@@ -575,8 +614,20 @@ AwqPlan awq_plan(int M, int N, int K) {
     p.part_bytes = p.splits > 1 ? (((size_t)p.splits * M * N * sizeof(float) + up) & ~up) : 0;
   } else {
     p.tiles_m = 1;
-    p.tiles_n = N / awq_sm::kCols;
-    p.tiles = p.tiles_n;
+    p.sm_nb = M <= 16 && N / 64 >= kAwqCus ? 4 : 2;
+    p.tiles_n = N / (16 * p.sm_nb);
+    // fewer column blocks than CUs and a long K: split the groups too (at
+    // least 4 per workgroup), so that every CU streams codes (for short K the
+    // merge costs more than the idle CUs)
+    if (p.tiles_n < kAwqCus && p.groups >= 64)
+      p.splits = std::max(1, std::min((kAwqCus + p.tiles_n - 1) / p.tiles_n, p.groups / 4));
+    p.groups_per_split = (p.groups + p.splits - 1) / p.splits;
+    p.splits = (p.groups + p.groups_per_split - 1) / p.groups_per_split;
+    p.tiles = (int64_t)p.tiles_n * p.splits;
+    if (p.splits > 1) {
+      p.part_bytes = ((size_t)p.splits * M * N * sizeof(float) + up) & ~up;
+      p.counter_bytes = ((size_t)p.tiles_n * sizeof(int) + up) & ~up;
+    }
     p.m_pad = M <= 16 ? 16 : (M <= 32 ? 32 : 64);
     p.xr_bytes = (size_t)p.groups * p.m_pad * kAwqGroup * 2;
   }
@@ -589,9 +640,12 @@ hipError_t launch_awq_gemm(const AwqArgs& a, hipStream_t stream) {
   bf16_t* sp = reinterpret_cast<bf16_t*>(ws);
   float* part = reinterpret_cast<float*>(ws + p.sp_bytes);
   bf16_t* xr = p.large ? nullptr : reinterpret_cast<bf16_t*>(ws + p.sp_bytes + p.part_bytes);
-  const int64_t nsum = (int64_t)p.groups * (p.large ? a.M : p.m_pad) * 16;   // 16 lanes per row
+  int* counters = reinterpret_cast<int*>(ws + p.sp_bytes + p.part_bytes + p.xr_bytes);
+  const int n_counters = (int)(p.counter_bytes / sizeof(int));
+  const int64_t nsum = std::max<int64_t>((int64_t)p.groups * (p.large ? a.M : p.m_pad) * 16,
+                                         n_counters);   // 16 lanes per row
   hipLaunchKernelGGL(awq_group_sums_kernel, dim3((unsigned)((nsum + 255) / 256)), dim3(256), 0,
-                     stream, (const bf16_t*)a.x, sp, xr, a.M, p.m_pad, a.K);
+                     stream, (const bf16_t*)a.x, sp, xr, counters, n_counters, a.M, p.m_pad, a.K);
   const bf16_t* x = (const bf16_t*)a.x;
   const uint32_t* qw = (const uint32_t*)a.qweight;
   const bf16_t* sc = (const bf16_t*)a.scales;
@@ -611,17 +665,23 @@ hipError_t launch_awq_gemm(const AwqArgs& a, hipStream_t stream) {
                          p.tiles_m, p.tiles_n, p.tiles_per_xcd);
     }
   } else {
-    const bool wide = p.tiles_n >= kAwqCus;
-    const dim3 grid((unsigned)p.tiles_n), block(wide ? 256 : 512);
+    const bool wide = p.tiles >= kAwqCus;
+    const dim3 grid((unsigned)p.tiles_n, (unsigned)p.splits), block(wide ? 256 : 512);
     auto go = [&](auto kernel) {
-      hipLaunchKernelGGL(kernel, grid, block, 0, stream, xr, qw, sc, a.zeros, sp, y, a.M, a.N, a.K);
+      hipLaunchKernelGGL(kernel, grid, block, 0, stream, xr, qw, sc, a.zeros, sp, y, part, counters,
+                         a.M, a.N, a.K, p.splits);
     };
-    if (a.M <= 16)
-      wide ? go(awq_gemm_sm_kernel<1, 4>) : go(awq_gemm_sm_kernel<1, 8>);
-    else if (a.M <= 32)
-      wide ? go(awq_gemm_sm_kernel<2, 4>) : go(awq_gemm_sm_kernel<2, 8>);
-    else
-      wide ? go(awq_gemm_sm_kernel<4, 4>) : go(awq_gemm_sm_kernel<4, 8>);
+    const int mb = a.M <= 16 ? 1 : (a.M <= 32 ? 2 : 4);
+    switch (mb * 100 + p.sm_nb * 10 + (wide ? 4 : 8)) {
+      case 124: go(awq_gemm_sm_kernel<1, 2, 4>); break;
+      case 128: go(awq_gemm_sm_kernel<1, 2, 8>); break;
+      case 144: go(awq_gemm_sm_kernel<1, 4, 4>); break;
+      case 148: go(awq_gemm_sm_kernel<1, 4, 8>); break;
+      case 224: go(awq_gemm_sm_kernel<2, 2, 4>); break;
+      case 228: go(awq_gemm_sm_kernel<2, 2, 8>); break;
+      case 424: go(awq_gemm_sm_kernel<4, 2, 4>); break;
+      default: go(awq_gemm_sm_kernel<4, 2, 8>); break;
+    }
   }
   return hipGetLastError();
 }

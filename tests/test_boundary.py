@@ -231,11 +231,18 @@ def test_awq_workspace_size():
     M, N, K = 200, 1024, 2048
     pieces = -(-(K // 128) * M * 16 // 256) * 256
     assert ws(M, N, K) > pieces and (ws(M, N, K) - pieces) % (M * N * 4) == 0
-    # small batches never split: group sums and the padded group-major x
+    # small batches: group sums and the padded group-major x; with fewer
+    # column blocks than CUs also split partials and arrival counters
+    def pieces(M, K):
+        return -(-(K // 128) * M * 16 // 256) * 256
+    M, N, K = 16, 28672, 4096
+    assert ws(M, N, K) == pieces(M, K) + 16 * K * 2
     M, N, K = 16, 4096, 4096
-    assert ws(M, N, K) == -(-(K // 128) * M * 16 // 256) * 256 + 16 * K * 2
+    assert ws(M, N, K) == pieces(M, K) + 16 * K * 2
+    M, N, K = 16, 4096, 14336
+    assert ws(M, N, K) >= pieces(M, K) + 2 * M * N * 4 + 16 * K * 2 + (N // 32) * 4
     M = 20
-    assert ws(M, N, K) == -(-(K // 128) * M * 16 // 256) * 256 + 32 * K * 2
+    assert ws(M, N, K) >= pieces(M, K) + 2 * M * N * 4 + 32 * K * 2 + (N // 32) * 4
 
 
 def test_awq_pack_layout():
