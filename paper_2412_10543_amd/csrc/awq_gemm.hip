@@ -9,10 +9,11 @@
 //     sum_k X[m, k] W[k, n] = s[g, n] * (P[m, n] - (128 + z[g, n]) * S[g, m]),
 //     P = sum_k X[m, k] (128 + q[k, n]),   S[g, m] = sum of X[m, k] over g.
 // A pre-pass computes S in fp32 and stores it as three bf16 pieces
-// S1 + S2 + S3 = S (exact: 24 bits in 3 x 8).  The large-batch kernel folds
-// the zero-point term into the matrix cores as a ninth MFMA per group (A =
-// the pieces, B = -(128 + z), which bf16 holds exactly as bits 0xC300 | z),
-// so the per-group scale is one fp32 FMA per output element.
+// S1 + S2 + S3 = S (exact: 24 bits in 3 x 8).  Both kernels fold the
+// zero-point term into the matrix cores as one more MFMA per group (A = the
+// pieces, B = -(128 + z), which bf16 holds exactly as bits 0xC300 | z); the
+// scale is then one fp32 FMA per output element and group (small batches) or
+// a running rescale of the accumulators (large batches, see there).
 //
 // Packed weight layout (rag_awq_pack_weights): int32 [K/128][N][16].  The
 // 16 words of (group g, column n) are 64 contiguous bytes; word
@@ -139,7 +140,7 @@ constexpr int kBM = 128;
 constexpr int kBN = 512;
 constexpr int kStages = 2;
 constexpr int kX = kBM * kAwqGroup * 2;          // 32768
-constexpr int kW = kBN * kAwqGroup / 2;          // 16384
+constexpr int kW = kBN * kAwqGroup / 2;          // 32768
 constexpr int kSP = kBM * 16;                    // 2048
 constexpr int kSZ = kBN * 3;                     // 1536
 constexpr int kStage = kX + kW + kSP + kSZ;      // 69120
