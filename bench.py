@@ -34,6 +34,7 @@ sys.path.insert(0, ROOT)
 METRIC = "prefill attn TFLOP/s (% MFMA peak); decode attn KV GB/s (% HBM peak)"
 PEAK_BF16_TFLOPS = 2516.6     # 256 CU x 4096 FLOP/clk x 2.4 GHz, dense
 PEAK_HBM_GBS = 8000.0
+WARMUP_REPS = 5               # untimed repetitions before each extra phase
 PROFILES = os.path.join(ROOT, "profiles")
 
 
@@ -106,6 +107,52 @@ class Timer:
 
     def ms(self, name):
         return [a.elapsed_time(b) for a, b in self.pairs.get(name, [])]
+
+
+def read_clocks():
+    """Current and maximum shader clock and memory clock of GPU 0 from
+    `amd-smi metric --clock --json` (a child process; read-only).  None-valued
+    or an error note when the tool or a field is missing."""
+    import subprocess
+    try:
+        r = subprocess.run(["amd-smi", "metric", "--clock", "--json"], capture_output=True,
+                           text=True, timeout=30)
+        d = json.loads(r.stdout[r.stdout.index("{"):] if "{" in r.stdout else "{}")
+        gpus = d.get("gpu_data", d) if isinstance(d, dict) else d
+        c = gpus[0]["clock"]
+
+        def vals(prefix, field):
+            out = []
+            for k, v in c.items():
+                f = v.get(field) if k.startswith(prefix) and isinstance(v, dict) else None
+                if isinstance(f, dict) and isinstance(f.get("value"), (int, float)):
+                    out.append(f["value"])
+            return max(out) if out else None
+        return {"sclk_mhz": vals("gfx", "clk"), "sclk_max_mhz": vals("gfx", "max_clk"),
+                "mclk_mhz": vals("mem", "clk")}
+    except Exception as e:   # a missing tool must not stop the bench
+        return {"error": f"{type(e).__name__}: {str(e)[:60]}"}
+
+
+class ClockSampler:
+    """One clock reading taken `delay` seconds after start(), from a thread,
+    while the GPU is busy with the work that follows."""
+
+    def __init__(self, delay=2.0):
+        import threading
+        self.result = None
+        self.thread = threading.Thread(target=self._run, args=(delay,), daemon=True)
+
+    def _run(self, delay):
+        time.sleep(delay)
+        self.result = read_clocks()
+
+    def start(self):
+        self.thread.start()
+
+    def join(self):
+        self.thread.join(timeout=60)
+        return self.result
 
 
 # ---------------------------------------------------------------------------
@@ -196,7 +243,8 @@ def median(x):
 def bench_phase_stuff(torch, w, dev, reps):
     st = setup_stuff(torch, w, dev)
     fl, pb, db = stuff_work(st)
-    run_stuff_step(st, None, plan=False)
+    for _ in range(WARMUP_REPS):
+        run_stuff_step(st, None, plan=False)
     torch.cuda.synchronize()
     timer = Timer(torch)
     for _ in range(reps):
@@ -257,8 +305,8 @@ def run_mixed(st, pool_index=0):
 def bench_phase_mixed(torch, dev, reps):
     st = setup_mixed(torch, dev)
     w = st["w"]
-    for i in range(len(st["pools"])):   # first touch of each pool (page-table walks)
-        run_mixed(st, i)
+    for i in range(max(WARMUP_REPS, len(st["pools"]))):   # includes first touch of each pool
+        run_mixed(st, i % len(st["pools"]))
     torch.cuda.synchronize()
     timer = Timer(torch)
     for r in range(reps):
@@ -308,7 +356,8 @@ def bench_phase_kv_write(torch, dev, reps):
         v = normal_bf16((ntok, w.hkv, w.d), 32, dev)
         kc = torch.empty((nblocks, w.hkv, 16, w.d), dtype=torch.bfloat16, device=dev)
         vc = torch.empty_like(kc)
-        binding.rag_kv_cache_write(k, v, kc, vc, slots)
+        for _ in range(WARMUP_REPS):
+            binding.rag_kv_cache_write(k, v, kc, vc, slots)
         torch.cuda.synchronize()
         timer = Timer(torch)
         for _ in range(reps):
@@ -349,7 +398,8 @@ def bench_phase_awq(torch, dev, reps, batches=(16, 8192), graph=True):
             y = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
             ws = torch.empty(max(binding.rag_awq_workspace_size(M, N, K), 1), dtype=torch.uint8,
                              device=dev)
-            binding.rag_awq_gemm(x, qw, sc, z, y, ws)
+            for _ in range(WARMUP_REPS):
+                binding.rag_awq_gemm(x, qw, sc, z, y, ws)
             torch.cuda.synchronize()
             want = y.clone()
             timer = Timer(torch)
@@ -486,21 +536,30 @@ def copy_calibration(torch, gib=1.0):
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawTextHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=10)
-    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-extra", action="store_true", help="skip the other workloads")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--extra-reps", type=int, default=5)
+    ap.add_argument("--extra-reps", type=int, default=20)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a 1 GiB device copy (counter calibration)")
     ap.add_argument("--awq-only", action="store_true",
                     help="only the int4-weight GEMM phase, eager calls (for profiling)")
+    ap.add_argument("--no-clocks", action="store_true",
+                    help="do not query amd-smi for the clocks (skipped under rocprofv3 anyway)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU: this build has no multi-GPU path "
               "(sequences shard across GPUs with no exchange; see DESIGN.md). "
               "Run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
+
+    # Clock readings come from an amd-smi child process; not under a profiler,
+    # whose preloaded library the child would inherit.
+    under_profiler = any(k.startswith("ROCPROF") for k in os.environ) or \
+        "rocprof" in os.environ.get("LD_PRELOAD", "")
+    want_clocks = not (args.no_clocks or under_profiler or args.copy_calibration or args.awq_only)
+    clocks = {"idle_before": read_clocks()} if want_clocks else None
 
     import torch
     if not torch.cuda.is_available():
@@ -571,7 +630,11 @@ def main():
         "roofline": dominant,
         "rooflines": {"prefill": rl_pf, "decode": rl_dec},
     }
+    sampler = None
     if not args.no_extra:
+        if want_clocks:
+            sampler = ClockSampler(delay=2.0)   # lands in the mapred7b / long70b phases
+            sampler.start()
         phases = {}
         for fn in (mapred7b, long70b):
             phases[fn.__name__] = bench_phase_stuff(torch, fn(), dev, args.extra_reps)
@@ -583,6 +646,10 @@ def main():
         res["phases"] = phases
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(torch, st)
+    if want_clocks:
+        clocks["under_load"] = sampler.join() if sampler else None
+        clocks["idle_after"] = read_clocks()
+        res["clocks"] = clocks
     print(json.dumps(res))
 
 
