@@ -202,16 +202,20 @@ def run_stuff_step(st, timer=None, plan=True):
                                     st["cu_t"], L, L, w.scale, True)
     if timer:
         timer.stop("prefill")
+    # The decode launches go back to back between one pair of events: an
+    # event pair around every launch would add the events' own cost to each
+    # (about 2.5 us of 81).  The average launch duration is the pair's time
+    # over the number of launches (inter-launch gaps included).
     pools = st.get("pools", [])
+    if timer and st["decode_steps"]:
+        timer.start("decode")
     for t in range(st["decode_steps"]):
         pool = pools[t % len(pools)]
-        if timer:
-            timer.start("decode")
         binding.rag_attn_decode_paged(st["dq"][t], pool.k_cache, pool.v_cache, st["do"],
                                       pool.block_tables, st["kv_steps"][t], w.scale,
                                       workspace=st["ws"])
-        if timer:
-            timer.stop("decode")
+    if timer and st["decode_steps"]:
+        timer.stop("decode")
 
 
 def stuff_work(st):
