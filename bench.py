@@ -526,6 +526,32 @@ def cpu_baseline(torch, st, budget_s=12.0):
 
 
 # ---------------------------------------------------------------------------
+def prefill_only(torch, name, dev, reps):
+    """The packed prefill of one workload, `reps` launches back to back (the
+    first warms up), for counter runs that should see nothing else."""
+    from paper_2412_10543_amd import binding, workloads
+    w = getattr(workloads, name)()
+    cu, _ = binding.rag_plan_prompts(w.method, w.query_lens, w.num_chunks, w.chunk_len,
+                                     w.intermediate_length, w.answer_len)
+    lens = [b - a for a, b in zip(cu[:-1], cu[1:])]
+    T = cu[-1]
+    q = workloads.normal_bf16((T, w.hq, w.d), w.seed, dev)
+    k = workloads.normal_bf16((T, w.hkv, w.d), w.seed + 1, dev)
+    v = workloads.normal_bf16((T, w.hkv, w.d), w.seed + 2, dev)
+    o = torch.empty_like(q)
+    cu_t = torch.tensor(cu, dtype=torch.int32, device=dev)
+    timer = Timer(torch)
+    for _ in range(reps):
+        timer.start("p")
+        binding.rag_attn_prefill_varlen(q, k, v, o, None, cu_t, cu_t, max(lens), max(lens),
+                                        w.scale, True)
+        timer.stop("p")
+    torch.cuda.synchronize()
+    return {"workload": name, "launches": reps, "ms": [round(x, 4) for x in timer.ms("p")],
+            "algorithmic_flops": prefill_flops(lens, lens, w.hq, w.d),
+            "algorithmic_bytes": prefill_bytes(lens, lens, w.hq, w.hkv, w.d)}
+
+
 def copy_calibration(torch, gib=1.0):
     """A plain device copy of known size, for scaling the HBM traffic counters."""
     n = int(gib * (1 << 30))
@@ -549,6 +575,9 @@ def main():
                     help="only run a 1 GiB device copy (counter calibration)")
     ap.add_argument("--awq-only", action="store_true",
                     help="only the int4-weight GEMM phase, eager calls (for profiling)")
+    ap.add_argument("--prefill-only", metavar="WORKLOAD",
+                    help="only run this workload's packed prefill --reps times (for counter runs)")
+    ap.add_argument("--reps", type=int, default=2)
     ap.add_argument("--no-clocks", action="store_true",
                     help="do not query amd-smi for the clocks (skipped under rocprofv3 anyway)")
     args = ap.parse_args()
@@ -562,7 +591,8 @@ def main():
     # whose preloaded library the child would inherit.
     under_profiler = any(k.startswith("ROCPROF") for k in os.environ) or \
         "rocprof" in os.environ.get("LD_PRELOAD", "")
-    want_clocks = not (args.no_clocks or under_profiler or args.copy_calibration or args.awq_only)
+    want_clocks = not (args.no_clocks or under_profiler or args.copy_calibration or args.awq_only
+                       or args.prefill_only)
     clocks = {"idle_before": read_clocks()} if want_clocks else None
 
     import torch
@@ -580,6 +610,9 @@ def main():
     from paper_2412_10543_amd.workloads import long70b, mapred7b, stuff7b
     binding.lib()
     dev = torch.device("cuda:0")
+    if args.prefill_only:
+        print(json.dumps(prefill_only(torch, args.prefill_only, dev, args.reps)))
+        return
 
     w = stuff7b()
     st = setup_stuff(torch, w, dev)
