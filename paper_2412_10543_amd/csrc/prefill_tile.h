@@ -499,8 +499,8 @@ struct PfGroup {
 //     tile are copied into LDS in the last three tiles of the current item,
 //     each into the stage the current item has just retired (so the HBM
 //     latency of Q is hidden behind the current item's compute);
-//   * the current item's output leaves (through LDS) after the next item's
-//     first tiles have been requested, and is not waited for.
+//   * the current item's output leaves (through LDS) between the requests
+//     of the next item's tiles 1 and 2, and is not waited for.
 // Rows past the sequence end are read from its last row (finite data; those
 // rows are never stored).
 // ---------------------------------------------------------------------------
@@ -821,9 +821,14 @@ __device__ __forceinline__ void prefill_items(const PfGroup& g, const KV& kv, co
     // output accumulators are untouched by the read.
     pf_read_q(st, (wave < 4 ? cur : next) + (wave & 3) * 32 * D);
     pf_barrier();                                // Q read, last PV done: cur, next, prev free
+    // Tile 1 goes out before the output stores and tile 2 after them.  The
+    // next item's first wait leaves one tile's copies in flight, and the
+    // vector-memory counter does not tell copies from stores: with the
+    // stores issued last, that wait also had to see tile 2 or the stores
+    // complete; issued between the tiles, only tile 2 stays in flight.
     if (ntn > 1) issue_tile(prev, kPfBN);
-    if (ntn > 2) issue_tile(next, 2 * kPfBN);
     pf_store(st, o_w, g.q_stride, lse_w, r0, nq, g.scale, cur + wave * 16 * D);
+    if (ntn > 2) issue_tile(next, 2 * kPfBN);
     // next item's stages: tile 0 in after, tile 1 in prev, tile 2 in next;
     // cur (the output staging) receives tile 3.
     bf16_t* const st_out = cur;
