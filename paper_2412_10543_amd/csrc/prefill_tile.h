@@ -371,13 +371,18 @@ struct PfPipeCtx {
 // step and empty asm statements on the values each step produces keep the
 // compiler from regrouping the work (left alone it clusters the MFMAs, and
 // the two units take turns).
-template <int D, int HK, int HV>
+// `hook(i)` runs at the start of step i (the steady loop issues the next
+// tile's copies through it, one instruction every other step).
+struct PfNoHook {
+  __device__ __forceinline__ void operator()(int) const {}
+};
+template <int D, int HK, int HV, class Hook = PfNoHook>
 __device__ __forceinline__ float pf_full_slot(PfState<D>& st, const ChunkLayout<D>& lay,
                                               const bf16_t* __restrict__ kst,
                                               const bf16_t* __restrict__ vstage,
                                               const f32x16& s_cur, f32x16& s_next,
                                               bf16x8 (&p_cur)[2], const bf16x8 (&p_prev)[2],
-                                              float c, float nm) {
+                                              float c, float nm, const Hook& hook = Hook()) {
   const bf16_t* vst = vstage + kPfBN * D;   // V follows K in a stage
   constexpr int kSteps = D / 16;          // QK MFMAs = PV MFMAs = steps
   constexpr int kDt = D / 32;
@@ -426,6 +431,7 @@ __device__ __forceinline__ float pf_full_slot(PfState<D>& st, const ChunkLayout<
 #pragma unroll
   for (int i = 0; i < kSteps; ++i) {
     if (i + 2 < kSteps) load(i + 2);
+    hook(i);
     __builtin_amdgcn_sched_barrier(0);
     acc = mfma32(ka[i], st.qf[i], acc);
     if (i + 1 < kSteps) arg(i + 1);
@@ -625,6 +631,39 @@ __device__ __forceinline__ void prefill_items(const PfGroup& g, const KV& kv, co
     }
     load_ids(k0 + kPfBN);   // the tile issued next is the following one
   };
+  // Instruction `part` (0..3: K, V, K, V) of issue_tile for a tile, in the
+  // same order (a paged cache's next page ids are read after the last); a
+  // partial tile goes out whole at part 0.
+  auto issue_tile_part = [&](bf16_t* stage, int k0, int part) {
+    if (k0 + kPfBN > nk) {
+      if (part == 0) issue_tile(stage, k0);
+      return;
+    }
+    const int g0 = wave * kInstr;
+    if (part >= 2 * kInstr) return;
+    if constexpr (KV::kPaged) {
+      int kr0, vr0, unused;
+      Lay::k_src(64 * g0, kr0, unused);
+      Lay::v_src(64 * g0, vr0, unused);
+      if (part == 0) dma16_s(kv.k + kv.at(pick(kr0 >> 4), 0), k_off0, stage + 64 * g0 * 8);
+      if (part == 1)
+        dma16_s(kv.v + kv.at(pick(vr0 >> 4), 0), v_off0, stage + kPfBN * D + 64 * g0 * 8);
+      if (part == 2)
+        dma16_s(kv.k + kv.at(pick(kr0 >> 4), 0) + 32, k_off0, stage + 64 * (g0 + 1) * 8);
+      if (part == 3)
+        dma16_s(kv.v + kv.at(pick((vr0 >> 4) + 1), 0), v_off0,
+                stage + kPfBN * D + 64 * (g0 + 1) * 8);
+      if (part == 2 * kInstr - 1) load_ids(k0 + kPfBN);
+    } else {
+      const bf16_t* kb = kv.krow(k0);
+      const bf16_t* vb = kv.vrow(k0);
+      if (part == 0) dma16_s(kb, k_off0, stage + 64 * g0 * 8);
+      if (part == 1) dma16_s(vb, v_off0, stage + kPfBN * D + 64 * g0 * 8);
+      if (part == 2) dma16_s(kb + 32, k_off0, stage + 64 * (g0 + 1) * 8);
+      if (part == 3)
+        dma16_s(vb + (size_t)16 * kv.stride, v_off0, stage + kPfBN * D + 64 * (g0 + 1) * 8);
+    }
+  };
   // Q rows of waves [4*part, 4*part + 4) of the item starting at row q0 (the
   // layout pf_read_q expects).
   auto issue_q = [&](bf16_t* stage, int part, int q0) {
@@ -764,8 +803,15 @@ __device__ __forceinline__ void prefill_items(const PfGroup& g, const KV& kv, co
       st.l += sum;
       wait_tiles(1);
       pf_barrier();
-      issue_tile(prev, (t + 3) * kPfBN);
-      sum = pf_full_slot<D, 0, 0>(st, lay, next, cur, sO, sE, pO, pE, cx.c, -st.m_used * cx.c);
+      // The copies of tile t+3 go out one instruction every other step of
+      // the slot rather than all at once: their LDS writes then interleave
+      // with the slot's LDS reads instead of arriving as one burst.
+      bf16_t* const dst = prev;
+      const int k3 = (t + 3) * kPfBN;
+      sum = pf_full_slot<D, 0, 0>(st, lay, next, cur, sO, sE, pO, pE, cx.c, -st.m_used * cx.c,
+                                  [&](int i) {
+                                    if ((i & 1) == 0) issue_tile_part(dst, k3, i >> 1);
+                                  });
       if (__builtin_expect(wave_any(!(sum <= kPfSumBound)), 0))
         sum = pf_reref(st, sO, cx.c, pO);
       st.l += sum;
