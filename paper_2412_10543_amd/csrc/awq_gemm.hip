@@ -254,6 +254,37 @@ __global__ __launch_bounds__(awq_lg::kThreads) void awq_gemm_lg_kernel(
       if (lane < 32) dma16(zeros + (size_t)g * N + szoff, (bf16_t*)(S + kX + kW + kSP + 1024));
     }
   };
+  // The same copies one part at a time (parts 0-1: X rows, group sums, scales
+  // and zero points; parts 2-3: code words), issued at k-steps 0-3 of the
+  // previous group rather than all at once after its barrier, so that their
+  // LDS writes interleave with that group's operand reads.
+  auto issue_part = [&](int g, int st, int part) {
+    char* S = lds + st * kStage;
+    if (part < 2) {
+      const bf16_t* xb = x + (size_t)m0 * K + (size_t)g * kAwqGroup;
+#pragma unroll
+      for (int jj = 0; jj < 2; ++jj) {
+        const int j = 2 * part + jj;
+        dma16_s(xb, xoff[j], (bf16_t*)(S + (4 * w + j) * 1024));
+      }
+      if (part == 0) {
+        if (w < 2) {
+          dma16_s(sp + (size_t)g * M * 8, spoff, (bf16_t*)(S + kX + kW + w * 1024));
+        } else if (w == 2) {
+          dma16((const char*)(scales + (size_t)g * N) + szoff, (bf16_t*)(S + kX + kW + kSP));
+        } else if (w == 3) {
+          if (lane < 32) dma16(zeros + (size_t)g * N + szoff, (bf16_t*)(S + kX + kW + kSP + 1024));
+        }
+      }
+    } else {
+      const uint32_t* wb = qw + ((size_t)g * N + n0) * 16;
+#pragma unroll
+      for (int jj = 0; jj < 2; ++jj) {
+        const int j = 2 * (part - 2) + jj;
+        dma16_s(wb, woff[j], (bf16_t*)(S + kX + (4 * w + j) * 1024));
+      }
+    }
+  };
   const int r = lane & 31, h = lane >> 5;
   f32x16 u[4][2];
 #pragma unroll
@@ -270,7 +301,8 @@ __global__ __launch_bounds__(awq_lg::kThreads) void awq_gemm_lg_kernel(
     // wave is done with the stage the next group's copies overwrite
     wait_vm<0>();
     __syncthreads();
-    if (it + 1 < n_groups) issue(g_begin + it + 1, (it + 1) % kStages);
+    const bool more = it + 1 < n_groups;
+    const int g_next = g_begin + it + 1, st_next = (it + 1) % kStages;
     const char* S = lds + (it % kStages) * kStage;
     const char* SX = S;
     const char* SW = S + kX;
@@ -328,6 +360,7 @@ __global__ __launch_bounds__(awq_lg::kThreads) void awq_gemm_lg_kernel(
       // one k-step at a time (the A operands of step t + 1 are loaded during
       // step t, no earlier: the accumulators need the registers)
       __builtin_amdgcn_sched_barrier(0);
+      if (t < 4 && more) issue_part(g_next, st_next, t);
       bf16x8 anxt[4];
       if (t < 7) {
 #pragma unroll
