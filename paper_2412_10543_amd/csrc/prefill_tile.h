@@ -766,6 +766,19 @@ __device__ __forceinline__ void prefill_items(const PfGroup& g, const KV& kv, co
       ++jobs;
     };
 
+    // An item of one or two key tiles leaves stages unused (after; next too
+    // for one tile): the next item's Q goes there now, where the loop end
+    // would have put it, instead of after the loop with nothing to hide it.
+    bool early0 = false, early1 = false;
+    if (has_next && nt == 1) {
+      issue_job(next, 0);
+      issue_job(after, 1);
+      early0 = early1 = true;
+    } else if (has_next && nt == 2) {
+      issue_job(after, 0);
+      early0 = true;
+    }
+
     f32x16 sE = {}, sO = {};
     bf16x8 pE[2] = {}, pO[2] = {};
     if (cx.nbw > 0) sE = pf_qk<D, 0>(st, lay, cur);
@@ -858,8 +871,8 @@ __device__ __forceinline__ void prefill_items(const PfGroup& g, const KV& kv, co
     // The next item's jobs the loop did not issue (those of tiles before 0)
     // go out now; the stages of tiles before nt-1 were retired by the last
     // barrier.
-    if (nt < 3) issue_job(cur, 0);
-    if (nt < 2) issue_job(next, 1);
+    if (nt < 3 && !early0) issue_job(cur, 0);
+    if (nt < 2 && !early1) issue_job(next, 1);
     if (nt < 1) issue_job(after, 2);
     wait_tiles(0);
     pf_barrier();                                // its Q and first tile are in LDS
