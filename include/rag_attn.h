@@ -300,26 +300,28 @@ rag_status rag_prune_config_space(const rag_query_profile *profile,
 
 /*
  * KV-cache memory requirement of one configuration, in bytes, with the
- * paper's 2% buffer: tokens * kv_bytes_per_token * 1.02, rounded up.  A call
- * holds its prompt and the tokens it generates.  stuff: one call of
- * num_chunks * chunk_len + query_len prompt tokens; map_rerank: num_chunks
- * calls of chunk_len + query_len, run together; map_reduce: the larger of its
- * num_chunks mappers (chunk_len + query_len prompt, intermediate_length
- * summary tokens each) and its reduce call (num_chunks * intermediate_length
- * + query_len).  -1 for an invalid argument.
+ * paper's 2% buffer: tokens * kv_bytes_per_token * 1.02, rounded up (Sec.
+ * "Joint configuration-scheduling adaptation").  It is the memory the
+ * configuration needs free to start -- the one quantity rag_choose_config
+ * compares with the available memory and ranks by.  A call holds its prompt
+ * and the tokens it generates.  stuff: one call of num_chunks * chunk_len +
+ * query_len prompt tokens; map_rerank: num_chunks calls of chunk_len +
+ * query_len, which run together; map_reduce: its largest single call, a
+ * mapper (chunk_len + query_len prompt, intermediate_length summary tokens)
+ * or the reduce call (num_chunks * intermediate_length + query_len), since
+ * its mappers enter the running batch one by one as memory allows and the
+ * reduce call runs after them.  -1 for an invalid argument.
  */
 int64_t rag_config_kv_bytes(int32_t method, int32_t num_chunks,
                             int32_t intermediate_length,
                             const rag_request_shape *shape);
 
 /*
- * Best-fit choice: among the configurations of the pruned space that can
- * start in available_bytes -- stuff and map_rerank when their whole
- * requirement fits, map_reduce when its largest single call fits (its mappers
- * enter the running batch as memory allows) -- the one with the highest
- * requirement; ties go to more chunks, then a longer intermediate length,
- * then stuff, map_reduce, map_rerank in that order.  If none fits, a cheaper
- * configuration just outside the space: stuff (joint reasoning) or
+ * Best-fit choice: among the configurations of the pruned space whose
+ * requirement (rag_config_kv_bytes) fits in available_bytes, the one with the
+ * highest requirement; ties go to more chunks, then a longer intermediate
+ * length, then stuff, map_reduce, map_rerank in that order.  If none fits, a
+ * cheaper configuration just outside the space: stuff (joint reasoning) or
  * map_rerank (otherwise) with as many chunks as fit (fallback = 1).  Returns
  * RAG_OK, RAG_NO_FIT (not even one chunk fits: the request waits; *out has
  * method -1) or RAG_ERR_INVALID_ARG.

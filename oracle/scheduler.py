@@ -11,24 +11,30 @@ Yes/No, pieces of information n, summarization length range) --
   * joint reasoning, high complexity -> stuff or map_reduce;
   * num_chunks in [n, 3n]; intermediate_length in the summary-length range.
 
-Sec. "Joint configuration-scheduling adaptation": the KV-cache memory of a
+Sec. "Joint configuration-scheduling adaptation": the memory requirement of a
 configuration follows from its token counts and the model's bytes per token,
-plus a 2% buffer; among the configurations of the pruned space that fit in the
-available GPU memory the one with the highest memory requirement is chosen;
-if none fits, a cheaper configuration just outside the space is used --
-map_rerank (no joint reasoning) or stuff (joint reasoning) with as many chunks
-as fit -- and if not even that fits, the request waits.
+plus a 2% buffer; it is compared with the available GPU memory to see what
+fits, and among the configurations of the pruned space that fit, the one with
+the highest requirement is chosen; if none fits, a cheaper configuration just
+outside the space is used -- map_rerank (no joint reasoning) or stuff (joint
+reasoning) with as many chunks as fit -- and if not even that fits, the
+request waits.
 
-Readings (the paper gives no formulas): a call's KV holds its prompt and the
-tokens it generates (answer_len for answer calls, intermediate_length for a
-mapper); stuff is one call of n*C + Lq prompt tokens; map_rerank's n calls
-run together (the fallback's "as many chunks as fit"); map_reduce's mappers
-are admitted into the running batch as memory allows (the scheduling
-illustration: its mappers start while stuff would queue), so it fits when its
-largest single call fits; its requirement is the larger of its n mappers and
-its reduce call.  Ties are broken towards more chunks, then a longer
-intermediate length, then the method listed first (stuff, map_reduce,
-map_rerank).
+Readings (the paper gives no formulas):
+  * a call's KV holds its prompt and the tokens it generates (answer_len for
+    an answer, intermediate_length for a mapper's summary);
+  * the requirement is ONE quantity, used both to decide fit and to rank: the
+    KV memory the configuration must have free to start.  stuff: its one call
+    of n*C + Lq prompt tokens.  map_rerank: its n calls of C + Lq, which run
+    together (the fallback takes "as many chunks as fit").  map_reduce: its
+    largest single call -- a mapper (C + Lq + IL) or the reduce call
+    (n*IL + Lq + answer) -- because its mappers enter the running batch one by
+    one as memory allows and the reduce call runs after they have finished
+    (the scheduling illustration: with 20 chunks and intermediate length 100,
+    map_reduce starts in memory where stuff has to queue, so its requirement
+    is below stuff's);
+  * ties go to more chunks, then a longer intermediate length, then the method
+    listed first (stuff, map_reduce, map_rerank).
 """
 from __future__ import annotations
 
@@ -52,31 +58,27 @@ def kv_bytes(tokens: int, bytes_per_token: int) -> int:
     return -(-tokens * bytes_per_token * 102 // 100)
 
 
-def call_tokens(method, n, il, query_len, chunk_len, answer_len):
-    """Token counts of the LLM calls of a configuration: (calls run together
-    first, the calls after them)."""
+def resident_sets(method, n, il, query_len, chunk_len, answer_len):
+    """Token counts of the groups of calls that must be resident together for
+    the configuration to run: one group per start condition."""
     if method == STUFF:
-        return [n * chunk_len + query_len + answer_len], []
+        return [[n * chunk_len + query_len + answer_len]]
     if method == MAP_RERANK:
-        return [chunk_len + query_len + answer_len] * n, []
-    mappers = [chunk_len + query_len + il] * n
-    return mappers, [n * il + query_len + answer_len]
+        return [[chunk_len + query_len + answer_len] * n]
+    # map_reduce: any one mapper (the rest follow as memory frees), then the
+    # reduce call once the mappers are done
+    return [[chunk_len + query_len + il], [n * il + query_len + answer_len]]
 
 
 def requirement(method, n, il, shape):
-    first, later = call_tokens(method, n, il, shape["query_len"], shape["chunk_len"],
-                               shape["answer_len"])
-    bpt = shape["bytes_per_token"]
-    return max(kv_bytes(sum(first), bpt), kv_bytes(sum(later), bpt) if later else 0)
+    """Memory the configuration needs free to start (see the readings)."""
+    sets = resident_sets(method, n, il, shape["query_len"], shape["chunk_len"],
+                         shape["answer_len"])
+    return max(kv_bytes(sum(s), shape["bytes_per_token"]) for s in sets)
 
 
 def fits(method, n, il, shape, available: int) -> bool:
-    first, later = call_tokens(method, n, il, shape["query_len"], shape["chunk_len"],
-                               shape["answer_len"])
-    bpt = shape["bytes_per_token"]
-    if method == MAP_REDUCE:
-        return max(kv_bytes(t, bpt) for t in first + later) <= available
-    return kv_bytes(sum(first), bpt) <= available
+    return requirement(method, n, il, shape) <= available
 
 
 def candidates(methods, chunks, ils):

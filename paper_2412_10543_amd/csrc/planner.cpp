@@ -17,32 +17,22 @@ constexpr uint32_t bit(int m) { return 1u << m; }
 // KV memory of `tokens` tokens with the 2% buffer, rounded up to a byte.
 int64_t kv_of(int64_t tokens, int64_t bpt) { return (tokens * bpt * 102 + 99) / 100; }
 
-struct Need {
-  int64_t requirement;   // memory the configuration holds once running
-  int64_t admit;         // memory that must be free for it to start
-};
-
-// Token counts of the configuration's calls (a call holds its prompt and the
-// tokens it generates): stuff one call of n*C + Lq prompt tokens; map_rerank n
-// calls of C + Lq that run together; map_reduce n mappers of C + Lq that each
-// write `il` summary tokens, admitted as memory allows, then a reduce call of
-// n*il + Lq.
-Need need_of(int method, int64_t n, int64_t il, const rag_request_shape& s) {
+// Memory a configuration needs free to start: one quantity, used both to
+// decide whether it fits and to rank the configurations that do.  A call
+// holds its prompt and the tokens it generates.  stuff: its one call of
+// n*C + Lq prompt tokens; map_rerank: its n calls of C + Lq, which run
+// together; map_reduce: its largest single call -- a mapper of C + Lq that
+// writes `il` summary tokens, or the reduce call of n*il + Lq -- because the
+// mappers enter the running batch one by one as memory allows and the reduce
+// call starts after they have finished.
+int64_t requirement_of(int method, int64_t n, int64_t il, const rag_request_shape& s) {
   const int64_t bpt = s.kv_bytes_per_token;
   const int64_t c = s.chunk_len, q = s.query_len, a = s.answer_len;
-  Need r{0, 0};
-  if (method == RAG_STUFF) {
-    r.requirement = r.admit = kv_of(n * c + q + a, bpt);
-  } else if (method == RAG_MAP_RERANK) {
-    r.requirement = r.admit = kv_of(n * (c + q + a), bpt);
-  } else {
-    const int64_t mappers = kv_of(n * (c + q + il), bpt);
-    const int64_t reduce = kv_of(n * il + q + a, bpt);
-    const int64_t one_mapper = kv_of(c + q + il, bpt);
-    r.requirement = mappers > reduce ? mappers : reduce;
-    r.admit = one_mapper > reduce ? one_mapper : reduce;
-  }
-  return r;
+  if (method == RAG_STUFF) return kv_of(n * c + q + a, bpt);
+  if (method == RAG_MAP_RERANK) return kv_of(n * (c + q + a), bpt);
+  const int64_t one_mapper = kv_of(c + q + il, bpt);
+  const int64_t reduce = kv_of(n * il + q + a, bpt);
+  return one_mapper > reduce ? one_mapper : reduce;
 }
 
 rag_status check_shape(const rag_request_shape* s) {
@@ -97,7 +87,7 @@ int64_t rag_config_kv_bytes(int32_t method, int32_t num_chunks, int32_t intermed
                             const rag_request_shape* shape) {
   if (check_shape(shape) != RAG_OK || num_chunks < 0 || intermediate_length < 0) return -1;
   if (method != RAG_STUFF && method != RAG_MAP_REDUCE_MAP && method != RAG_MAP_RERANK) return -1;
-  return need_of(method, num_chunks, intermediate_length, *shape).requirement;
+  return requirement_of(method, num_chunks, intermediate_length, *shape);
 }
 
 rag_status rag_choose_config(const rag_query_profile* profile, const rag_request_shape* shape,
@@ -111,9 +101,9 @@ rag_status rag_choose_config(const rag_query_profile* profile, const rag_request
   rag_config_space sp;
   rag_prune_config_space(profile, &sp);
   // Best fit: the configuration of the pruned space with the highest memory
-  // requirement among those that can start in the available memory; ties go to
-  // more chunks, a longer intermediate length, then stuff, map_reduce,
-  // map_rerank in that order.
+  // requirement among those whose requirement fits in the available memory;
+  // ties go to more chunks, a longer intermediate length, then stuff,
+  // map_reduce, map_rerank in that order.
   bool found = false;
   rag_config best{};
   const int order[3] = {RAG_STUFF, RAG_MAP_REDUCE_MAP, RAG_MAP_RERANK};
@@ -124,15 +114,15 @@ rag_status rag_choose_config(const rag_query_profile* profile, const rag_request
     const int il_hi = m == RAG_MAP_REDUCE_MAP ? sp.intermediate_length_max : 0;
     for (int n = sp.num_chunks_min; n <= sp.num_chunks_max; ++n)
       for (int il = il_lo; il <= il_hi; ++il) {
-        const Need nd = need_of(m, n, il, *shape);
-        if (nd.admit > available_bytes) continue;
+        const int64_t need = requirement_of(m, n, il, *shape);
+        if (need > available_bytes) continue;
         const bool better =
-            !found || nd.requirement > best.kv_bytes ||
-            (nd.requirement == best.kv_bytes &&
+            !found || need > best.kv_bytes ||
+            (need == best.kv_bytes &&
              (n > best.num_chunks ||
               (n == best.num_chunks && il > best.intermediate_length)));
         if (better) {
-          best = rag_config{m, n, il, 0, nd.requirement};
+          best = rag_config{m, n, il, 0, need};
           found = true;
         }
       }
@@ -143,9 +133,9 @@ rag_status rag_choose_config(const rag_query_profile* profile, const rag_request
     // with as many chunks as fit; if not even one chunk fits, the request waits.
     const int m = profile->joint_reasoning ? RAG_STUFF : RAG_MAP_RERANK;
     for (int n = sp.num_chunks_max; n >= 1 && !found; --n) {
-      const Need nd = need_of(m, n, 0, *shape);
-      if (nd.admit <= available_bytes) {
-        best = rag_config{m, n, 0, 1, nd.requirement};
+      const int64_t need = requirement_of(m, n, 0, *shape);
+      if (need <= available_bytes) {
+        best = rag_config{m, n, 0, 1, need};
         found = true;
       }
     }

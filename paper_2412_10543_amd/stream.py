@@ -5,8 +5,8 @@ Each query arrives (Poisson arrivals, as in the paper's evaluation, Sec.
 "Setup") with a profile; when the engine admits it, rag_choose_config picks its
 configuration from the KV memory free at that moment (Sec. "Joint
 configuration-scheduling adaptation"), and the configuration becomes LLM calls
-(rag_plan_prompts' shapes: one stuff call, n mappers then a reduce call, or n
-map_rerank calls).  An engine iteration
+whose prompt and decode lengths come from rag_plan_prompts (one stuff call, n
+mappers then a reduce call, or n map_rerank calls).  An engine iteration
   1. admits waiting queries in arrival order while the planner finds a
      configuration that fits (a query that does not fit waits, and so do the
      queries behind it), and admits queued calls (mappers, reduce calls) whose
@@ -121,17 +121,23 @@ class Engine:
         return torch.randn(shape, generator=self.gen, device=self.dev).to(torch.bfloat16)
 
     # -- admission ------------------------------------------------------------
-    def _first_calls(self, q: Query) -> List[Call]:
+    def _planned_calls(self, q: Query, method: str, kind: str) -> List[Call]:
+        """The LLM calls of one synthesis phase, with the prompt and decode
+        lengths rag_plan_prompts gives for this query and configuration."""
         cfg = q.config
-        n, m = cfg["num_chunks"], cfg["method"]
+        cu, dec = binding.rag_plan_prompts(method, [q.query_len], [cfg["num_chunks"]],
+                                           self.chunk_len, cfg["intermediate_length"],
+                                           self.answer_len)
+        return [Call(q, cu[i + 1] - cu[i], dec[i], kind) for i in range(len(dec))]
+
+    def _first_calls(self, q: Query) -> List[Call]:
+        m = q.config["method"]
         if m == "stuff":
-            calls = [Call(q, n * self.chunk_len + q.query_len, self.answer_len, "stuff")]
+            calls = self._planned_calls(q, "stuff", "stuff")
         elif m == "map_rerank":
-            calls = [Call(q, self.chunk_len + q.query_len, self.answer_len, "rerank")
-                     for _ in range(n)]
+            calls = self._planned_calls(q, "map_rerank", "rerank")
         else:
-            calls = [Call(q, self.chunk_len + q.query_len, cfg["intermediate_length"], "mapper")
-                     for _ in range(n)]
+            calls = self._planned_calls(q, "map_reduce_map", "mapper")
         q.pending = len(calls)
         return calls
 
@@ -241,11 +247,9 @@ class Engine:
             if q.pending > 0:
                 continue
             if c.kind == "mapper":                     # all summaries written: reduce
-                cfg = q.config
-                q.pending = 1
-                self.queued_calls.append(Call(
-                    q, cfg["num_chunks"] * cfg["intermediate_length"] + q.query_len,
-                    self.answer_len, "reduce"))
+                reduce = self._planned_calls(q, "map_reduce_reduce", "reduce")
+                q.pending = len(reduce)
+                self.queued_calls.extend(reduce)
             else:
                 q.finished = now
         self.running = keep

@@ -78,6 +78,32 @@ def test_best_fit_example_through_library():
     assert {k: got[k] for k in b["choice"]} == b["choice"]
 
 
+def _choose(profile, shape, avail):
+    return binding.rag_choose_config(profile["complexity_high"], profile["joint_reasoning"],
+                                     profile["pieces"], tuple(profile["summary_range"]),
+                                     shape["query_len"], shape["chunk_len"], shape["answer_len"],
+                                     shape["bytes_per_token"], avail)
+
+
+def test_hand_computed_requirements_through_library():
+    sh = GOLDEN["shape_7b"]
+    for c in GOLDEN["requirements"]:
+        assert binding.rag_config_kv_bytes(c["method"], c["num_chunks"], c["intermediate_length"],
+                                           sh["query_len"], sh["chunk_len"], sh["answer_len"],
+                                           sh["bytes_per_token"]) == c["kv_bytes"], c["cite"]
+
+
+def test_scheduling_and_fallback_examples_through_library():
+    """A complex profile: ample memory gives stuff, memory below stuff's
+    minimum but above one map_reduce call gives map_reduce, then the stuff
+    fallback, then a wait; and the two fallback methods."""
+    sh = GOLDEN["shape_7b"]
+    for c in GOLDEN["scheduling"]["cases"]:
+        assert _choose(GOLDEN["scheduling"]["profile"], sh, c["available"]) == c["choice"], c["why"]
+    for c in GOLDEN["fallback"]["cases"]:
+        assert _choose(c["profile"], sh, c["available"]) == c["choice"], c["why"]
+
+
 @pytest.mark.parametrize("args", [
     dict(pieces=0), dict(summary_range=(50, 40)), dict(summary_range=(0, 10)),
     dict(complexity_high=2), dict(bytes_per_token=0), dict(query_len=-1),
