@@ -31,6 +31,10 @@
  *     synchronously and returns RAG_ERR_INVALID_ARG on a violation).
  *   - Calls are thread-safe; the only mutable global state is the
  *     thread-local error message.
+ *   - RAG_ATTN_PF_ITEMS=n (read at each rag_attn_prefill_varlen call) fixes
+ *     how many query tiles one prefill workgroup runs in sequence instead of
+ *     the library's load-balancing choice; a testing and tuning knob that
+ *     changes no output bit.
  *
  * Attention here is softmax(q k^T * softmax_scale) v per query row, with
  * grouped-query heads (q head h reads kv head h / (num_q_heads / num_kv_heads))

@@ -7,6 +7,7 @@
 //                          paged cache in one launch
 #include <algorithm>
 #include <climits>
+#include <cstdlib>
 
 #include "common.h"
 #include "decode_unit.h"
@@ -69,6 +70,17 @@ __device__ __forceinline__ int snake_tile(int j, int k, int per) {
 struct PfSplit {
   int items, per, n_qt;
 };
+// RAG_ATTN_PF_ITEMS=n (read at each launch) fixes the query tiles per
+// workgroup at n instead of the load-balancing choice below: a testing and
+// tuning knob (every tile is computed the same way whichever workgroup runs
+// it, so outputs are bit-identical for any n).
+static int pf_items_override() {
+  const char* e = std::getenv("RAG_ATTN_PF_ITEMS");
+  if (e == nullptr || e[0] == 0) return 0;
+  const int n = std::atoi(e);
+  return n >= 1 ? std::min(n, kPfMaxItems) : 0;
+}
+
 static PfSplit pf_split(int num_seqs, int hkv, int group, int max_seqlen_q, bool multi) {
   const int rows = pf_rows_per_tile(group, kPfWavesDense);
   PfSplit p;
@@ -77,6 +89,11 @@ static PfSplit pf_split(int num_seqs, int hkv, int group, int max_seqlen_q, bool
   if (!multi || p.n_qt <= 1) {
     p.items = 1;
     p.per = p.n_qt;
+    return p;
+  }
+  if (const int forced = pf_items_override()) {
+    p.items = std::min(forced, p.n_qt);
+    p.per = (p.n_qt + p.items - 1) / p.items;
     return p;
   }
   const int64_t want = (int64_t)kPfWgPerCu * kPfCus;
