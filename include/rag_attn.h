@@ -30,7 +30,8 @@
  *     RAG_ATTN_CHECK=1 is set (the call then copies them to the host
  *     synchronously and returns RAG_ERR_INVALID_ARG on a violation).
  *   - Calls are thread-safe; the only mutable global state is the
- *     thread-local error message.
+ *     thread-local error message (and the static scratch of
+ *     rag_attn_decode_paged_noalloc, see there).
  *   - RAG_ATTN_PF_ITEMS=n (read at each rag_attn_prefill_varlen call) fixes
  *     how many query tiles one prefill workgroup runs in sequence instead of
  *     the library's load-balancing choice; a testing and tuning knob that
@@ -183,6 +184,36 @@ rag_status rag_attn_decode_paged(const void *q, const void *k_cache,
                                  float softmax_scale, int32_t num_splits,
                                  void *workspace, size_t workspace_bytes,
                                  hipStream_t stream);
+
+/*
+ * rag_attn_decode_paged without a workspace argument, for callers that cannot
+ * allocate device memory: code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc.  Arguments, results and errors are those of
+ * rag_attn_decode_paged (same kernels, same split policy, bit-identical
+ * outputs); the split partials and arrival counters live instead in a static
+ * per-device scratch array inside the library (32 MiB per GPU the library
+ * runs on, held until the process ends; set up on the current device at the
+ * first call, which zeroes its counters with a small kernel on `stream`).  The
+ * call allocates and frees nothing.  It returns RAG_ERR_WORKSPACE when the
+ * decode rows need more than 65,536 (row, kv head) counters or more than
+ * 32 MiB - 256 KiB of partials (num_decode_seqs * num_q_heads * splits *
+ * (head_dim + 1) * 4 bytes, each part rounded up to 256).  Every call on a GPU
+ * shares that GPU's scratch: calls that may overlap on one GPU (different
+ * streams, or graphs replayed concurrently) race and must be serialised by the
+ * caller.
+ */
+rag_status rag_attn_decode_paged_noalloc(const void *q, const void *k_cache,
+                                         const void *v_cache, void *o,
+                                         const int32_t *block_tables,
+                                         const int32_t *kv_lens,
+                                         const int32_t *cu_seqlens_q,
+                                         int32_t num_seqs, int32_t num_decode_seqs,
+                                         int32_t max_blocks_per_seq,
+                                         int32_t max_seqlen_q, int32_t num_blocks,
+                                         int32_t num_q_heads, int32_t num_kv_heads,
+                                         int32_t head_dim, int32_t block_size,
+                                         float softmax_scale, int32_t num_splits,
+                                         hipStream_t stream);
 
 /*
  * Paged KV-cache write: store the keys and values of a batch of new tokens in

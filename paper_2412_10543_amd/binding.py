@@ -47,7 +47,7 @@ _lib = None
 def exported_symbols():
     return ["rag_abi_version", "rag_last_error", "rag_attn_prefill_varlen",
             "rag_attn_decode_num_splits", "rag_attn_decode_workspace_size",
-            "rag_attn_decode_paged", "rag_kv_cache_write", "rag_plan_prompts",
+            "rag_attn_decode_paged", "rag_attn_decode_paged_noalloc", "rag_kv_cache_write", "rag_plan_prompts",
             "rag_prune_config_space", "rag_config_kv_bytes", "rag_choose_config",
             "rag_device_free_memory", "rag_awq_pack_weights", "rag_awq_workspace_size",
             "rag_awq_gemm"]
@@ -98,6 +98,10 @@ def lib():
     L.rag_attn_decode_paged.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _i32, _i32, _i32,
                                         _i32, _i32, _i32, _i32, _i32, _i32, ctypes.c_float,
                                         _i32, _vp, ctypes.c_size_t, _vp]
+    L.rag_attn_decode_paged_noalloc.restype = ctypes.c_int
+    L.rag_attn_decode_paged_noalloc.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _i32, _i32,
+                                                _i32, _i32, _i32, _i32, _i32, _i32, _i32,
+                                                ctypes.c_float, _i32, _vp]
     L.rag_kv_cache_write.restype = ctypes.c_int
     L.rag_kv_cache_write.argtypes = [_vp, _vp, _vp, _vp, _vp, _i32, _i32, _i32, _i32, _i32, _vp]
     L.rag_prune_config_space.restype = ctypes.c_int
@@ -218,6 +222,29 @@ def rag_attn_decode_paged(q, k_cache, v_cache, o, block_tables, kv_lens, softmax
         int(max_seqlen_q), k_cache.shape[0], q.shape[1], k_cache.shape[1], q.shape[2],
         k_cache.shape[2], float(softmax_scale), int(num_splits), _ptr(workspace), ws_bytes,
         _stream(stream)))
+
+
+def rag_attn_decode_paged_noalloc(q, k_cache, v_cache, o, block_tables, kv_lens, softmax_scale,
+                                  cu_seqlens_q=None, num_decode_seqs=None, max_seqlen_q=1,
+                                  num_splits=0, stream=None) -> None:
+    """rag_attn_decode_paged with the library's static scratch instead of a
+    workspace (allocates nothing)."""
+    for t, n in ((q, "q"), (o, "o")):
+        _need(t, torch.bfloat16, n, 3)
+    for t, n in ((k_cache, "k_cache"), (v_cache, "v_cache")):
+        _need(t, torch.bfloat16, n, 4)
+    _need(block_tables, torch.int32, "block_tables", 2)
+    _need(kv_lens, torch.int32, "kv_lens", 1)
+    if cu_seqlens_q is not None:
+        _need(cu_seqlens_q, torch.int32, "cu_seqlens_q", 1)
+    num_seqs = block_tables.shape[0]
+    if num_decode_seqs is None:
+        num_decode_seqs = num_seqs
+    _check(lib().rag_attn_decode_paged_noalloc(
+        _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(o), _ptr(block_tables), _ptr(kv_lens),
+        _ptr(cu_seqlens_q), num_seqs, int(num_decode_seqs), block_tables.shape[1],
+        int(max_seqlen_q), k_cache.shape[0], q.shape[1], k_cache.shape[1], q.shape[2],
+        k_cache.shape[2], float(softmax_scale), int(num_splits), _stream(stream)))
 
 
 def rag_kv_cache_write(k, v, k_cache, v_cache, slot_mapping, stream=None) -> None:

@@ -26,7 +26,8 @@ COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-I", INCLUDE,
 # ordinary VGPRs, where the per-group rescaling (a VALU multiply) can reach
 # them without AGPR copies.
 SOURCE_FLAGS = {"awq_gemm.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]}
-SOURCES = ["kernels.hip", "kv_cache.hip", "awq_gemm.hip", "api.cpp", "awq_api.cpp", "planner.cpp"]
+SOURCES = ["kernels.hip", "kv_cache.hip", "awq_gemm.hip", "decode_scratch.hip", "api.cpp",
+           "awq_api.cpp", "planner.cpp"]
 HEADERS = ["common.h", "prefill_tile.h", "decode_unit.h", "launch.h", "errors.h", "awq.h"]
 
 

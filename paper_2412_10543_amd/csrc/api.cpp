@@ -121,6 +121,131 @@ WsLayout workspace_layout(int32_t num_decode, int32_t hq, int32_t hkv, int32_t d
   return w;
 }
 
+// The decode call behind both entry points.  scratch == false: the split
+// partials go to the caller's workspace (standard layout).  scratch == true:
+// to the library's static per-device scratch (rag::decode_scratch); workspace
+// and workspace_bytes are then unused.
+rag_status decode_paged_impl(const void* q, const void* k_cache, const void* v_cache, void* o,
+                             const int32_t* block_tables, const int32_t* kv_lens,
+                             const int32_t* cu_seqlens_q, int32_t num_seqs,
+                             int32_t num_decode_seqs, int32_t max_blocks_per_seq,
+                             int32_t max_seqlen_q, int32_t num_blocks, int32_t num_q_heads,
+                             int32_t num_kv_heads, int32_t head_dim, int32_t block_size,
+                             float softmax_scale, int32_t num_splits, void* workspace,
+                             size_t workspace_bytes, bool scratch, hipStream_t stream) {
+  if (!q || !k_cache || !v_cache || !o || !block_tables || !kv_lens)
+    return fail(RAG_ERR_INVALID_ARG, "decode: null pointer argument");
+  if (num_seqs < 0 || max_blocks_per_seq < 0 || num_blocks < 0 || max_seqlen_q < 0 ||
+      num_splits < 0)
+    return fail(RAG_ERR_INVALID_ARG, "decode: negative size");
+  if (num_q_heads <= 0 || num_kv_heads <= 0 || num_q_heads % num_kv_heads != 0)
+    return fail(RAG_ERR_INVALID_ARG, "decode: num_q_heads %d must be a positive multiple of "
+                                     "num_kv_heads %d", num_q_heads, num_kv_heads);
+  if (!(softmax_scale > 0.f) || softmax_scale > 1e30f)
+    return fail(RAG_ERR_INVALID_ARG, "decode: softmax_scale must be positive and finite");
+  if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned16(o))
+    return fail(RAG_ERR_INVALID_ARG, "decode: q/k_cache/v_cache/o must be 16-byte aligned");
+  if (head_dim != 64 && head_dim != 128)
+    return fail(RAG_ERR_UNSUPPORTED, "decode: head_dim %d (supported: 64, 128)", head_dim);
+  if (block_size != kBlock)
+    return fail(RAG_ERR_UNSUPPORTED, "decode: block_size %d (supported: 16)", block_size);
+  const int32_t num_decode = cu_seqlens_q ? num_decode_seqs : num_seqs;
+  if (num_decode < 0 || num_decode > num_seqs)
+    return fail(RAG_ERR_INVALID_ARG, "decode: num_decode_seqs %d outside [0, %d]",
+                num_decode_seqs, num_seqs);
+  if (num_decode > 0 && num_q_heads / num_kv_heads > kMaxGroupDecode)
+    return fail(RAG_ERR_UNSUPPORTED, "decode: %d q heads per kv head (max %d)",
+                num_q_heads / num_kv_heads, kMaxGroupDecode);
+  if (num_seqs == 0) return ok();
+  if (max_blocks_per_seq == 0) return fail(RAG_ERR_INVALID_ARG, "decode: max_blocks_per_seq is 0");
+
+  const int32_t splits =
+      num_decode > 0 ? resolve_splits(num_decode, num_kv_heads, max_blocks_per_seq, num_splits)
+                     : 1;
+  const WsLayout ws = workspace_layout(num_decode, num_q_heads, num_kv_heads, head_dim, splits);
+  const size_t need = ws.bytes;
+  if (!scratch && need > 0 && (workspace == nullptr || workspace_bytes < need))
+    return fail(RAG_ERR_WORKSPACE, "decode: workspace of %zu bytes needed, %zu given", need,
+                workspace == nullptr ? (size_t)0 : workspace_bytes);
+  if (!scratch && need > 0 && (reinterpret_cast<uintptr_t>(workspace) & 255u) != 0)
+    return fail(RAG_ERR_INVALID_ARG, "decode: workspace must be 256-byte aligned");
+  const int32_t group = num_q_heads / num_kv_heads;
+  const bool mixed = cu_seqlens_q != nullptr && num_seqs > num_decode;
+  const int64_t grid =
+      (mixed ? rag::paged_prefill_grid(num_seqs - num_decode, num_kv_heads, group, max_seqlen_q)
+             : 0) +
+      rag::paged_decode_grid(num_decode, num_kv_heads, splits) + 8;   // + group padding
+  if (grid > INT_MAX) return fail(RAG_ERR_UNSUPPORTED, "decode: batch too large for one grid");
+
+  if (check_mode()) {
+    std::vector<int32_t> kl, bt, cq;
+    if (!fetch(kl, kv_lens, num_seqs, stream) ||
+        !fetch(bt, block_tables, (size_t)num_seqs * max_blocks_per_seq, stream) ||
+        (cu_seqlens_q && !fetch(cq, cu_seqlens_q, num_seqs + 1, stream)))
+      return fail(RAG_ERR_HIP, "decode: debug copy of device arrays failed");
+    if (cu_seqlens_q) {
+      rag_status st = check_cu(cq, "cu_seqlens_q", std::max(max_seqlen_q, 1));
+      if (st != RAG_OK) return st;
+    }
+    for (int32_t s = 0; s < num_seqs; ++s) {
+      const int32_t n = kl[s];
+      const int32_t nq = cu_seqlens_q ? cq[s + 1] - cq[s] : 1;
+      if (n < 1 || (int64_t)n > (int64_t)max_blocks_per_seq * kBlock)
+        return fail(RAG_ERR_INVALID_ARG, "decode: kv_lens[%d] = %d outside [1, %d]", s, n,
+                    max_blocks_per_seq * kBlock);
+      if (s < num_decode && nq != 1)
+        return fail(RAG_ERR_INVALID_ARG, "decode: decode sequence %d has %d query rows", s, nq);
+      if (nq > n)
+        return fail(RAG_ERR_INVALID_ARG, "decode: sequence %d has %d query rows > %d keys", s,
+                    nq, n);
+      for (int32_t b = 0; b < (n + kBlock - 1) / kBlock; ++b) {
+        const int32_t id = bt[(size_t)s * max_blocks_per_seq + b];
+        if (id < 0 || id >= num_blocks)
+          return fail(RAG_ERR_INVALID_ARG, "decode: block_tables[%d][%d] = %d outside [0, %d)",
+                      s, b, id, num_blocks);
+      }
+    }
+  }
+
+  rag::PagedArgs a;
+  a.q = q;
+  a.k_cache = k_cache;
+  a.v_cache = v_cache;
+  a.o = o;
+  a.block_tables = block_tables;
+  a.kv_lens = kv_lens;
+  a.cu_q = cu_seqlens_q;
+  a.num_seqs = num_seqs;
+  a.num_decode = num_decode;
+  a.max_blocks = max_blocks_per_seq;
+  a.max_seqlen_q = max_seqlen_q;
+  a.hq = num_q_heads;
+  a.hkv = num_kv_heads;
+  a.d = head_dim;
+  a.num_splits = splits;
+  a.scale = softmax_scale;
+  a.arrivals = nullptr;
+  a.part_o = a.part_lse = nullptr;
+  if (need > 0 && scratch) {
+    // counters in the scratch's own counter region, partials after it
+    const size_t counters = (size_t)num_decode * num_kv_heads;
+    const size_t partials = need - ws.o_off;
+    char* part = nullptr;
+    const rag_status st = rag::decode_scratch(counters, partials, stream, &a.arrivals, &part);
+    if (st != RAG_OK) return st;
+    a.part_o = reinterpret_cast<float*>(part);
+    a.part_lse = reinterpret_cast<float*>(part + (ws.lse_off - ws.o_off));
+  } else if (need > 0) {
+    char* wsb = static_cast<char*>(workspace);
+    a.arrivals = reinterpret_cast<int*>(wsb);
+    a.part_o = reinterpret_cast<float*>(wsb + ws.o_off);
+    a.part_lse = reinterpret_cast<float*>(wsb + ws.lse_off);
+  }
+  const hipError_t e = rag::launch_paged(a, stream);
+  if (e != hipSuccess) return fail(RAG_ERR_HIP, "decode launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
 }  // namespace
 
 extern "C" {
@@ -203,104 +328,25 @@ rag_status rag_attn_decode_paged(const void* q, const void* k_cache, const void*
                                  int32_t num_kv_heads, int32_t head_dim, int32_t block_size,
                                  float softmax_scale, int32_t num_splits, void* workspace,
                                  size_t workspace_bytes, hipStream_t stream) {
-  if (!q || !k_cache || !v_cache || !o || !block_tables || !kv_lens)
-    return fail(RAG_ERR_INVALID_ARG, "decode: null pointer argument");
-  if (num_seqs < 0 || max_blocks_per_seq < 0 || num_blocks < 0 || max_seqlen_q < 0 ||
-      num_splits < 0)
-    return fail(RAG_ERR_INVALID_ARG, "decode: negative size");
-  if (num_q_heads <= 0 || num_kv_heads <= 0 || num_q_heads % num_kv_heads != 0)
-    return fail(RAG_ERR_INVALID_ARG, "decode: num_q_heads %d must be a positive multiple of "
-                                     "num_kv_heads %d", num_q_heads, num_kv_heads);
-  if (!(softmax_scale > 0.f) || softmax_scale > 1e30f)
-    return fail(RAG_ERR_INVALID_ARG, "decode: softmax_scale must be positive and finite");
-  if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned16(o))
-    return fail(RAG_ERR_INVALID_ARG, "decode: q/k_cache/v_cache/o must be 16-byte aligned");
-  if (head_dim != 64 && head_dim != 128)
-    return fail(RAG_ERR_UNSUPPORTED, "decode: head_dim %d (supported: 64, 128)", head_dim);
-  if (block_size != kBlock)
-    return fail(RAG_ERR_UNSUPPORTED, "decode: block_size %d (supported: 16)", block_size);
-  const int32_t num_decode = cu_seqlens_q ? num_decode_seqs : num_seqs;
-  if (num_decode < 0 || num_decode > num_seqs)
-    return fail(RAG_ERR_INVALID_ARG, "decode: num_decode_seqs %d outside [0, %d]",
-                num_decode_seqs, num_seqs);
-  if (num_decode > 0 && num_q_heads / num_kv_heads > kMaxGroupDecode)
-    return fail(RAG_ERR_UNSUPPORTED, "decode: %d q heads per kv head (max %d)",
-                num_q_heads / num_kv_heads, kMaxGroupDecode);
-  if (num_seqs == 0) return ok();
-  if (max_blocks_per_seq == 0) return fail(RAG_ERR_INVALID_ARG, "decode: max_blocks_per_seq is 0");
+  return decode_paged_impl(q, k_cache, v_cache, o, block_tables, kv_lens, cu_seqlens_q, num_seqs,
+                           num_decode_seqs, max_blocks_per_seq, max_seqlen_q, num_blocks,
+                           num_q_heads, num_kv_heads, head_dim, block_size, softmax_scale,
+                           num_splits, workspace, workspace_bytes, false, stream);
+}
 
-  const int32_t splits =
-      num_decode > 0 ? resolve_splits(num_decode, num_kv_heads, max_blocks_per_seq, num_splits)
-                     : 1;
-  const WsLayout ws = workspace_layout(num_decode, num_q_heads, num_kv_heads, head_dim, splits);
-  const size_t need = ws.bytes;
-  if (need > 0 && (workspace == nullptr || workspace_bytes < need))
-    return fail(RAG_ERR_WORKSPACE, "decode: workspace of %zu bytes needed, %zu given", need,
-                workspace == nullptr ? (size_t)0 : workspace_bytes);
-  if (need > 0 && (reinterpret_cast<uintptr_t>(workspace) & 255u) != 0)
-    return fail(RAG_ERR_INVALID_ARG, "decode: workspace must be 256-byte aligned");
-  const int32_t group = num_q_heads / num_kv_heads;
-  const bool mixed = cu_seqlens_q != nullptr && num_seqs > num_decode;
-  const int64_t grid =
-      (mixed ? rag::paged_prefill_grid(num_seqs - num_decode, num_kv_heads, group, max_seqlen_q)
-             : 0) +
-      rag::paged_decode_grid(num_decode, num_kv_heads, splits) + 8;   // + group padding
-  if (grid > INT_MAX) return fail(RAG_ERR_UNSUPPORTED, "decode: batch too large for one grid");
-
-  if (check_mode()) {
-    std::vector<int32_t> kl, bt, cq;
-    if (!fetch(kl, kv_lens, num_seqs, stream) ||
-        !fetch(bt, block_tables, (size_t)num_seqs * max_blocks_per_seq, stream) ||
-        (cu_seqlens_q && !fetch(cq, cu_seqlens_q, num_seqs + 1, stream)))
-      return fail(RAG_ERR_HIP, "decode: debug copy of device arrays failed");
-    if (cu_seqlens_q) {
-      rag_status st = check_cu(cq, "cu_seqlens_q", std::max(max_seqlen_q, 1));
-      if (st != RAG_OK) return st;
-    }
-    for (int32_t s = 0; s < num_seqs; ++s) {
-      const int32_t n = kl[s];
-      const int32_t nq = cu_seqlens_q ? cq[s + 1] - cq[s] : 1;
-      if (n < 1 || (int64_t)n > (int64_t)max_blocks_per_seq * kBlock)
-        return fail(RAG_ERR_INVALID_ARG, "decode: kv_lens[%d] = %d outside [1, %d]", s, n,
-                    max_blocks_per_seq * kBlock);
-      if (s < num_decode && nq != 1)
-        return fail(RAG_ERR_INVALID_ARG, "decode: decode sequence %d has %d query rows", s, nq);
-      if (nq > n)
-        return fail(RAG_ERR_INVALID_ARG, "decode: sequence %d has %d query rows > %d keys", s,
-                    nq, n);
-      for (int32_t b = 0; b < (n + kBlock - 1) / kBlock; ++b) {
-        const int32_t id = bt[(size_t)s * max_blocks_per_seq + b];
-        if (id < 0 || id >= num_blocks)
-          return fail(RAG_ERR_INVALID_ARG, "decode: block_tables[%d][%d] = %d outside [0, %d)",
-                      s, b, id, num_blocks);
-      }
-    }
-  }
-
-  rag::PagedArgs a;
-  a.q = q;
-  a.k_cache = k_cache;
-  a.v_cache = v_cache;
-  a.o = o;
-  a.block_tables = block_tables;
-  a.kv_lens = kv_lens;
-  a.cu_q = cu_seqlens_q;
-  a.num_seqs = num_seqs;
-  a.num_decode = num_decode;
-  a.max_blocks = max_blocks_per_seq;
-  a.max_seqlen_q = max_seqlen_q;
-  a.hq = num_q_heads;
-  a.hkv = num_kv_heads;
-  a.d = head_dim;
-  a.num_splits = splits;
-  a.scale = softmax_scale;
-  char* wsb = static_cast<char*>(workspace);
-  a.arrivals = need > 0 ? reinterpret_cast<int*>(wsb) : nullptr;
-  a.part_o = need > 0 ? reinterpret_cast<float*>(wsb + ws.o_off) : nullptr;
-  a.part_lse = need > 0 ? reinterpret_cast<float*>(wsb + ws.lse_off) : nullptr;
-  const hipError_t e = rag::launch_paged(a, stream);
-  if (e != hipSuccess) return fail(RAG_ERR_HIP, "decode launch: %s", hipGetErrorString(e));
-  return ok();
+rag_status rag_attn_decode_paged_noalloc(const void* q, const void* k_cache, const void* v_cache,
+                                         void* o, const int32_t* block_tables,
+                                         const int32_t* kv_lens, const int32_t* cu_seqlens_q,
+                                         int32_t num_seqs, int32_t num_decode_seqs,
+                                         int32_t max_blocks_per_seq, int32_t max_seqlen_q,
+                                         int32_t num_blocks, int32_t num_q_heads,
+                                         int32_t num_kv_heads, int32_t head_dim,
+                                         int32_t block_size, float softmax_scale,
+                                         int32_t num_splits, hipStream_t stream) {
+  return decode_paged_impl(q, k_cache, v_cache, o, block_tables, kv_lens, cu_seqlens_q, num_seqs,
+                           num_decode_seqs, max_blocks_per_seq, max_seqlen_q, num_blocks,
+                           num_q_heads, num_kv_heads, head_dim, block_size, softmax_scale,
+                           num_splits, nullptr, 0, true, stream);
 }
 
 rag_status rag_kv_cache_write(const void* k, const void* v, void* k_cache, void* v_cache,

@@ -7,6 +7,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include "rag_attn.h"
+
 namespace rag {
 
 struct PrefillArgs {
@@ -56,5 +58,13 @@ hipError_t launch_prefill_varlen(const PrefillArgs& a, hipStream_t stream);
 hipError_t launch_paged(const PagedArgs& a, hipStream_t stream);
 int64_t kv_cache_write_grid(int64_t num_tokens, int hkv, int d);
 hipError_t launch_kv_cache_write(const KvWriteArgs& a, hipStream_t stream);
+
+// Static per-device scratch of rag_attn_decode_paged_noalloc
+// (decode_scratch.hip): sets it up on the current device at the first call,
+// checks the sizes against its fixed capacity and returns the device
+// addresses of its zeroed counter region and of its partial-result region.
+rag_status decode_scratch(size_t counters, size_t partial_bytes, hipStream_t stream,
+                          int** counters_out, char** partials_out);
+size_t decode_scratch_capacity();
 
 }  // namespace rag

@@ -106,6 +106,36 @@ def test_decode_validation(kw, status):
     assert _decode(**kw) == status
 
 
+def _decode_noalloc(**kw):
+    a = dict(q=FAKE, kc=FAKE, vc=FAKE, o=FAKE, bt=FAKE, kl=FAKE, cu=None, num_seqs=4,
+             num_decode=4, max_blocks=64, max_q=1, num_blocks=300, hq=32, hkv=8, d=128, bs=16,
+             scale=0.088, splits=0)
+    a.update(kw)
+    return binding.lib().rag_attn_decode_paged_noalloc(
+        a["q"], a["kc"], a["vc"], a["o"], a["bt"], a["kl"], a["cu"], a["num_seqs"],
+        a["num_decode"], a["max_blocks"], a["max_q"], a["num_blocks"], a["hq"], a["hkv"],
+        a["d"], a["bs"], a["scale"], a["splits"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(kc=None), binding.RAG_ERR_INVALID_ARG),
+    (dict(num_seqs=-2), binding.RAG_ERR_INVALID_ARG),
+    (dict(hq=12, hkv=8), binding.RAG_ERR_INVALID_ARG),
+    (dict(d=80), binding.RAG_ERR_UNSUPPORTED),
+    (dict(num_seqs=0), binding.RAG_OK),
+    # beyond the static scratch: 4096 rows x 32 heads x 64 splits x 129 x 4 B of partials
+    (dict(num_seqs=4096, num_decode=4096, splits=64), binding.RAG_ERR_WORKSPACE),
+    # 16384 rows x 8 kv heads = 131072 arrival counters (> 65536)
+    (dict(num_seqs=16384, num_decode=16384, max_blocks=4, splits=2), binding.RAG_ERR_WORKSPACE),
+])
+def test_decode_noalloc_validation(kw, status):
+    """Rejected before any HIP call: the size checks come before the scratch
+    set-up, so none of these needs a GPU."""
+    assert _decode_noalloc(**kw) == status
+    if status == binding.RAG_ERR_WORKSPACE:
+        assert "no-alloc" in binding.rag_last_error()
+
+
 def _kv_write(**kw):
     a = dict(k=FAKE, v=FAKE, kc=FAKE, vc=FAKE, slots=FAKE, T=16, hkv=8, d=128, bs=16,
              num_blocks=100)
