@@ -12,9 +12,13 @@ in HBM before the timed region.  Two KV pools alternate between decode steps
 so that a step does not find the previous step's pages in the 256 MB
 Infinity Cache.
 
-Printed: one JSON line with the prefill TFLOP/s (value), the decode KV GB/s,
-roofline objects, extra phases (map_reduce mappers, 70B long stuff, mixed
-decode + chunked prefill) and the oracle's CPU baseline on a bounded sample.
+Printed: one JSON line with the prefill TFLOP/s (value; median over the timed
+steps), the decode KV GB/s, roofline objects, extra phases (map_reduce mappers,
+70B long stuff, mixed decode + chunked prefill, KV-cache write, int4 GEMMs,
+query streams), the clocks (idle, and under a prefill load, with the MFMA
+fractions at that shader clock) and the oracle's CPU baseline: for every
+workload a bounded sample (measured seconds) and the full work's time
+extrapolated from it.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-extra] [--no-cpu-baseline]
 """
@@ -35,6 +39,7 @@ METRIC = "prefill attn TFLOP/s (% MFMA peak); decode attn KV GB/s (% HBM peak)"
 PEAK_BF16_TFLOPS = 2516.6     # 256 CU x 4096 FLOP/clk x 2.4 GHz, dense
 PEAK_HBM_GBS = 8000.0
 WARMUP_REPS = 5               # untimed repetitions before each extra phase
+CPU_BUDGET_S = 2.0            # oracle seconds per sampled part of each workload
 PROFILES = os.path.join(ROOT, "profiles")
 
 
@@ -113,11 +118,21 @@ def read_clocks():
     """Current and maximum shader clock and memory clock of GPU 0 from
     `amd-smi metric --clock --json` (a child process; read-only).  None-valued
     or an error note when the tool or a field is missing."""
+    import signal
     import subprocess
     try:
-        r = subprocess.run(["amd-smi", "metric", "--clock", "--json"], capture_output=True,
-                           text=True, timeout=30)
-        d = json.loads(r.stdout[r.stdout.index("{"):] if "{" in r.stdout else "{}")
+        # own session: whatever the tool leaves behind is ended with its group
+        p = subprocess.Popen(["amd-smi", "metric", "--clock", "--json"], stdout=subprocess.PIPE,
+                             stderr=subprocess.DEVNULL, text=True, start_new_session=True)
+        try:
+            out, _ = p.communicate(timeout=30)
+        finally:
+            try:
+                os.killpg(p.pid, signal.SIGKILL)
+            except ProcessLookupError:
+                pass
+            p.wait()
+        d = json.loads(out[out.index("{"):] if "{" in out else "{}")
         gpus = d.get("gpu_data", d) if isinstance(d, dict) else d
         c = gpus[0]["clock"]
 
@@ -155,6 +170,19 @@ class ClockSampler:
         return self.result
 
 
+def clock_under_load(torch, st, seconds=2.5):
+    """Clocks read (from a thread) while the GPU runs the step's prefill back
+    to back for `seconds`: the shader clock the MFMA-bound work runs at."""
+    sampler = ClockSampler(delay=0.6 * seconds)
+    sampler.start()
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < seconds:
+        for _ in range(10):
+            run_stuff_step(st, None, plan=False, decode=False)
+        torch.cuda.synchronize()
+    return sampler.join()
+
+
 # ---------------------------------------------------------------------------
 # workload set-up
 # ---------------------------------------------------------------------------
@@ -189,7 +217,7 @@ def setup_stuff(torch, w, dev, n_pools=2):
     return st
 
 
-def run_stuff_step(st, timer=None, plan=True):
+def run_stuff_step(st, timer=None, plan=True, decode=True):
     from paper_2412_10543_amd import binding
     w = st["w"]
     if plan:
@@ -207,6 +235,8 @@ def run_stuff_step(st, timer=None, plan=True):
     # (about 2.5 us of 81).  The average launch duration is the pair's time
     # over the number of launches (inter-launch gaps included).
     pools = st.get("pools", [])
+    if not decode:
+        return
     if timer and st["decode_steps"]:
         timer.start("decode")
     for t in range(st["decode_steps"]):
@@ -244,7 +274,9 @@ def median(x):
 # ---------------------------------------------------------------------------
 # extra phases (other workloads; measured, not part of the step)
 # ---------------------------------------------------------------------------
-def bench_phase_stuff(torch, w, dev, reps):
+def bench_phase_stuff(torch, w, dev, reps, cpu=None):
+    """`cpu` (seconds) also samples the oracle on this workload (returned under
+    "_cpu", moved to cpu_baseline by the caller)."""
     st = setup_stuff(torch, w, dev)
     fl, pb, db = stuff_work(st)
     for _ in range(WARMUP_REPS):
@@ -267,6 +299,11 @@ def bench_phase_stuff(torch, w, dev, reps):
         out.update({"decode_steps": per, "decode_us_per_step": round(tot / per * 1e3, 2),
                     "decode_gbs": round(gbs, 1), "decode_frac_hbm": round(gbs / PEAK_HBM_GBS, 4),
                     "decode_splits": st["splits"]})
+    if cpu:
+        if w.name == "mapred7b":
+            out["_cpu"] = cpu_baseline_mapred(torch, st, cpu, seed=w.seed)
+        else:
+            out["_cpu"] = cpu_baseline_stuff(torch, st, cpu, seed=w.seed)
     del st
     torch.cuda.empty_cache()
     return out
@@ -306,7 +343,7 @@ def run_mixed(st, pool_index=0):
                                   workspace=st["ws"])
 
 
-def bench_phase_mixed(torch, dev, reps):
+def bench_phase_mixed(torch, dev, reps, cpu=None):
     st = setup_mixed(torch, dev)
     w = st["w"]
     for i in range(max(WARMUP_REPS, len(st["pools"]))):   # includes first touch of each pool
@@ -333,6 +370,8 @@ def bench_phase_mixed(torch, dev, reps):
            "roofline_ms_serial": round(t_hbm + t_mfma, 4),
            "frac_of_overlapped_roofline": round(max(t_hbm, t_mfma) / ms, 4),
            "splits": st["splits"]}
+    if cpu:
+        out["_cpu"] = cpu_baseline_mixed(torch, st, cpu, seed=w.seed)
     del st
     torch.cuda.empty_cache()
     return out
@@ -468,61 +507,230 @@ def bench_phase_stream(torch, n=32, rate=100.0, budget_gb=16):
 
 
 # ---------------------------------------------------------------------------
-# CPU baseline: the oracle on a bounded sample of the same workload
+# CPU baseline: the oracle on a bounded sample of each workload
 # ---------------------------------------------------------------------------
-def cpu_baseline(torch, st, budget_s=12.0):
+def _cores():
+    return len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
+
+
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
+def _f64_of(t):
+    """GPU bf16 tensor -> fp64 numpy (exact widening), outside the timed calls."""
+    import oracle
+    from paper_2412_10543_amd.workloads import bf16_bits
+    return oracle.bf16_bits_to_f64(bf16_bits(t))
+
+
+def oracle_prefill_sample(torch, q, k, v, cu_q, cu_k, hq, scale, budget_s, seed):
+    """The oracle on seeded random (row, head) pairs of packed prompts, drawn
+    sequence by sequence (sequences in proportion to their work) until
+    `budget_s` seconds of oracle time; the full launch's time is extrapolated
+    from the sampled pairs' share of the algorithmic FLOPs."""
     import numpy as np
 
     import oracle
-    from paper_2412_10543_amd.workloads import bf16_bits
+    orc = oracle.default()
+    d = q.shape[2]
+    lq = [b - a for a, b in zip(cu_q[:-1], cu_q[1:])]
+    lk = [b - a for a, b in zip(cu_k[:-1], cu_k[1:])]
+    full = prefill_flops(lq, lk, hq, d)
+    per_seq = np.array([prefill_flops([a], [b], hq, d) for a, b in zip(lq, lk)])
+    rng = np.random.Generator(np.random.PCG64(seed))
+    flops, secs, pairs, seqs = 0.0, 0.0, 0, set()
+    while secs < budget_s:
+        s = int(rng.choice(len(lq), p=per_seq / per_seq.sum()))
+        nq, nk = lq[s], lk[s]
+        kk, vv = _f64_of(k[cu_k[s]:cu_k[s + 1]]), _f64_of(v[cu_k[s]:cu_k[s + 1]])
+        for _ in range(4):
+            rows = np.sort(rng.integers(0, nq, size=128)).astype(np.int32)
+            heads = rng.integers(0, hq, size=128).astype(np.int32)
+            qr = _f64_of(q[cu_q[s]:cu_q[s + 1]][torch.as_tensor(rows, device=q.device).long(),
+                                                 torch.as_tensor(heads, device=q.device).long()])
+            t0 = time.perf_counter()
+            orc.seq_rows(qr, kk, vv, nq, rows, heads, hq, scale, True)
+            secs += time.perf_counter() - t0
+            flops += float(sum(4 * d * (nk - nq + int(r) + 1) for r in rows))
+            pairs += len(rows)
+            if secs >= budget_s:
+                break
+        seqs.add(s)
+    return {"sample": f"{pairs} random (row, head) pairs of {len(seqs)} of {len(lq)} prompts",
+            "sample_s": round(secs, 3), "sample_gflop": round(flops / 1e9, 3),
+            "tflops": round(flops / secs / 1e12, 6),
+            "full_tflop": round(full / 1e12, 4),
+            "extrapolated_full_s": round(secs * full / flops, 1)}
+
+
+def oracle_decode_sample(torch, q_rows, pool, kv_lens, seqs, hq, scale, full_bytes, budget_s):
+    """The oracle on one decode row per listed sequence (all heads), pages
+    gathered from the pool, until `budget_s` seconds; the full phase's time is
+    extrapolated from the sampled rows' share of the algorithmic bytes."""
+    import numpy as np
+
+    import oracle
+    orc = oracle.default()
+    hkv, d = pool.k_cache.shape[1], pool.k_cache.shape[3]
+    tables = pool.block_tables.cpu().numpy()
+    nbytes, secs, n = 0.0, 0.0, 0
+    for s in seqs:
+        nb = (kv_lens[s] + 15) // 16
+        blocks = torch.as_tensor(tables[s, :nb], device=pool.k_cache.device).long()
+        kc, vc = _f64_of(pool.k_cache[blocks]), _f64_of(pool.v_cache[blocks])
+        qd = _f64_of(q_rows[s:s + 1])
+        t0 = time.perf_counter()
+        orc.paged(qd, kc, vc, np.arange(nb, dtype=np.int32)[None, :], [kv_lens[s]], scale,
+                  want_lse=False)
+        secs += time.perf_counter() - t0
+        nbytes += decode_bytes([kv_lens[s]], hq, hkv, d)
+        n += 1
+        if secs >= budget_s:
+            break
+    return {"sample": f"one decode row (all {hq} heads) of {n} sequences",
+            "sample_s": round(secs, 3), "sample_gb": round(nbytes / 1e9, 4),
+            "gbs": round(nbytes / secs / 1e9, 4), "full_gb": round(full_bytes / 1e9, 3),
+            "extrapolated_full_s": round(secs * full_bytes / nbytes, 1)}
+
+
+def cpu_baseline_tiny(torch, dev):
+    """The tiny stuff query in full: prefill of its 288 tokens and its 16
+    decode steps (measured, nothing extrapolated)."""
+    import oracle
+    from paper_2412_10543_amd import binding
+    from paper_2412_10543_amd.workloads import normal_bf16, paged_pool, tiny
+    w = tiny()
+    cu, dec = binding.rag_plan_prompts(w.method, w.query_lens, w.num_chunks, w.chunk_len,
+                                       w.intermediate_length, w.answer_len)
+    T = cu[-1]
+    q = _f64_of(normal_bf16((T, w.hq, w.d), w.seed, dev))
+    k = _f64_of(normal_bf16((T, w.hkv, w.d), w.seed + 1, dev))
+    v = _f64_of(normal_bf16((T, w.hkv, w.d), w.seed + 2, dev))
+    orc = oracle.default()
+    t0 = time.perf_counter()
+    orc.varlen(q, k, v, cu, cu, w.scale, True)
+    pf_s = time.perf_counter() - t0
+    steps = dec[0]
+    pool = paged_pool([T + steps], w.hkv, w.d, w.seed + 100, device=dev)
+    kc, vc = _f64_of(pool.k_cache), _f64_of(pool.v_cache)
+    table = pool.block_tables.cpu().numpy()
+    qd = _f64_of(normal_bf16((steps, 1, w.hq, w.d), w.seed + 7, dev))
+    t0 = time.perf_counter()
+    for t in range(steps):
+        orc.paged(qd[t], kc, vc, table, [T + t + 1], w.scale, want_lse=False)
+    dec_s = time.perf_counter() - t0
+    fl = prefill_flops([T], [T], w.hq, w.d)
+    db = sum(decode_bytes([T + t + 1], w.hq, w.hkv, w.d) for t in range(steps))
+    return {"prefill": {"sample": "full", "sample_s": round(pf_s, 4),
+                        "tflops": round(fl / pf_s / 1e12, 6)},
+            "decode": {"sample": f"all {steps} steps", "sample_s": round(dec_s, 4),
+                       "gbs": round(db / dec_s / 1e9, 4)}}
+
+
+def cpu_baseline_stuff(torch, st, budget_s, seed):
+    """Sampled prefill rows and decode rows of a stuff-shaped workload (the
+    step's stuff7b or the long70b phase)."""
+    w = st["w"]
+    out = {"prefill": oracle_prefill_sample(torch, st["q"], st["k"], st["v"], st["cu"], st["cu"],
+                                            w.hq, w.scale, budget_s, seed)}
+    if st["decode_steps"]:
+        lens = st["lens"]
+        full = sum(decode_bytes([n + t + 1 for n in lens], w.hq, w.hkv, w.d)
+                   for t in range(st["decode_steps"]))
+        order = sorted(range(len(lens)), key=lambda s: -lens[s])
+        out["decode"] = oracle_decode_sample(torch, st["dq"][0], st["pools"][0],
+                                             [n + 1 for n in lens], order, w.hq, w.scale,
+                                             full, budget_s)
+        out["decode"]["sample"] += " (step 0, longest first)"
+    return out
+
+
+def cpu_baseline_mapred(torch, st, budget_s, seed):
+    """Whole mapper prompts (every row and head) of the map_reduce map phase,
+    one after another until the budget, and sampled decode rows."""
+    import numpy as np
+
+    import oracle
     w = st["w"]
     orc = oracle.default()
     lens, cu = st["lens"], st["cu"]
-    s = int(np.argmax(lens))           # the longest prompt
-    L = lens[s]
-    k = bf16_bits(st["k"][cu[s]:cu[s + 1]])
-    v = bf16_bits(st["v"][cu[s]:cu[s + 1]])
-    qs = st["q"][cu[s]:cu[s + 1]]
-    rng = np.random.Generator(np.random.PCG64(0))
-    flops, secs, nrows = 0.0, 0.0, 0
-    while secs < budget_s * 0.5 and nrows < L * w.hq:
-        rows = np.sort(rng.integers(0, L, size=64)).astype(np.int32)
-        heads = rng.integers(0, w.hq, size=64).astype(np.int32)
-        qr = bf16_bits(qs[torch.as_tensor(rows, device=qs.device).long(),
-                          torch.as_tensor(heads, device=qs.device).long()])
+    rng = np.random.Generator(np.random.PCG64(seed))
+    flops, secs, n = 0.0, 0.0, 0
+    for s in rng.permutation(len(lens)):
+        s = int(s)
+        sl = slice(cu[s], cu[s + 1])
+        qq, kk, vv = _f64_of(st["q"][sl]), _f64_of(st["k"][sl]), _f64_of(st["v"][sl])
         t0 = time.perf_counter()
-        orc.seq_rows(qr, k, v, L, rows, heads, w.hq, w.scale, True)
+        orc.varlen(qq, kk, vv, [0, lens[s]], [0, lens[s]], w.scale, True, want_lse=False)
         secs += time.perf_counter() - t0
-        flops += float(sum(4 * w.d * (r + 1) for r in rows))
-        nrows += len(rows)
-    out = {"value": round(flops / secs / 1e12, 6), "unit": "TFLOP/s",
-           "cores": len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else
-           os.cpu_count(), "kind": "oracle",
-           "sample": f"prefill: {nrows} (row, head) pairs of the longest stuff prompt "
-                     f"(L={L}), {secs:.1f}s"}
-    # decode: one step for as many sequences as fit in the budget
-    pool = st["pools"][0]
-    steps_kv = [n + 1 for n in lens]
-    tables = pool.block_tables.cpu().numpy()
-    dbytes, dsecs, nseq = 0.0, 0.0, 0
-    for si in np.argsort(lens)[::-1]:
-        if dsecs >= budget_s * 0.5:
+        flops += prefill_flops([lens[s]], [lens[s]], w.hq, w.d)
+        n += 1
+        if secs >= budget_s:
             break
-        nb = (steps_kv[si] + 15) // 16
-        blocks = torch.as_tensor(tables[si, :nb], device=pool.k_cache.device).long()
-        kc = bf16_bits(pool.k_cache[blocks])
-        vc = bf16_bits(pool.v_cache[blocks])
-        qd = bf16_bits(st["dq"][0][si:si + 1])
-        table = np.arange(nb, dtype=np.int32)[None, :]
-        t0 = time.perf_counter()
-        orc.paged(qd, kc, vc, table, [steps_kv[si]], w.scale, want_lse=False)
-        dsecs += time.perf_counter() - t0
-        dbytes += decode_bytes([steps_kv[si]], w.hq, w.hkv, w.d)
-        nseq += 1
-    out["decode"] = {"value": round(dbytes / dsecs / 1e9, 4), "unit": "GB/s",
-                     "sample": f"decode step 0 of {nseq} sequences, {dsecs:.1f}s"}
-    out["omp_threads"] = os.environ.get("OMP_NUM_THREADS", "default")
+    full = prefill_flops(lens, lens, w.hq, w.d)
+    out = {"prefill": {"sample": f"{n} whole mapper prompts of {len(lens)} (every row and head)",
+                       "sample_s": round(secs, 3), "sample_gflop": round(flops / 1e9, 3),
+                       "tflops": round(flops / secs / 1e12, 6), "full_tflop": round(full / 1e12, 4),
+                       "extrapolated_full_s": round(secs * full / flops, 1)}}
+    fullb = sum(decode_bytes([x + t + 1 for x in lens], w.hq, w.hkv, w.d)
+                for t in range(st["decode_steps"]))
+    out["decode"] = oracle_decode_sample(torch, st["dq"][0], st["pools"][0],
+                                         [x + 1 for x in lens],
+                                         [int(x) for x in rng.permutation(len(lens))], w.hq,
+                                         w.scale, fullb, budget_s)
+    out["decode"]["sample"] += " (step 0)"
     return out
+
+
+def cpu_baseline_mixed(torch, st, budget_s, seed):
+    """Sampled decode rows and chunked-prefill rows of the mixed batch."""
+    import numpy as np
+    w = st["w"]
+    nd = st["nd"]
+    pool = st["pools"][0]
+    out = {}
+    full = decode_bytes(w.decode_kv_lens, w.hq, w.hkv, w.d)
+    rng = np.random.Generator(np.random.PCG64(seed))
+    out["decode"] = oracle_decode_sample(torch, st["q"], pool, st["kv"],
+                                         [int(s) for s in rng.permutation(nd)], w.hq, w.scale,
+                                         full, budget_s)
+    # pieces: rows of each piece against its paged keys (gathered densely)
+    cu = st["cu"]
+    qs, ks, vs, cq, ck = [], [], [], [0], [0]
+    tables = pool.block_tables.cpu().numpy()
+    for s in range(nd, len(st["kv"])):
+        n = st["kv"][s]
+        nb = (n + 15) // 16
+        blocks = torch.as_tensor(tables[s, :nb], device=pool.k_cache.device).long()
+        ks.append(pool.k_cache[blocks].permute(0, 2, 1, 3).reshape(nb * 16, w.hkv, w.d)[:n])
+        vs.append(pool.v_cache[blocks].permute(0, 2, 1, 3).reshape(nb * 16, w.hkv, w.d)[:n])
+        qs.append(st["q"][cu[s]:cu[s + 1]])
+        cq.append(cq[-1] + cu[s + 1] - cu[s])
+        ck.append(ck[-1] + n)
+    out["pieces"] = oracle_prefill_sample(torch, torch.cat(qs), torch.cat(ks), torch.cat(vs),
+                                          cq, ck, w.hq, w.scale, budget_s, seed + 1)
+    return out
+
+
+def cpu_baseline_summary(per_config):
+    """The headline figure (stuff7b prefill, the bench's `value` metric) with
+    the per-workload samples beside it."""
+    pf = per_config["stuff7b"]["prefill"]
+    return {"value": pf["tflops"], "unit": "TFLOP/s", "cores": _cores(), "kind": "oracle",
+            "sample": f"stuff7b prefill: {pf['sample']}, {pf['sample_s']} s of oracle time "
+                      f"(full launch extrapolated: {pf['extrapolated_full_s']} s)",
+            "cpu_model": _cpu_model(), "omp_threads": os.environ.get("OMP_NUM_THREADS", "default"),
+            "note": "oracle = plain fp64 C (OpenMP over sequence x head); sample_s measured, "
+                    "extrapolated_full_s = sample_s x (full work / sampled work)",
+            "per_config": per_config}
 
 
 # ---------------------------------------------------------------------------
@@ -631,11 +839,12 @@ def main():
 
     pf_ms = timer.ms("prefill")
     dec_ms = timer.ms("decode")
-    pf_avg = sum(pf_ms) / len(pf_ms)
-    dec_total = sum(dec_ms) / args.steps                   # ms of decode per step
+    pf_med = median(pf_ms)                                 # headline: median over steps
+    pf_mean = sum(pf_ms) / len(pf_ms)
+    dec_total = median(dec_ms)                             # ms of decode per step (median)
     nsteps = st["decode_steps"]
     dec_avg = dec_total / nsteps                           # ms per decode launch
-    tflops = fl / pf_avg / 1e9
+    tflops = fl / pf_med / 1e9
     dec_gbs = sum(db) / dec_total / 1e6
     dec_bytes_avg = sum(db) / nsteps
 
@@ -645,7 +854,7 @@ def main():
     rl_dec = roofline("hbm", dec_gbs, PEAK_HBM_GBS, "GB/s",
                       traffic=stored_traffic("paged_kernel"),
                       kernel="paged_decode_kernel<128> (rag_attn_decode_paged)")
-    dominant = rl_dec if dec_total > pf_avg else rl_pf
+    dominant = rl_dec if dec_total > pf_med else rl_pf
 
     res = {
         "metric": METRIC, "value": round(tflops, 2), "unit": "TFLOP/s",
@@ -657,36 +866,55 @@ def main():
                    "num_chunks": w.num_chunks, "tokens": st["cu"][-1], "hq": w.hq,
                    "hkv": w.hkv, "d": w.d, "decode_steps": nsteps, "block_size": 16,
                    "decode_splits": st["splits"]},
-        "prefill": {"ms": round(pf_avg, 4), "tflops": round(tflops, 2),
+        "prefill": {"ms": round(pf_med, 4), "ms_mean": round(pf_mean, 4),
+                    "ms_min": round(min(pf_ms), 4), "ms_max": round(max(pf_ms), 4),
+                    "tflops": round(tflops, 2),
                     "frac_mfma": round(tflops / PEAK_BF16_TFLOPS, 4),
                     "algorithmic_flops": fl, "algorithmic_bytes": pb},
         "decode": {"value": round(dec_gbs, 1), "unit": "GB/s",
                    "frac_hbm": round(dec_gbs / PEAK_HBM_GBS, 4),
                    "us_per_step": round(dec_avg * 1e3, 3),
+                   "us_per_step_mean": round(sum(dec_ms) / len(dec_ms) / nsteps * 1e3, 3),
                    "algorithmic_bytes_per_launch": round(dec_bytes_avg)},
+        "timing": "median over the timed steps: prefill = one event pair per launch; decode = "
+                  "one event pair around a step's launches, divided by their number",
         "roofline": dominant,
         "rooflines": {"prefill": rl_pf, "decode": rl_dec},
     }
-    sampler = None
+    if want_clocks:
+        clocks["under_load"] = clock_under_load(torch, st)
     if not args.no_extra:
-        if want_clocks:
-            sampler = ClockSampler(delay=2.0)   # lands in the mapred7b / long70b phases
-            sampler.start()
         phases = {}
+        cpu = None if args.no_cpu_baseline else CPU_BUDGET_S
         for fn in (mapred7b, long70b):
-            phases[fn.__name__] = bench_phase_stuff(torch, fn(), dev, args.extra_reps)
-        phases["mixed"] = bench_phase_mixed(torch, dev, args.extra_reps)
+            phases[fn.__name__] = bench_phase_stuff(torch, fn(), dev, args.extra_reps, cpu=cpu)
+        phases["mixed"] = bench_phase_mixed(torch, dev, args.extra_reps, cpu=cpu)
         phases["kv_write"] = bench_phase_kv_write(torch, dev, max(args.extra_reps, 10))
         phases["awq_gemm_7b"] = bench_phase_awq(torch, dev, max(args.extra_reps, 10))
         phases["query_stream"] = bench_phase_stream(torch)
         phases["query_stream_tight"] = bench_phase_stream(torch, n=32, rate=2000.0, budget_gb=1)
         res["phases"] = phases
     if not args.no_cpu_baseline:
-        res["cpu_baseline"] = cpu_baseline(torch, st)
+        per = {"tiny": cpu_baseline_tiny(torch, dev),
+               "stuff7b": cpu_baseline_stuff(torch, st, CPU_BUDGET_S, seed=w.seed)}
+        for name, ph in res.get("phases", {}).items():
+            if isinstance(ph, dict) and "_cpu" in ph:
+                per[name] = ph.pop("_cpu")
+        res["cpu_baseline"] = cpu_baseline_summary(per)
     if want_clocks:
-        clocks["under_load"] = sampler.join() if sampler else None
         clocks["idle_after"] = read_clocks()
         res["clocks"] = clocks
+        sclk = (clocks.get("under_load") or {}).get("sclk_mhz")
+        if isinstance(sclk, (int, float)) and sclk > 0:
+            # the same work against the MFMA peak at the shader clock read under load
+            peak = PEAK_BF16_TFLOPS * sclk / 2400.0
+            res["at_measured_sclk"] = {
+                "sclk_mhz": sclk, "bf16_peak_tflops": round(peak, 1),
+                "prefill_frac_mfma": round(tflops / peak, 4),
+                "phases_prefill_frac_mfma": {
+                    k: round(v["prefill_tflops"] / peak, 4)
+                    for k, v in res.get("phases", {}).items()
+                    if isinstance(v, dict) and "prefill_tflops" in v}}
     print(json.dumps(res))
 
 
