@@ -418,6 +418,129 @@ def bench_phase_kv_write(torch, dev, reps):
     return out
 
 
+def bench_phase_fused_kv(torch, dev, reps):
+    """The KV-cache writes on either side of the hot path, separate and fused:
+    prompt prefill then rag_kv_cache_write vs rag_attn_prefill_varlen_kvcache
+    (stuff7b and the map_reduce mappers; each sequence's tokens in consecutive
+    slots of randomly permuted pages), and a stuff7b decode step as
+    rag_kv_cache_write + rag_attn_decode_paged vs rag_attn_decode_paged_append."""
+    import numpy as np
+
+    from paper_2412_10543_amd import binding, workloads
+    from paper_2412_10543_amd.workloads import normal_bf16, paged_pool
+    out = {}
+
+    def timed(fn, name):
+        for _ in range(WARMUP_REPS):
+            fn()
+        torch.cuda.synchronize()
+        timer = Timer(torch)
+        for _ in range(reps):
+            timer.start(name)
+            fn()
+            timer.stop(name)
+        torch.cuda.synchronize()
+        return median(timer.ms(name))
+
+    for wname in ("mapred7b", "stuff7b"):
+        w = getattr(workloads, wname)()
+        cu, dec = binding.rag_plan_prompts(w.method, w.query_lens, w.num_chunks, w.chunk_len,
+                                           w.intermediate_length, w.answer_len)
+        lens = [b - a for a, b in zip(cu[:-1], cu[1:])]
+        T, L = cu[-1], max(lens)
+        q = normal_bf16((T, w.hq, w.d), w.seed, dev)
+        k = normal_bf16((T, w.hkv, w.d), w.seed + 1, dev)
+        v = normal_bf16((T, w.hkv, w.d), w.seed + 2, dev)
+        o = torch.empty_like(q)
+        cu_t = torch.tensor(cu, dtype=torch.int32, device=dev)
+        nblk = [(n + 15) // 16 for n in lens]
+        num_blocks = int(sum(nblk) * 1.25) + 1
+        perm = np.random.Generator(np.random.PCG64(23)).permutation(num_blocks)
+        slots, pos = [], 0
+        for n, nb in zip(lens, nblk):
+            pages = perm[pos:pos + nb]
+            pos += nb
+            j = np.arange(n)
+            slots.append(pages[j // 16] * 16 + j % 16)
+        slots_t = torch.tensor(np.concatenate(slots).astype(np.int32), device=dev)
+        kc = torch.empty((num_blocks, w.hkv, 16, w.d), dtype=torch.bfloat16, device=dev)
+        vc = torch.empty_like(kc)
+
+        def prefill():
+            binding.rag_attn_prefill_varlen(q, k, v, o, None, cu_t, cu_t, L, L, w.scale, True)
+
+        def separate():
+            prefill()
+            binding.rag_kv_cache_write(k, v, kc, vc, slots_t)
+
+        def fused():
+            binding.rag_attn_prefill_varlen_kvcache(q, k, v, o, None, cu_t, L, w.scale, kc, vc,
+                                                    slots_t)
+        ms = {n: timed(f, n) for n, f in (("prefill", prefill), ("separate", separate),
+                                          ("fused", fused))}
+        out[f"{wname}_prefill"] = {
+            "tokens": T, "prefill_only_ms": round(ms["prefill"], 4),
+            "prefill_then_write_ms": round(ms["separate"], 4),
+            "fused_ms": round(ms["fused"], 4),
+            "write_cost_fused_ms": round(ms["fused"] - ms["prefill"], 4),
+            "write_cost_separate_ms": round(ms["separate"] - ms["prefill"], 4)}
+        del q, k, v, o, kc, vc
+        torch.cuda.empty_cache()
+
+    # decode step 0 of stuff7b with its new token appended
+    w = workloads.stuff7b()
+    cu, _ = binding.rag_plan_prompts(w.method, w.query_lens, w.num_chunks, w.chunk_len,
+                                     w.intermediate_length, w.answer_len)
+    lens = [b - a for a, b in zip(cu[:-1], cu[1:])]
+    S = len(lens)
+    kvl = [n + 1 for n in lens]
+    pools = [paged_pool(kvl, w.hkv, w.d, w.seed + 300 + i, device=dev, poison=False)
+             for i in range(2)]
+    kvl_t = torch.tensor(kvl, dtype=torch.int32, device=dev)
+    qd = normal_bf16((S, w.hq, w.d), 61, dev)
+    kn = normal_bf16((S, w.hkv, w.d), 62, dev)
+    vn = normal_bf16((S, w.hkv, w.d), 63, dev)
+    od = torch.empty_like(qd)
+    mb = pools[0].block_tables.shape[1]
+    nws = binding.rag_attn_decode_workspace_size(S, w.hq, w.hkv, w.d, mb)
+    ws = torch.zeros(max(nws, 256), dtype=torch.uint8, device=dev)
+    new_slots = []
+    for pool in pools:
+        tb = pool.block_tables.cpu().numpy()
+        new_slots.append(torch.tensor([int(tb[s, (n - 1) // 16]) * 16 + (n - 1) % 16
+                                       for s, n in enumerate(kvl)], dtype=torch.int32,
+                                      device=dev))
+    it = [0]
+
+    def separate_step():
+        i = it[0] = it[0] ^ 1
+        p = pools[i]
+        binding.rag_kv_cache_write(kn, vn, p.k_cache, p.v_cache, new_slots[i])
+        binding.rag_attn_decode_paged(qd, p.k_cache, p.v_cache, od, p.block_tables, kvl_t,
+                                      w.scale, workspace=ws)
+
+    def append_step():
+        i = it[0] = it[0] ^ 1
+        p = pools[i]
+        binding.rag_attn_decode_paged_append(qd, kn, vn, p.k_cache, p.v_cache, od,
+                                             p.block_tables, kvl_t, w.scale, workspace=ws)
+
+    def loop(fn):
+        def run():
+            for _ in range(16):
+                fn()
+        return run
+    sep = timed(loop(separate_step), "dsep") / 16
+    app = timed(loop(append_step), "dapp") / 16
+    out["stuff7b_decode_step"] = {"write_then_decode_us": round(sep * 1e3, 2),
+                                  "append_us": round(app * 1e3, 2),
+                                  "note": "16 launches (pairs) back to back between one event "
+                                          "pair, two pools alternating"}
+    del pools
+    torch.cuda.empty_cache()
+    return out
+
+
 def bench_phase_awq(torch, dev, reps, batches=(16, 8192), graph=True):
     """Group-quantized int4-weight GEMMs of the 7B model's linear layers
     (qkv, o, gate_up, down) at a decode batch of 16 rows (HBM-bound: the packed
@@ -890,6 +1013,7 @@ def main():
             phases[fn.__name__] = bench_phase_stuff(torch, fn(), dev, args.extra_reps, cpu=cpu)
         phases["mixed"] = bench_phase_mixed(torch, dev, args.extra_reps, cpu=cpu)
         phases["kv_write"] = bench_phase_kv_write(torch, dev, max(args.extra_reps, 10))
+        phases["fused_kv"] = bench_phase_fused_kv(torch, dev, max(args.extra_reps, 10))
         phases["awq_gemm_7b"] = bench_phase_awq(torch, dev, max(args.extra_reps, 10))
         phases["query_stream"] = bench_phase_stream(torch)
         phases["query_stream_tight"] = bench_phase_stream(torch, n=32, rate=2000.0, budget_gb=1)

@@ -111,6 +111,38 @@ rag_status rag_attn_prefill_varlen(const void *q, const void *k, const void *v,
                                    hipStream_t stream);
 
 /*
+ * The prompt prefill with the paged KV-cache write fused in: the causal
+ * attention of rag_attn_prefill_varlen over self-attention prompts (query rows
+ * are the key rows: one cu_seqlens), which also stores every K and V row in
+ * the paged cache rag_attn_decode_paged reads -- the step on either side of
+ * the hot path in the serving engine the paper builds on (Sec.
+ * "Implementation": a paged KV cache), so that decode starts on the pages with
+ * no separate copy.  Each prefill workgroup writes the key rows of its own
+ * query tiles after computing them, while they are still in the GPU's caches.
+ *
+ *   q, k, v, o, lse  as in rag_attn_prefill_varlen, with cu_seqlens_q =
+ *            cu_seqlens_k = cu_seqlens and causal = 1.
+ *   k_cache, v_cache  device [num_blocks, num_kv_heads, block_size, head_dim]
+ *   slot_mapping  device int32 [cu_seqlens[num_seqs]]: the slot (page * 16 +
+ *            offset) of each packed token; negative = not written.
+ *            Precondition: slots below num_blocks * 16, none repeated (checked
+ *            when RAG_ATTN_CHECK=1).  The result in the cache is that of
+ *            rag_kv_cache_write(k, v, ...) with the same slot mapping.
+ *   block_size  must be 16.
+ *
+ * Returns the statuses of rag_attn_prefill_varlen, and RAG_ERR_INVALID_ARG for
+ * a null or misaligned cache or slot pointer, RAG_ERR_UNSUPPORTED for a block
+ * size other than 16.
+ */
+rag_status rag_attn_prefill_varlen_kvcache(
+    const void *q, const void *k, const void *v, void *o, float *lse,
+    const int32_t *cu_seqlens, int32_t num_seqs, int32_t max_seqlen,
+    int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+    float softmax_scale, void *k_cache, void *v_cache,
+    const int32_t *slot_mapping, int32_t num_blocks, int32_t block_size,
+    hipStream_t stream);
+
+/*
  * Number of KV splits rag_attn_decode_paged uses for its decode rows when it
  * is passed num_splits (0 = choose automatically), given the number of decode
  * rows, kv heads and the block-table width.  Always >= 1.
@@ -184,6 +216,33 @@ rag_status rag_attn_decode_paged(const void *q, const void *k_cache,
                                  float softmax_scale, int32_t num_splits,
                                  void *workspace, size_t workspace_bytes,
                                  hipStream_t stream);
+
+/*
+ * One decode step with the step's new token appended in the same launch: for
+ * each decode row s, key kv_lens[s] - 1 is the new token, whose K and V rows
+ * k_new[s], v_new[s] are stored into its cache slot (block_tables[s][(kv_lens[s]
+ * - 1) / 16] * 16 + (kv_lens[s] - 1) % 16) and attended together with the keys
+ * already in the cache.  Equivalent to rag_kv_cache_write of the new tokens
+ * followed by rag_attn_decode_paged, in one launch (the serving engine's
+ * decode iteration, Sec. "Implementation").
+ *
+ *   q        device [num_seqs, num_q_heads, head_dim]: one decode row per
+ *            sequence (no chunked-prefill pieces)
+ *   k_new, v_new  device [num_seqs, num_kv_heads, head_dim], 16-byte aligned
+ *   the rest as in rag_attn_decode_paged (cu_seqlens_q = NULL).  The caches
+ *            are written (one slot per sequence and kv head).
+ *
+ * Returns the statuses of rag_attn_decode_paged, and RAG_ERR_INVALID_ARG for a
+ * null or misaligned k_new / v_new.
+ */
+rag_status rag_attn_decode_paged_append(
+    const void *q, const void *k_new, const void *v_new, void *k_cache,
+    void *v_cache, void *o, const int32_t *block_tables,
+    const int32_t *kv_lens, int32_t num_seqs, int32_t max_blocks_per_seq,
+    int32_t num_blocks, int32_t num_q_heads, int32_t num_kv_heads,
+    int32_t head_dim, int32_t block_size, float softmax_scale,
+    int32_t num_splits, void *workspace, size_t workspace_bytes,
+    hipStream_t stream);
 
 /*
  * rag_attn_decode_paged without a workspace argument, for callers that cannot

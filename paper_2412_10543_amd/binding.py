@@ -46,6 +46,7 @@ _lib = None
 
 def exported_symbols():
     return ["rag_abi_version", "rag_last_error", "rag_attn_prefill_varlen",
+            "rag_attn_prefill_varlen_kvcache", "rag_attn_decode_paged_append",
             "rag_attn_decode_num_splits", "rag_attn_decode_workspace_size",
             "rag_attn_decode_paged", "rag_attn_decode_paged_noalloc", "rag_kv_cache_write", "rag_plan_prompts",
             "rag_prune_config_space", "rag_config_kv_bytes", "rag_choose_config",
@@ -90,6 +91,14 @@ def lib():
     L.rag_attn_prefill_varlen.restype = ctypes.c_int
     L.rag_attn_prefill_varlen.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _i32, _i32, _i32,
                                           _i32, _i32, _i32, ctypes.c_float, _i32, _vp]
+    L.rag_attn_prefill_varlen_kvcache.restype = ctypes.c_int
+    L.rag_attn_prefill_varlen_kvcache.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _i32, _i32, _i32,
+                                                  _i32, _i32, ctypes.c_float, _vp, _vp, _vp,
+                                                  _i32, _i32, _vp]
+    L.rag_attn_decode_paged_append.restype = ctypes.c_int
+    L.rag_attn_decode_paged_append.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i32, _i32,
+                                               _i32, _i32, _i32, _i32, _i32, ctypes.c_float,
+                                               _i32, _vp, ctypes.c_size_t, _vp]
     L.rag_attn_decode_num_splits.restype = _i32
     L.rag_attn_decode_num_splits.argtypes = [_i32, _i32, _i32, _i32, _i32]
     L.rag_attn_decode_workspace_size.restype = ctypes.c_size_t
@@ -178,6 +187,48 @@ def rag_attn_prefill_varlen(q, k, v, o, lse, cu_seqlens_q, cu_seqlens_k, max_seq
         _ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), _ptr(cu_seqlens_q), _ptr(cu_seqlens_k),
         cu_seqlens_q.numel() - 1, int(max_seqlen_q), int(max_seqlen_k), q.shape[1], k.shape[1],
         q.shape[2], float(softmax_scale), int(bool(causal)), _stream(stream)))
+
+
+def rag_attn_prefill_varlen_kvcache(q, k, v, o, lse, cu_seqlens, max_seqlen, softmax_scale,
+                                    k_cache, v_cache, slot_mapping, stream=None) -> None:
+    """Causal prompt prefill that also writes K/V into the paged cache.
+    q, o [T, Hq, d]; k, v [T, Hkv, d] bf16; cu_seqlens int32 [S+1]; caches
+    [num_blocks, Hkv, 16, d] bf16; slot_mapping int32 [T] (negative = skip)."""
+    for t, n in ((q, "q"), (k, "k"), (v, "v"), (o, "o")):
+        _need(t, torch.bfloat16, n, 3)
+    for t, n in ((k_cache, "k_cache"), (v_cache, "v_cache")):
+        _need(t, torch.bfloat16, n, 4)
+    _need(cu_seqlens, torch.int32, "cu_seqlens", 1)
+    _need(slot_mapping, torch.int32, "slot_mapping", 1)
+    if lse is not None:
+        _need(lse, torch.float32, "lse", 2)
+    _check(lib().rag_attn_prefill_varlen_kvcache(
+        _ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), _ptr(cu_seqlens), cu_seqlens.shape[0] - 1,
+        int(max_seqlen), q.shape[1], k.shape[1], q.shape[2], float(softmax_scale),
+        _ptr(k_cache), _ptr(v_cache), _ptr(slot_mapping), k_cache.shape[0], k_cache.shape[2],
+        _stream(stream)))
+
+
+def rag_attn_decode_paged_append(q, k_new, v_new, k_cache, v_cache, o, block_tables, kv_lens,
+                                 softmax_scale, num_splits=0, workspace=None, stream=None):
+    """One decode step that appends each row's new token (k_new, v_new
+    [S, Hkv, d]) to the cache at key kv_lens[s] - 1 and attends it."""
+    for t, n in ((q, "q"), (o, "o"), (k_new, "k_new"), (v_new, "v_new")):
+        _need(t, torch.bfloat16, n, 3)
+    for t, n in ((k_cache, "k_cache"), (v_cache, "v_cache")):
+        _need(t, torch.bfloat16, n, 4)
+    _need(block_tables, torch.int32, "block_tables", 2)
+    _need(kv_lens, torch.int32, "kv_lens", 1)
+    ws_bytes = 0
+    if workspace is not None:
+        if not workspace.is_cuda or not workspace.is_contiguous():
+            raise ValueError("workspace must be a contiguous GPU tensor")
+        ws_bytes = workspace.numel() * workspace.element_size()
+    _check(lib().rag_attn_decode_paged_append(
+        _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(k_cache), _ptr(v_cache), _ptr(o),
+        _ptr(block_tables), _ptr(kv_lens), block_tables.shape[0], block_tables.shape[1],
+        k_cache.shape[0], q.shape[1], k_cache.shape[1], q.shape[2], k_cache.shape[2],
+        float(softmax_scale), int(num_splits), _ptr(workspace), ws_bytes, _stream(stream)))
 
 
 def rag_attn_decode_num_splits(num_decode_seqs, num_kv_heads, max_blocks_per_seq,

@@ -121,6 +121,82 @@ WsLayout workspace_layout(int32_t num_decode, int32_t hq, int32_t hkv, int32_t d
   return w;
 }
 
+// Debug-mode check of a slot mapping: in range, no slot written twice.
+rag_status check_slots(const std::vector<int32_t>& sl, int32_t num_blocks, const char* who) {
+  const int64_t slots = (int64_t)num_blocks * kBlock;
+  std::vector<char> seen((size_t)std::max<int64_t>(slots, 0), 0);
+  for (size_t t = 0; t < sl.size(); ++t) {
+    const int32_t s = sl[t];
+    if (s < 0) continue;
+    if (s >= slots)
+      return fail(RAG_ERR_INVALID_ARG, "%s: slot_mapping[%zu] = %d outside [0, %lld)", who, t, s,
+                  (long long)slots);
+    if (seen[(size_t)s]++)
+      return fail(RAG_ERR_INVALID_ARG, "%s: slot %d is written by two tokens", who, s);
+  }
+  return RAG_OK;
+}
+
+// The prefill behind both entry points; k_cache/v_cache/slots non-null: the
+// prompt prefill that also stores every K/V row in the paged cache.
+rag_status prefill_impl(const void* q, const void* k, const void* v, void* o, float* lse,
+                        const int32_t* cu_seqlens_q, const int32_t* cu_seqlens_k,
+                        int32_t num_seqs, int32_t max_seqlen_q, int32_t max_seqlen_k,
+                        int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
+                        float softmax_scale, int32_t causal, hipStream_t stream,
+                        void* k_cache = nullptr, void* v_cache = nullptr,
+                        const int32_t* slots = nullptr, int32_t num_blocks = 0) {
+  if (!q || !k || !v || !o || !cu_seqlens_q || !cu_seqlens_k)
+    return fail(RAG_ERR_INVALID_ARG, "prefill: null pointer argument");
+  if (num_seqs < 0 || max_seqlen_q < 0 || max_seqlen_k < 0)
+    return fail(RAG_ERR_INVALID_ARG, "prefill: negative size");
+  if (num_q_heads <= 0 || num_kv_heads <= 0 || num_q_heads % num_kv_heads != 0)
+    return fail(RAG_ERR_INVALID_ARG, "prefill: num_q_heads %d must be a positive multiple of "
+                                     "num_kv_heads %d", num_q_heads, num_kv_heads);
+  if (causal != 0 && causal != 1) return fail(RAG_ERR_INVALID_ARG, "prefill: causal must be 0/1");
+  if (!(softmax_scale > 0.f) || softmax_scale > 1e30f)
+    return fail(RAG_ERR_INVALID_ARG, "prefill: softmax_scale must be positive and finite");
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o))
+    return fail(RAG_ERR_INVALID_ARG, "prefill: q/k/v/o must be 16-byte aligned");
+  if (head_dim != 64 && head_dim != 128)
+    return fail(RAG_ERR_UNSUPPORTED, "prefill: head_dim %d (supported: 64, 128)", head_dim);
+  if (num_seqs == 0 || max_seqlen_q == 0) return ok();
+  const int64_t grid = rag::prefill_grid(num_seqs, num_kv_heads, num_q_heads / num_kv_heads,
+                                         max_seqlen_q);
+  if (grid > INT_MAX) return fail(RAG_ERR_UNSUPPORTED, "prefill: batch too large for one grid");
+
+  if (check_mode()) {
+    std::vector<int32_t> cq, ck;
+    if (!fetch(cq, cu_seqlens_q, num_seqs + 1, stream) ||
+        !fetch(ck, cu_seqlens_k, num_seqs + 1, stream))
+      return fail(RAG_ERR_HIP, "prefill: debug copy of cu_seqlens failed");
+    rag_status st = check_cu(cq, "cu_seqlens_q", max_seqlen_q);
+    if (st != RAG_OK) return st;
+    st = check_cu(ck, "cu_seqlens_k", max_seqlen_k);
+    if (st != RAG_OK) return st;
+    if (causal)
+      for (int32_t s = 0; s < num_seqs; ++s)
+        if (cq[s + 1] - cq[s] > ck[s + 1] - ck[s])
+          return fail(RAG_ERR_INVALID_ARG, "prefill: sequence %d has more query rows than keys", s);
+    if (slots) {
+      std::vector<int32_t> sl;
+      if (!fetch(sl, slots, (size_t)ck[num_seqs], stream))
+        return fail(RAG_ERR_HIP, "prefill kvcache: debug copy of slot_mapping failed");
+      rag_status st2 = check_slots(sl, num_blocks, "prefill kvcache");
+      if (st2 != RAG_OK) return st2;
+    }
+  }
+
+  rag::PrefillArgs a{q, k, v, o, lse, cu_seqlens_q, cu_seqlens_k, num_seqs, max_seqlen_q,
+                     num_q_heads, num_kv_heads, head_dim, causal, softmax_scale};
+  a.k_cache = k_cache;
+  a.v_cache = v_cache;
+  a.slots = slots;
+  const hipError_t e = rag::launch_prefill_varlen(a, stream);
+  if (e != hipSuccess) return fail(RAG_ERR_HIP, "prefill launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
 // The decode call behind both entry points.  scratch == false: the split
 // partials go to the caller's workspace (standard layout).  scratch == true:
 // to the library's static per-device scratch (rag::decode_scratch); workspace
@@ -132,7 +208,8 @@ rag_status decode_paged_impl(const void* q, const void* k_cache, const void* v_c
                              int32_t max_seqlen_q, int32_t num_blocks, int32_t num_q_heads,
                              int32_t num_kv_heads, int32_t head_dim, int32_t block_size,
                              float softmax_scale, int32_t num_splits, void* workspace,
-                             size_t workspace_bytes, bool scratch, hipStream_t stream) {
+                             size_t workspace_bytes, bool scratch, hipStream_t stream,
+                             const void* k_new = nullptr, const void* v_new = nullptr) {
   if (!q || !k_cache || !v_cache || !o || !block_tables || !kv_lens)
     return fail(RAG_ERR_INVALID_ARG, "decode: null pointer argument");
   if (num_seqs < 0 || max_blocks_per_seq < 0 || num_blocks < 0 || max_seqlen_q < 0 ||
@@ -224,6 +301,8 @@ rag_status decode_paged_impl(const void* q, const void* k_cache, const void* v_c
   a.d = head_dim;
   a.num_splits = splits;
   a.scale = softmax_scale;
+  a.k_new = k_new;
+  a.v_new = v_new;
   a.arrivals = nullptr;
   a.part_o = a.part_lse = nullptr;
   if (need > 0 && scratch) {
@@ -260,45 +339,9 @@ rag_status rag_attn_prefill_varlen(const void* q, const void* k, const void* v, 
                                    int32_t max_seqlen_q, int32_t max_seqlen_k,
                                    int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
                                    float softmax_scale, int32_t causal, hipStream_t stream) {
-  if (!q || !k || !v || !o || !cu_seqlens_q || !cu_seqlens_k)
-    return fail(RAG_ERR_INVALID_ARG, "prefill: null pointer argument");
-  if (num_seqs < 0 || max_seqlen_q < 0 || max_seqlen_k < 0)
-    return fail(RAG_ERR_INVALID_ARG, "prefill: negative size");
-  if (num_q_heads <= 0 || num_kv_heads <= 0 || num_q_heads % num_kv_heads != 0)
-    return fail(RAG_ERR_INVALID_ARG, "prefill: num_q_heads %d must be a positive multiple of "
-                                     "num_kv_heads %d", num_q_heads, num_kv_heads);
-  if (causal != 0 && causal != 1) return fail(RAG_ERR_INVALID_ARG, "prefill: causal must be 0/1");
-  if (!(softmax_scale > 0.f) || softmax_scale > 1e30f)
-    return fail(RAG_ERR_INVALID_ARG, "prefill: softmax_scale must be positive and finite");
-  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o))
-    return fail(RAG_ERR_INVALID_ARG, "prefill: q/k/v/o must be 16-byte aligned");
-  if (head_dim != 64 && head_dim != 128)
-    return fail(RAG_ERR_UNSUPPORTED, "prefill: head_dim %d (supported: 64, 128)", head_dim);
-  if (num_seqs == 0 || max_seqlen_q == 0) return ok();
-  const int64_t grid = rag::prefill_grid(num_seqs, num_kv_heads, num_q_heads / num_kv_heads,
-                                         max_seqlen_q);
-  if (grid > INT_MAX) return fail(RAG_ERR_UNSUPPORTED, "prefill: batch too large for one grid");
-
-  if (check_mode()) {
-    std::vector<int32_t> cq, ck;
-    if (!fetch(cq, cu_seqlens_q, num_seqs + 1, stream) ||
-        !fetch(ck, cu_seqlens_k, num_seqs + 1, stream))
-      return fail(RAG_ERR_HIP, "prefill: debug copy of cu_seqlens failed");
-    rag_status st = check_cu(cq, "cu_seqlens_q", max_seqlen_q);
-    if (st != RAG_OK) return st;
-    st = check_cu(ck, "cu_seqlens_k", max_seqlen_k);
-    if (st != RAG_OK) return st;
-    if (causal)
-      for (int32_t s = 0; s < num_seqs; ++s)
-        if (cq[s + 1] - cq[s] > ck[s + 1] - ck[s])
-          return fail(RAG_ERR_INVALID_ARG, "prefill: sequence %d has more query rows than keys", s);
-  }
-
-  rag::PrefillArgs a{q, k, v, o, lse, cu_seqlens_q, cu_seqlens_k, num_seqs, max_seqlen_q,
-                     num_q_heads, num_kv_heads, head_dim, causal, softmax_scale};
-  const hipError_t e = rag::launch_prefill_varlen(a, stream);
-  if (e != hipSuccess) return fail(RAG_ERR_HIP, "prefill launch: %s", hipGetErrorString(e));
-  return ok();
+  return prefill_impl(q, k, v, o, lse, cu_seqlens_q, cu_seqlens_k, num_seqs, max_seqlen_q,
+                      max_seqlen_k, num_q_heads, num_kv_heads, head_dim, softmax_scale, causal,
+                      stream);
 }
 
 int32_t rag_attn_decode_num_splits(int32_t num_decode_seqs, int32_t num_kv_heads,
@@ -349,6 +392,45 @@ rag_status rag_attn_decode_paged_noalloc(const void* q, const void* k_cache, con
                            num_splits, nullptr, 0, true, stream);
 }
 
+rag_status rag_attn_decode_paged_append(const void* q, const void* k_new, const void* v_new,
+                                        void* k_cache, void* v_cache, void* o,
+                                        const int32_t* block_tables, const int32_t* kv_lens,
+                                        int32_t num_seqs, int32_t max_blocks_per_seq,
+                                        int32_t num_blocks, int32_t num_q_heads,
+                                        int32_t num_kv_heads, int32_t head_dim,
+                                        int32_t block_size, float softmax_scale,
+                                        int32_t num_splits, void* workspace,
+                                        size_t workspace_bytes, hipStream_t stream) {
+  if (!k_new || !v_new) return fail(RAG_ERR_INVALID_ARG, "decode append: null k_new/v_new");
+  if (!aligned16(k_new) || !aligned16(v_new))
+    return fail(RAG_ERR_INVALID_ARG, "decode append: k_new/v_new must be 16-byte aligned");
+  return decode_paged_impl(q, k_cache, v_cache, o, block_tables, kv_lens, nullptr, num_seqs,
+                           num_seqs, max_blocks_per_seq, 1, num_blocks, num_q_heads,
+                           num_kv_heads, head_dim, block_size, softmax_scale, num_splits,
+                           workspace, workspace_bytes, false, stream, k_new, v_new);
+}
+
+rag_status rag_attn_prefill_varlen_kvcache(const void* q, const void* k, const void* v, void* o,
+                                           float* lse, const int32_t* cu_seqlens,
+                                           int32_t num_seqs, int32_t max_seqlen,
+                                           int32_t num_q_heads, int32_t num_kv_heads,
+                                           int32_t head_dim, float softmax_scale, void* k_cache,
+                                           void* v_cache, const int32_t* slot_mapping,
+                                           int32_t num_blocks, int32_t block_size,
+                                           hipStream_t stream) {
+  if (!k_cache || !v_cache || !slot_mapping)
+    return fail(RAG_ERR_INVALID_ARG, "prefill kvcache: null cache or slot_mapping");
+  if (!aligned16(k_cache) || !aligned16(v_cache))
+    return fail(RAG_ERR_INVALID_ARG, "prefill kvcache: k_cache/v_cache must be 16-byte aligned");
+  if (block_size != kBlock)
+    return fail(RAG_ERR_UNSUPPORTED, "prefill kvcache: block_size %d (supported: 16)",
+                block_size);
+  if (num_blocks < 0) return fail(RAG_ERR_INVALID_ARG, "prefill kvcache: negative num_blocks");
+  return prefill_impl(q, k, v, o, lse, cu_seqlens, cu_seqlens, num_seqs, max_seqlen, max_seqlen,
+                      num_q_heads, num_kv_heads, head_dim, softmax_scale, 1, stream, k_cache,
+                      v_cache, slot_mapping, num_blocks);
+}
+
 rag_status rag_kv_cache_write(const void* k, const void* v, void* k_cache, void* v_cache,
                               const int32_t* slot_mapping, int32_t num_tokens,
                               int32_t num_kv_heads, int32_t head_dim, int32_t block_size,
@@ -371,17 +453,8 @@ rag_status rag_kv_cache_write(const void* k, const void* v, void* k_cache, void*
     std::vector<int32_t> sl;
     if (!fetch(sl, slot_mapping, (size_t)num_tokens, stream))
       return fail(RAG_ERR_HIP, "kv write: debug copy of slot_mapping failed");
-    const int64_t slots = (int64_t)num_blocks * kBlock;
-    std::vector<char> seen((size_t)slots, 0);
-    for (int32_t t = 0; t < num_tokens; ++t) {
-      const int32_t s = sl[t];
-      if (s < 0) continue;
-      if (s >= slots)
-        return fail(RAG_ERR_INVALID_ARG, "kv write: slot_mapping[%d] = %d outside [0, %lld)", t, s,
-                    (long long)slots);
-      if (seen[(size_t)s]++)
-        return fail(RAG_ERR_INVALID_ARG, "kv write: slot %d is written by two tokens", s);
-    }
+    const rag_status st = check_slots(sl, num_blocks, "kv write");
+    if (st != RAG_OK) return st;
   }
   rag::KvWriteArgs a{k, v, k_cache, v_cache, slot_mapping, num_tokens, num_kv_heads, head_dim};
   const hipError_t e = rag::launch_kv_cache_write(a, stream);

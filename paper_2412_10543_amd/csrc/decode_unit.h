@@ -38,12 +38,18 @@ struct DecodeOut {
 // (head l16, lane group gq), the unnormalised O^T accumulators, the head's
 // sum of weights l (already reduced over the lane groups) and the reference
 // maximum m_used (raw score units).
-template <int D, int NP>
+//
+// kAppend: key kv_len - 1 is the step's new token, whose K and V rows are
+// k_new and v_new (this kv head's rows) rather than the cache: the lanes that
+// would load that slot read them there instead (the cache slot is written in
+// the same launch, see decode_unit).
+template <int D, int NP, bool kAppend = false>
 __device__ __forceinline__ void decode_wave(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ kc, const bf16_t* __restrict__ vc,
     size_t block_stride, const int32_t* __restrict__ table, int kv_len, int group,
     int p_first, int p_end, int p_stride, float scale, bf16_t* __restrict__ vt,
-    f32x4 (&oacc)[D / 16], float& m_used, float& l) {
+    f32x4 (&oacc)[D / 16], float& m_used, float& l, const bf16_t* __restrict__ k_new = nullptr,
+    const bf16_t* __restrict__ v_new = nullptr) {
   static_assert(NP % 2 == 0, "pages are consumed in pairs (32 keys per MFMA)");
   using L = DecLds<D, NP>;
   constexpr int kKs = D / 32;   // k-steps over d for S^T
@@ -86,12 +92,25 @@ __device__ __forceinline__ void decode_wave(
     for (int j = 0; j < NP; ++j) {
       const int id = __builtin_amdgcn_readlane(ids, k * NP + (p0 + j < p_end ? j : 0));
       const size_t base = (size_t)id * block_stride;
+      if constexpr (kAppend) {
+        const int key0 = 16 * (p0 + j);
+        const bf16_t* kp = key0 + l16 == kv_len - 1 ? k_new : kc + base + (size_t)l16 * D;
 #pragma unroll
-      for (int ks = 0; ks < kKs; ++ks)
-        kr[j][ks] = load16(kc + base + (size_t)l16 * D + ks * 32 + gq * 8);
+        for (int ks = 0; ks < kKs; ++ks) kr[j][ks] = load16(kp + ks * 32 + gq * 8);
 #pragma unroll
-      for (int t = 0; t < 4; ++t)
-        vr[j][t] = load16(vc + base + (size_t)(4 * gq + t) * D + (l16 % kVch) * 8);
+        for (int t = 0; t < 4; ++t) {
+          const bf16_t* vp =
+              key0 + 4 * gq + t == kv_len - 1 ? v_new : vc + base + (size_t)(4 * gq + t) * D;
+          vr[j][t] = load16(vp + (l16 % kVch) * 8);
+        }
+      } else {
+#pragma unroll
+        for (int ks = 0; ks < kKs; ++ks)
+          kr[j][ks] = load16(kc + base + (size_t)l16 * D + ks * 32 + gq * 8);
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+          vr[j][t] = load16(vc + base + (size_t)(4 * gq + t) * D + (l16 % kVch) * 8);
+      }
     }
   };
 
@@ -247,21 +266,38 @@ constexpr int dec_merge_bytes() {
 // [p_begin, p_end) in interleaved steps of NP pages, merge through LDS and
 // write either the final rows (n_sp == 1) or this split's partial rows; the
 // last split of the row to arrive then merges all partials.
-template <int D, int NP, int W>
+//
+// kAppend: the unit whose range holds the last page also stores the new
+// token's K and V rows (k_new, v_new) into its cache slot, key kv_len - 1 of
+// the block table.  No unit of this launch reads that slot from the cache.
+template <int D, int NP, int W, bool kAppend = false>
 __device__ __forceinline__ void decode_unit(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ kc, const bf16_t* __restrict__ vc,
     size_t block_stride, const int32_t* __restrict__ table, int kv_len, int group,
-    int p_begin, int p_end, float scale, const DecodeOut& out, bf16_t* __restrict__ lds) {
+    int p_begin, int p_end, float scale, const DecodeOut& out, bf16_t* __restrict__ lds,
+    const bf16_t* __restrict__ k_new = nullptr, const bf16_t* __restrict__ v_new = nullptr) {
   using L = DecLds<D, NP, W>;
   static_assert(dec_merge_bytes<D, W>() <= L::kBytes, "merge area must fit in the V slices");
   constexpr int kDt = D / 16;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int l16 = lane & 15, gq = lane >> 4;
 
+  if constexpr (kAppend) {
+    constexpr int kCh = D / 8;
+    if (wave == 0 && p_end == (kv_len + 15) >> 4 && lane < 2 * kCh) {
+      const int key = kv_len - 1;
+      const size_t dst = (size_t)table[key >> 4] * block_stride + (size_t)(key & 15) * D +
+                         (lane % kCh) * 8;
+      const bf16_t* src = (lane < kCh ? k_new : v_new) + (lane % kCh) * 8;
+      bf16_t* cache = const_cast<bf16_t*>(lane < kCh ? kc : vc);
+      *reinterpret_cast<u32x4*>(cache + dst) = load16(src);
+    }
+  }
   f32x4 oacc[kDt];
   float m_used, l;
-  decode_wave<D, NP>(q, kc, vc, block_stride, table, kv_len, group, p_begin + wave * NP, p_end,
-                     W * NP, scale, lds + wave * L::kElemsWave, oacc, m_used, l);
+  decode_wave<D, NP, kAppend>(q, kc, vc, block_stride, table, kv_len, group,
+                              p_begin + wave * NP, p_end, W * NP, scale,
+                              lds + wave * L::kElemsWave, oacc, m_used, l, k_new, v_new);
 
   // ---- merge the W waves through LDS (reusing the V slices) -------------
   // floats: O [wave][16 heads][D], then m [wave][16], then l [wave][16]

@@ -123,12 +123,43 @@ int64_t paged_decode_grid(int num_decode, int hkv, int num_splits) {
   return (int64_t)num_decode * hkv * num_splits;
 }
 
+// Paged KV-cache write fused into the prompt prefill: the K and V rows
+// [r0, r1) of one (sequence, kv head) stream go to their slots in the paged
+// cache (slot = page * 16 + offset; a negative slot skips the row).  Run by
+// each workgroup after its last item, for the key rows of its own query
+// tiles, so every row of a sequence is written once; the rows were streamed
+// through this XCD's L2 by the prefill itself.
+template <int D>
+__device__ __forceinline__ void prefill_rows_to_cache(const bf16_t* __restrict__ k,
+                                                      const bf16_t* __restrict__ v,
+                                                      size_t stride, bf16_t* __restrict__ kc,
+                                                      bf16_t* __restrict__ vc,
+                                                      size_t block_stride,
+                                                      const int32_t* __restrict__ slots,
+                                                      int r0, int r1) {
+  constexpr int kCh = D / 8;
+  const int n = (r1 - r0) * kCh;
+  for (int p = threadIdx.x; p < n; p += 64 * kPfWavesDense) {
+    const int r = r0 + p / kCh, c = p % kCh;
+    const int slot = slots[r];
+    if (slot < 0) continue;
+    const size_t src = (size_t)r * stride + c * 8;
+    const size_t dst = (size_t)(slot >> 4) * block_stride + (size_t)(slot & 15) * D + c * 8;
+    const u32x4 kx = load16(k + src);
+    const u32x4 vx = load16(v + src);
+    *reinterpret_cast<u32x4*>(kc + dst) = kx;
+    *reinterpret_cast<u32x4*>(vc + dst) = vx;
+  }
+}
+
 template <int D>
 __global__ __launch_bounds__(64 * kPfWavesDense, 2) void prefill_varlen_kernel(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ k,
     const bf16_t* __restrict__ v, bf16_t* __restrict__ o, float* __restrict__ lse,
     const int32_t* __restrict__ cu_q, const int32_t* __restrict__ cu_k, int num_seqs,
-    int hq, int hkv, int items, int per, float scale, int causal) {
+    int hq, int hkv, int items, int per, float scale, int causal,
+    bf16_t* __restrict__ k_cache, bf16_t* __restrict__ v_cache,
+    const int32_t* __restrict__ slots) {
   // four K/V stages (separate arrays: the compiler then knows a DMA write to
   // one stage never aliases an LDS read of another)
   __shared__ __attribute__((aligned(16))) bf16_t st0[ChunkLayout<D>::kElemsTile];
@@ -161,6 +192,18 @@ __global__ __launch_bounds__(64 * kPfWavesDense, 2) void prefill_varlen_kernel(
   prefill_items<D, kPfWavesDense, DenseKV>(
       g, kv, [j, per, rows](int it) { return snake_tile(j, it, per) * rows; }, items, st0, st1,
       st2, st3);
+  // Fused cache write (prompt prefill: query rows are the key rows): the
+  // first head group of the kv head writes the key rows of its query tiles.
+  if (slots != nullptr && tc.h0 == tc.kvh * group) {
+    const size_t block_stride = (size_t)hkv * 16 * D;
+    for (int it = 0; it < items; ++it) {
+      const int q0 = snake_tile(j, it, per) * rows;
+      if (q0 >= nq) continue;
+      prefill_rows_to_cache<D>(kv.k, kv.v, kv.stride, k_cache + (size_t)tc.kvh * 16 * D,
+                               v_cache + (size_t)tc.kvh * 16 * D, block_stride, slots + kb, q0,
+                               min(q0 + rows, nk));
+    }
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -184,6 +227,8 @@ struct PagedKernelArgs {
   float* part_o;
   float* part_lse;
   int* arrivals;              // one counter per (decode sequence, kv head)
+  const bf16_t* k_new;        // appended tokens [num_decode, hkv, D] (append launch only)
+  const bf16_t* v_new;
   int num_seqs, num_decode, max_blocks, hq, hkv, num_splits, pps;
   int n_pf_blocks, n_qt;
   int n_dec_groups;           // mixed batches: groups of eight decode units
@@ -192,7 +237,7 @@ struct PagedKernelArgs {
 
 // One piece of a decode row: pages [p_begin, p_end) of (row s, kv head kvh),
 // split sp of n_sp, on W waves taking NP pages a step.
-template <int D, int NP, int W>
+template <int D, int NP, int W, bool kAppend = false>
 __device__ __forceinline__ void decode_piece(const PagedKernelArgs& a, int group,
                                              size_t block_stride, int s, int kvh, int kv_len,
                                              int p_begin, int p_end, int sp, int n_sp,
@@ -209,14 +254,17 @@ __device__ __forceinline__ void decode_piece(const PagedKernelArgs& a, int group
   out.sp = sp;
   out.n_sp = n_sp;
   out.num_splits = a.num_splits;
-  decode_unit<D, NP, W>(a.q + ((size_t)row * a.hq + h0) * D, a.kc + (size_t)kvh * 16 * D,
-                            a.vc + (size_t)kvh * 16 * D, block_stride,
-                            a.tables + (size_t)s * a.max_blocks, kv_len, group, p_begin, p_end,
-                            a.scale, out, lds);
+  const size_t nrow = ((size_t)s * a.hkv + kvh) * D;
+  decode_unit<D, NP, W, kAppend>(a.q + ((size_t)row * a.hq + h0) * D,
+                                 a.kc + (size_t)kvh * 16 * D, a.vc + (size_t)kvh * 16 * D,
+                                 block_stride, a.tables + (size_t)s * a.max_blocks, kv_len, group,
+                                 p_begin, p_end, a.scale, out, lds,
+                                 kAppend ? a.k_new + nrow : nullptr,
+                                 kAppend ? a.v_new + nrow : nullptr);
 }
 
 // Decode unit u with fixed page ranges (see above), on W waves.
-template <int D, int NP, int W>
+template <int D, int NP, int W, bool kAppend = false>
 __device__ __forceinline__ void decode_block(const PagedKernelArgs& a, int u, int group,
                                              size_t block_stride, bf16_t* lds) {
   const int64_t pairs = (int64_t)a.num_decode * a.hkv;
@@ -230,14 +278,18 @@ __device__ __forceinline__ void decode_block(const PagedKernelArgs& a, int u, in
   if (sp >= n_sp && sp > 0) return;
   const int p_begin = sp * a.pps;
   const int p_end = min(n_pages, p_begin + a.pps);
-  decode_piece<D, NP, W>(a, group, block_stride, s, kvh, kv_len, p_begin, p_end, sp, n_sp, lds);
+  decode_piece<D, NP, W, kAppend>(a, group, block_stride, s, kvh, kv_len, p_begin, p_end, sp,
+                                  n_sp, lds);
 }
 
-// Decode rows only: one four-wave workgroup per decode unit.
-template <int D>
+// Decode rows only: one four-wave workgroup per decode unit.  kAppend: each
+// row's last key is the step's new token, taken from k_new / v_new and
+// stored into its cache slot by the same launch.
+template <int D, bool kAppend>
 __global__ __launch_bounds__(kDecThreads, 2) void paged_decode_kernel(PagedKernelArgs a) {
   __shared__ __attribute__((aligned(16))) bf16_t lds[DecLds<D>::kBytes / 2];
-  decode_block<D, kDecPages, kDecWaves>(a, blockIdx.x, a.hq / a.hkv, (size_t)a.hkv * 16 * D, lds);
+  decode_block<D, kDecPages, kDecWaves, kAppend>(a, blockIdx.x, a.hq / a.hkv,
+                                                 (size_t)a.hkv * 16 * D, lds);
 }
 
 // Mixed batch: eight-wave workgroups.  A chunked-prefill tile runs the dense
@@ -303,7 +355,7 @@ static hipError_t launch_prefill_d(const PrefillArgs& a, hipStream_t stream) {
                      stream,
                      (const bf16_t*)a.q, (const bf16_t*)a.k, (const bf16_t*)a.v, (bf16_t*)a.o,
                      a.lse, a.cu_q, a.cu_k, a.num_seqs, a.hq, a.hkv, sp.items, sp.per, a.scale,
-                     a.causal);
+                     a.causal, (bf16_t*)a.k_cache, (bf16_t*)a.v_cache, a.slots);
   return hipGetLastError();
 }
 
@@ -325,6 +377,8 @@ static hipError_t launch_paged_d(const PagedArgs& a, hipStream_t stream) {
   k.part_o = a.part_o;
   k.part_lse = a.part_lse;
   k.arrivals = a.arrivals;
+  k.k_new = (const bf16_t*)a.k_new;
+  k.v_new = (const bf16_t*)a.v_new;
   k.num_seqs = a.num_seqs;
   k.num_decode = a.num_decode;
   k.max_blocks = a.max_blocks;
@@ -348,9 +402,12 @@ static hipError_t launch_paged_d(const PagedArgs& a, hipStream_t stream) {
     if (pf > 0)
       hipLaunchKernelGGL(mixed_kernel<D>, dim3((unsigned)grid), dim3(64 * kPfWavesDense), 0,
                          stream, k);
+    else if (a.k_new != nullptr)
+      hipLaunchKernelGGL((paged_decode_kernel<D, true>), dim3((unsigned)grid), dim3(kDecThreads),
+                         0, stream, k);
     else
-      hipLaunchKernelGGL(paged_decode_kernel<D>, dim3((unsigned)grid), dim3(kDecThreads), 0,
-                         stream, k);
+      hipLaunchKernelGGL((paged_decode_kernel<D, false>), dim3((unsigned)grid), dim3(kDecThreads),
+                         0, stream, k);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }

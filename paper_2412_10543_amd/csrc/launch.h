@@ -21,6 +21,10 @@ struct PrefillArgs {
   const int32_t* cu_k;
   int num_seqs, max_seqlen_q, hq, hkv, d, causal;
   float scale;
+  // fused paged KV-cache write (prompt prefill); slots == null: none
+  void* k_cache = nullptr;
+  void* v_cache = nullptr;
+  const int32_t* slots = nullptr;
 };
 
 struct PagedArgs {
@@ -37,6 +41,10 @@ struct PagedArgs {
   float* part_o;                // workspace (null when num_splits == 1)
   float* part_lse;
   int* arrivals;
+  // pure decode only: the step's new tokens [num_seqs, hkv, d], appended to
+  // the cache and attended by the same launch (null: none)
+  const void* k_new = nullptr;
+  const void* v_new = nullptr;
 };
 
 struct KvWriteArgs {

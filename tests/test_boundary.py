@@ -136,6 +136,54 @@ def test_decode_noalloc_validation(kw, status):
         assert "no-alloc" in binding.rag_last_error()
 
 
+def _prefill_kvcache(**kw):
+    a = dict(q=FAKE, k=FAKE, v=FAKE, o=FAKE, lse=None, cu=FAKE, num_seqs=1, max_len=16, hq=4,
+             hkv=2, d=64, scale=0.125, kc=FAKE, vc=FAKE, slots=FAKE, num_blocks=10, bs=16)
+    a.update(kw)
+    return binding.lib().rag_attn_prefill_varlen_kvcache(
+        a["q"], a["k"], a["v"], a["o"], a["lse"], a["cu"], a["num_seqs"], a["max_len"], a["hq"],
+        a["hkv"], a["d"], a["scale"], a["kc"], a["vc"], a["slots"], a["num_blocks"], a["bs"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(q=None), binding.RAG_ERR_INVALID_ARG),
+    (dict(kc=None), binding.RAG_ERR_INVALID_ARG),
+    (dict(slots=None), binding.RAG_ERR_INVALID_ARG),
+    (dict(vc=FAKE + 8), binding.RAG_ERR_INVALID_ARG),
+    (dict(num_blocks=-1), binding.RAG_ERR_INVALID_ARG),
+    (dict(hq=6, hkv=4), binding.RAG_ERR_INVALID_ARG),
+    (dict(bs=32), binding.RAG_ERR_UNSUPPORTED),
+    (dict(d=96), binding.RAG_ERR_UNSUPPORTED),
+    (dict(num_seqs=0), binding.RAG_OK),
+])
+def test_prefill_kvcache_validation(kw, status):
+    assert _prefill_kvcache(**kw) == status
+
+
+def _decode_append(**kw):
+    a = dict(q=FAKE, kn=FAKE, vn=FAKE, kc=FAKE, vc=FAKE, o=FAKE, bt=FAKE, kl=FAKE, num_seqs=4,
+             max_blocks=64, num_blocks=300, hq=32, hkv=8, d=128, bs=16, scale=0.088, splits=0,
+             ws=None, ws_bytes=0)
+    a.update(kw)
+    return binding.lib().rag_attn_decode_paged_append(
+        a["q"], a["kn"], a["vn"], a["kc"], a["vc"], a["o"], a["bt"], a["kl"], a["num_seqs"],
+        a["max_blocks"], a["num_blocks"], a["hq"], a["hkv"], a["d"], a["bs"], a["scale"],
+        a["splits"], a["ws"], a["ws_bytes"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(kn=None), binding.RAG_ERR_INVALID_ARG),
+    (dict(vn=FAKE + 4), binding.RAG_ERR_INVALID_ARG),
+    (dict(kc=None), binding.RAG_ERR_INVALID_ARG),
+    (dict(hq=12, hkv=8), binding.RAG_ERR_INVALID_ARG),
+    (dict(bs=32), binding.RAG_ERR_UNSUPPORTED),
+    (dict(splits=4), binding.RAG_ERR_WORKSPACE),
+    (dict(num_seqs=0), binding.RAG_OK),
+])
+def test_decode_append_validation(kw, status):
+    assert _decode_append(**kw) == status
+
+
 def _kv_write(**kw):
     a = dict(k=FAKE, v=FAKE, kc=FAKE, vc=FAKE, slots=FAKE, T=16, hkv=8, d=128, bs=16,
              num_blocks=100)
