@@ -103,6 +103,26 @@ int32_t resolve_splits(int32_t num_decode, int32_t hkv, int32_t max_blocks, int3
   return std::max(1, (max_blocks + pps - 1) / pps);
 }
 
+// Balanced units per kv head for a pure decode launch with the automatic
+// policy when its (row, kv head) pairs are fewer than the units aimed at: the
+// pages of all rows are cut into equal ranges, so that rows of very different
+// lengths still give every CU the same amount to stream.  0: not used.
+int32_t balanced_units(int32_t num_decode, int32_t hkv, int32_t max_blocks, int32_t requested) {
+  // (the kernel plans over at most 4 x 64 rows, which this bound implies)
+  if (requested > 0 || num_decode <= 0 || (int64_t)num_decode * hkv >= kTargetUnits) return 0;
+  const int32_t units = std::min<int32_t>(kMaxSplits, (kTargetUnits + hkv - 1) / hkv);
+  // the kernel's page arithmetic is 32-bit
+  if ((int64_t)num_decode * std::max(max_blocks, 1) * (units + 1) >= ((int64_t)1 << 31)) return 0;
+  return units;
+}
+
+// Partial-result slots per decode row: the most pieces either policy cuts a
+// row into (this sizes the workspace whichever launch uses it).
+int32_t decode_slots(int32_t num_decode, int32_t hkv, int32_t max_blocks, int32_t requested) {
+  return std::max(resolve_splits(num_decode, hkv, max_blocks, requested),
+                  balanced_units(num_decode, hkv, max_blocks, requested));
+}
+
 // Workspace: [arrival counters int32, one per (decode row, kv head)]
 // [partial outputs fp32] [partial log-sum-exp fp32], each 256-byte aligned.
 struct WsLayout {
@@ -239,7 +259,12 @@ rag_status decode_paged_impl(const void* q, const void* k_cache, const void* v_c
   const int32_t splits =
       num_decode > 0 ? resolve_splits(num_decode, num_kv_heads, max_blocks_per_seq, num_splits)
                      : 1;
-  const WsLayout ws = workspace_layout(num_decode, num_q_heads, num_kv_heads, head_dim, splits);
+  const int32_t slots =
+      num_decode > 0 ? decode_slots(num_decode, num_kv_heads, max_blocks_per_seq, num_splits) : 1;
+  const int32_t bal = cu_seqlens_q == nullptr
+                          ? balanced_units(num_decode, num_kv_heads, max_blocks_per_seq, num_splits)
+                          : 0;
+  const WsLayout ws = workspace_layout(num_decode, num_q_heads, num_kv_heads, head_dim, slots);
   const size_t need = ws.bytes;
   if (!scratch && need > 0 && (workspace == nullptr || workspace_bytes < need))
     return fail(RAG_ERR_WORKSPACE, "decode: workspace of %zu bytes needed, %zu given", need,
@@ -251,7 +276,8 @@ rag_status decode_paged_impl(const void* q, const void* k_cache, const void* v_c
   const int64_t grid =
       (mixed ? rag::paged_prefill_grid(num_seqs - num_decode, num_kv_heads, group, max_seqlen_q)
              : 0) +
-      rag::paged_decode_grid(num_decode, num_kv_heads, splits) + 8;   // + group padding
+      std::max<int64_t>(rag::paged_decode_grid(num_decode, num_kv_heads, splits),
+                        (int64_t)bal * num_kv_heads) + 8;   // + group padding
   if (grid > INT_MAX) return fail(RAG_ERR_UNSUPPORTED, "decode: batch too large for one grid");
 
   if (check_mode()) {
@@ -300,6 +326,8 @@ rag_status decode_paged_impl(const void* q, const void* k_cache, const void* v_c
   a.hkv = num_kv_heads;
   a.d = head_dim;
   a.num_splits = splits;
+  a.slots = slots;
+  a.bal_units = bal;
   a.scale = softmax_scale;
   a.k_new = k_new;
   a.v_new = v_new;
@@ -349,7 +377,7 @@ int32_t rag_attn_decode_num_splits(int32_t num_decode_seqs, int32_t num_kv_heads
                                    int32_t num_splits) {
   (void)block_size;
   if (num_decode_seqs <= 0 || num_kv_heads <= 0 || max_blocks_per_seq <= 0) return 1;
-  return resolve_splits(num_decode_seqs, num_kv_heads, max_blocks_per_seq, num_splits);
+  return decode_slots(num_decode_seqs, num_kv_heads, max_blocks_per_seq, num_splits);
 }
 
 size_t rag_attn_decode_workspace_size(int32_t num_decode_seqs, int32_t num_q_heads,

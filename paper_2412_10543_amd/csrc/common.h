@@ -105,6 +105,10 @@ __device__ __forceinline__ void wave_lds_sync() {
 __device__ __forceinline__ u32x4 load16(const void* p) {
   return *reinterpret_cast<const u32x4*>(p);
 }
+// 16-byte load with the non-temporal (streaming) hint: data read once.
+__device__ __forceinline__ u32x4 load16_stream(const void* p) {
+  return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+}
 
 // gfx950 transposing LDS read (ds_read_b64_tr_b16).  Within each group of 16
 // lanes, lane i supplies the address of 4 consecutive bf16 values (row i of a
@@ -195,6 +199,7 @@ __host__ __device__ constexpr int pf_rows_per_tile(int group, int waves) {
 constexpr int kDecThreads = 256;
 constexpr int kDecWaves = kDecThreads / kWave;
 constexpr int kDecMaxGroup = 16;           // q heads per kv head (MFMA N)
+constexpr int kDecMinPages = 16;           // fewest pages a balanced decode unit takes
 
 // Per wave: the V rows of the NP pages of one step, row-major [16*NP][D + 16].
 #ifndef RAG_DEC_PAGES

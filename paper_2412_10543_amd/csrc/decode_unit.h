@@ -8,7 +8,11 @@
 // softmax in fp32.  Layout choices for CDNA4:
 //   * every K/V byte of the range is read once, for all G heads of the group,
 //     with 16-byte loads; the W waves take interleaved steps of NP pages,
-//     so at any time they stream neighbouring pages;
+//     so at any time they stream neighbouring pages; the V loads (each
+//     instruction covers four whole 256-byte rows) carry the non-temporal
+//     hint, as nothing of a decode step's pages is read again in the launch;
+//     the K loads (64 bytes of each of 16 rows per instruction, two
+//     instructions per 128-byte line) do not, as that made them slower;
 //   * both products run on v_mfma_f32_16x16x32_bf16 with the G query heads as
 //     the N dimension (padded to 16): S^T = K Q^T straight from registers,
 //     then O^T = V^T P^T with the V rows staged row-major in a per-wave LDS
@@ -101,7 +105,7 @@ __device__ __forceinline__ void decode_wave(
         for (int t = 0; t < 4; ++t) {
           const bf16_t* vp =
               key0 + 4 * gq + t == kv_len - 1 ? v_new : vc + base + (size_t)(4 * gq + t) * D;
-          vr[j][t] = load16(vp + (l16 % kVch) * 8);
+          vr[j][t] = load16_stream(vp + (l16 % kVch) * 8);
         }
       } else {
 #pragma unroll
@@ -109,7 +113,7 @@ __device__ __forceinline__ void decode_wave(
           kr[j][ks] = load16(kc + base + (size_t)l16 * D + ks * 32 + gq * 8);
 #pragma unroll
         for (int t = 0; t < 4; ++t)
-          vr[j][t] = load16(vc + base + (size_t)(4 * gq + t) * D + (l16 % kVch) * 8);
+          vr[j][t] = load16_stream(vc + base + (size_t)(4 * gq + t) * D + (l16 % kVch) * 8);
       }
     }
   };

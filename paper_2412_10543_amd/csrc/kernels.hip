@@ -230,6 +230,8 @@ struct PagedKernelArgs {
   const bf16_t* k_new;        // appended tokens [num_decode, hkv, D] (append launch only)
   const bf16_t* v_new;
   int num_seqs, num_decode, max_blocks, hq, hkv, num_splits, pps;
+  int slots;                  // partial-result slots per (row, head): workspace stride
+  int bal_units;              // balanced decode: units per kv head (0: uniform splits)
   int n_pf_blocks, n_qt;
   int n_dec_groups;           // mixed batches: groups of eight decode units
   float scale;
@@ -246,14 +248,13 @@ __device__ __forceinline__ void decode_piece(const PagedKernelArgs& a, int group
   const int h0 = kvh * group;
   DecodeOut out;
   out.o = a.o + ((size_t)row * a.hq + h0) * D;
-  out.part_o = a.part_o ? a.part_o + (size_t)s * a.hq * a.num_splits * D +
-                              (size_t)h0 * a.num_splits * D
+  out.part_o = a.part_o ? a.part_o + (size_t)s * a.hq * a.slots * D + (size_t)h0 * a.slots * D
                         : nullptr;
-  out.part_lse = a.part_lse ? a.part_lse + ((size_t)s * a.hq + h0) * a.num_splits : nullptr;
+  out.part_lse = a.part_lse ? a.part_lse + ((size_t)s * a.hq + h0) * a.slots : nullptr;
   out.arrival = a.arrivals ? a.arrivals + (size_t)s * a.hkv + kvh : nullptr;
   out.sp = sp;
   out.n_sp = n_sp;
-  out.num_splits = a.num_splits;
+  out.num_splits = a.slots;
   const size_t nrow = ((size_t)s * a.hkv + kvh) * D;
   decode_unit<D, NP, W, kAppend>(a.q + ((size_t)row * a.hq + h0) * D,
                                  a.kc + (size_t)kvh * 16 * D, a.vc + (size_t)kvh * 16 * D,
@@ -280,6 +281,71 @@ __device__ __forceinline__ void decode_block(const PagedKernelArgs& a, int u, in
   const int p_end = min(n_pages, p_begin + a.pps);
   decode_piece<D, NP, W, kAppend>(a, group, block_stride, s, kvh, kv_len, p_begin, p_end, sp,
                                   n_sp, lds);
+}
+
+// Balanced decode units: the pages of all rows of one kv head, laid end to
+// end (row by row), are cut into equal ranges of at least kDecMinPages pages
+// (at most bal_units of them); unit k of kv head kvh attends the pieces of the
+// rows its range covers (usually one or two), each piece split sp of the n_sp
+// units that cover its row.  Unit sizes no longer follow the rows' lengths,
+// so every CU streams the same number of pages and none is left with a long
+// tail.  The plan comes from kv_lens, loaded once (one lane per row, rows in
+// chunks of 64; fewer than 256 rows take this path) and walked with
+// wave-uniform reads.
+constexpr int kBalMaxChunks = 4;
+
+template <int D, int NP, int W, bool kAppend>
+__device__ __forceinline__ void decode_block_balanced(const PagedKernelArgs& a, int u, int group,
+                                                      size_t block_stride, bf16_t* lds) {
+  const int kvh = u % a.hkv, k = u / a.hkv;
+  if (k >= a.bal_units) return;
+  const int S = a.num_decode, lane = threadIdx.x & 63, cap = a.max_blocks * 16;
+  int kl[kBalMaxChunks];
+#pragma unroll
+  for (int c = 0; c < kBalMaxChunks; ++c) {
+    const int s = c * kWave + lane;
+    kl[c] = s < S ? min(a.kv_lens[s], cap) : 0;
+  }
+  int total = 0;
+#pragma unroll
+  for (int c = 0; c < kBalMaxChunks; ++c)
+    for (int i = 0; i < min(kWave, S - c * kWave); ++i)
+      total += (__builtin_amdgcn_readlane(kl[c], i) + 15) >> 4;
+  // at least kDecMinPages pages per unit (short batches use fewer units)
+  const int K = max(1, min(a.bal_units, total / kDecMinPages));
+  if (k >= K) return;
+  // 32-bit arithmetic: the host takes this path only when rows x table
+  // width x units stays below 2^31
+  const uint32_t ut = (uint32_t)total, uk = (uint32_t)K;
+  const int lo = (int)((uint32_t)k * ut / uk), hi = (int)((uint32_t)(k + 1) * ut / uk);
+  // unit holding global page g: ceil((g + 1) K / total) - 1
+  auto unit_of = [&](int g) { return (int)(((uint32_t)(g + 1) * uk + ut - 1) / ut) - 1; };
+  int gs = 0;                 // first global page of the row
+  bool first_piece = true;
+#pragma unroll
+  for (int c = 0; c < kBalMaxChunks; ++c) {
+    for (int i = 0; i < min(kWave, S - c * kWave) && gs < hi; ++i) {
+      const int kls = __builtin_amdgcn_readlane(kl[c], i);
+      const int ps = (kls + 15) >> 4;
+      if (ps > 0 && gs + ps > lo) {
+        const int first = unit_of(gs), last = unit_of(gs + ps - 1);
+        if (!first_piece) __syncthreads();   // LDS of the previous piece fully read
+        first_piece = false;
+        decode_piece<D, NP, W, kAppend>(a, group, block_stride, c * kWave + i, kvh, kls,
+                                        max(lo, gs) - gs, min(hi, gs + ps) - gs, k - first,
+                                        last - first + 1, lds);
+      }
+      gs += ps;
+    }
+  }
+}
+
+template <int D, bool kAppend>
+__global__ __launch_bounds__(kDecThreads, 2) void paged_decode_balanced_kernel(
+    PagedKernelArgs a) {
+  __shared__ __attribute__((aligned(16))) bf16_t lds[DecLds<D>::kBytes / 2];
+  decode_block_balanced<D, kDecPages, kDecWaves, kAppend>(a, blockIdx.x, a.hq / a.hkv,
+                                                          (size_t)a.hkv * 16 * D, lds);
 }
 
 // Decode rows only: one four-wave workgroup per decode unit.  kAppend: each
@@ -386,6 +452,8 @@ static hipError_t launch_paged_d(const PagedArgs& a, hipStream_t stream) {
   k.hkv = a.hkv;
   k.num_splits = a.num_splits;
   k.pps = std::max(1, (a.max_blocks + a.num_splits - 1) / a.num_splits);
+  k.slots = std::max(a.slots, a.num_splits);
+  k.bal_units = a.cu_q == nullptr ? a.bal_units : 0;
   k.scale = a.scale;
   const bool mixed = a.cu_q != nullptr && a.num_seqs > a.num_decode;
   const int pf_rows = pf_rows_per_tile(group, kPfWavesDense);
@@ -394,7 +462,8 @@ static hipError_t launch_paged_d(const PagedArgs& a, hipStream_t stream) {
                                                 a.max_seqlen_q)
                            : 0;
   k.n_pf_blocks = (int)pf;
-  int64_t dec = paged_decode_grid(a.num_decode, a.hkv, a.num_splits);
+  int64_t dec = k.bal_units > 0 ? (int64_t)k.bal_units * a.hkv
+                                : paged_decode_grid(a.num_decode, a.hkv, a.num_splits);
   if (pf > 0) dec = (dec + kNumXcd - 1) / kNumXcd * kNumXcd;   // whole groups of eight
   k.n_dec_groups = (int)(dec / kNumXcd);
   const int64_t grid = pf + dec;
@@ -402,6 +471,12 @@ static hipError_t launch_paged_d(const PagedArgs& a, hipStream_t stream) {
     if (pf > 0)
       hipLaunchKernelGGL(mixed_kernel<D>, dim3((unsigned)grid), dim3(64 * kPfWavesDense), 0,
                          stream, k);
+    else if (k.bal_units > 0 && a.k_new != nullptr)
+      hipLaunchKernelGGL((paged_decode_balanced_kernel<D, true>), dim3((unsigned)grid),
+                         dim3(kDecThreads), 0, stream, k);
+    else if (k.bal_units > 0)
+      hipLaunchKernelGGL((paged_decode_balanced_kernel<D, false>), dim3((unsigned)grid),
+                         dim3(kDecThreads), 0, stream, k);
     else if (a.k_new != nullptr)
       hipLaunchKernelGGL((paged_decode_kernel<D, true>), dim3((unsigned)grid), dim3(kDecThreads),
                          0, stream, k);

@@ -37,6 +37,8 @@ struct PagedArgs {
   const int32_t* cu_q;          // null: pure decode
   int num_seqs, num_decode, max_blocks, max_seqlen_q;
   int hq, hkv, d, num_splits;
+  int slots = 0;                // partial-result slots per (row, head) in the workspace
+  int bal_units = 0;            // pure decode: balanced units per kv head (0: uniform splits)
   float scale;
   float* part_o;                // workspace (null when num_splits == 1)
   float* part_lse;
