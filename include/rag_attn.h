@@ -143,9 +143,11 @@ rag_status rag_attn_prefill_varlen_kvcache(
     hipStream_t stream);
 
 /*
- * Number of KV splits rag_attn_decode_paged uses for its decode rows when it
- * is passed num_splits (0 = choose automatically), given the number of decode
- * rows, kv heads and the block-table width.  Always >= 1.
+ * Partial-result slots per decode row that rag_attn_decode_paged may use when
+ * it is passed num_splits (0 = choose automatically), given the number of
+ * decode rows, kv heads and the block-table width: the most pieces a row's
+ * keys are cut into (the workspace holds one partial output per slot).
+ * Always >= 1.
  */
 int32_t rag_attn_decode_num_splits(int32_t num_decode_seqs,
                                    int32_t num_kv_heads,
@@ -191,8 +193,14 @@ size_t rag_attn_decode_workspace_size(int32_t num_decode_seqs,
  *            num_q_heads / num_kv_heads <= 16.
  *   num_splits  0 = automatic; else the number of KV splits per decode row
  *            (clamped to [1, min(64, max_blocks_per_seq)]).
- *            Splits are merged (log-sum-exp) inside the same kernel by the
- *            last split of each row to finish.
+ *            Automatic: about one unit of work per CU.  A pure decode batch
+ *            (cu_seqlens_q == NULL) with fewer (row, kv head) pairs than that
+ *            has the pages of all its rows, per kv head, cut into equal
+ *            ranges of at least 16 pages, so that rows of different lengths
+ *            still give every unit the same amount to read; otherwise every
+ *            row is cut into the same number of splits.
+ *            Pieces of a row are merged (log-sum-exp) inside the same kernel
+ *            by the last one to finish.
  *   workspace, workspace_bytes  device scratch of at least
  *            rag_attn_decode_workspace_size(...) bytes (may be NULL when that
  *            is 0); 256-byte aligned.  It must be zero-filled before its first

@@ -91,6 +91,21 @@ def test_decode(orc, kv_lens, hq, hkv, d, splits):
     G.assert_parity(o, ro, f"decode splits={splits}")
 
 
+@pytest.mark.parametrize("seed", [1, 2])
+def test_decode_balanced_units_many_rows(orc, seed):
+    """Automatic policy with fewer (row, kv head) pairs than CUs: units cut
+    the pages of all rows into equal ranges, so one unit covers pieces of
+    several short rows and long rows span several units.  Against the oracle
+    and within rounding of a uniform two-way split."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    lens = [int(x) for x in rng.integers(1, 3000, size=30)] + [9000, 1]
+    q, pool = G.decode_case(lens, 32, 8, 128, seed=seed + 40)
+    o = G.gpu_paged(q, pool, 32, 8, 128, G.scale_for(128), num_splits=0)
+    G.assert_parity(o, G.oracle_paged(orc, q, pool, G.scale_for(128)), "balanced")
+    o2 = G.gpu_paged(q, pool, 32, 8, 128, G.scale_for(128), num_splits=2)
+    assert float((o.float() - o2.float()).abs().max()) < 1e-2
+
+
 def test_decode_peaky(orc):
     q, pool = G.decode_case([700, 33, 4000], 32, 8, 128, seed=3, q_scale=8.0)
     o = G.gpu_paged(q, pool, 32, 8, 128, G.scale_for(128))
