@@ -883,6 +883,96 @@ def prefill_only(torch, name, dev, reps):
             "algorithmic_bytes": prefill_bytes(lens, lens, w.hq, w.hkv, w.d)}
 
 
+def ceilings(torch, dev, reps=5, clocks=True):
+    """Hardware ceilings the roofline fractions are read against, measured
+    with the probes of libceiling_probes.so (HIP events around one launch,
+    median of `reps`): random 4 KB page reads (decode's access pattern; two
+    disjoint 512 MB page sets of an 8 GB pool alternate, so neither is found
+    in the 256 MB Infinity Cache), a contiguous 4 GB read, and a
+    dependency-free bf16 MFMA loop."""
+    import ctypes
+
+    import numpy as np
+
+    from paper_2412_10543_amd import build as pb
+    L = ctypes.CDLL(pb.PROBES)
+    vp = ctypes.c_void_p
+    L.rag_probe_page_read.argtypes = [vp, vp, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, vp, vp]
+    L.rag_probe_stream_read.argtypes = [vp, ctypes.c_int64, ctypes.c_int32, vp, vp]
+    L.rag_probe_mfma_loop.argtypes = [ctypes.c_int32, ctypes.c_int32, vp, vp]
+    stream = torch.cuda.current_stream().cuda_stream
+    sink = torch.zeros(1 << 16, dtype=torch.int32, device=dev)
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(reps):
+            a = torch.cuda.Event(enable_timing=True)
+            b = torch.cuda.Event(enable_timing=True)
+            a.record()
+            fn()
+            b.record()
+            torch.cuda.synchronize()
+            ts.append(a.elapsed_time(b))
+        return median(ts)
+
+    out = {}
+    pool_pages = 2 << 20                      # 8 GiB of 4 KB pages
+    pool = torch.empty(pool_pages * 1024, dtype=torch.int32, device=dev)
+    pool.fill_(7)
+    n = 128 << 10                             # 512 MiB per launch
+    perm = np.random.Generator(np.random.PCG64(5)).permutation(pool_pages).astype(np.int32)
+    sets = [torch.from_numpy(perm[i * n:(i + 1) * n].copy()).to(dev) for i in range(2)]
+    pages = {}
+    for hint in (0, 1):
+        for wg in (256, 512, 1024, 2048):
+            it = [0]
+
+            def run(wg=wg, hint=hint):
+                ids = sets[it[0] % 2]
+                it[0] += 1
+                assert L.rag_probe_page_read(pool.data_ptr(), ids.data_ptr(), n, wg, hint,
+                                             sink.data_ptr(), stream) == 0
+            ms = timed(run)
+            pages[f"{'nt' if hint else 'default'}_wg{wg}"] = round(n * 4096 / ms / 1e6, 1)
+    out["random_4k_page_read_gbs"] = pages
+    out["random_4k_page_read_best_gbs"] = max(pages.values())
+    del pool, sets
+    torch.cuda.empty_cache()
+    buf = torch.empty(1 << 30, dtype=torch.int32, device=dev)   # 4 GiB
+    buf.fill_(3)
+    stream_gbs = {}
+    for wg in (1024, 2048, 4096):
+        ms = timed(lambda wg=wg: L.rag_probe_stream_read(buf.data_ptr(), buf.numel() * 4, wg,
+                                                         sink.data_ptr(), stream))
+        stream_gbs[f"wg{wg}"] = round(buf.numel() * 4 / ms / 1e6, 1)
+    out["stream_read_gbs"] = stream_gbs
+    out["stream_read_best_gbs"] = max(stream_gbs.values())
+    del buf
+    torch.cuda.empty_cache()
+    mfma = {}
+    iters = 20000
+    for wg in (256, 512):
+        ms = timed(lambda wg=wg: L.rag_probe_mfma_loop(iters, wg, sink.data_ptr(), stream))
+        flops = wg * 8 * 4 * iters * 32768.0
+        mfma[f"wg{wg}_waves_per_simd{wg // 128}"] = round(flops / ms / 1e9, 1)
+    out["mfma_bf16_loop_tflops"] = mfma
+    out["mfma_bf16_loop_best_tflops"] = max(mfma.values())
+    if clocks:
+        # the shader clock while the MFMA loop runs (about 2 s of launches)
+        sampler = ClockSampler(delay=1.0)
+        sampler.start()
+        t0 = time.perf_counter()
+        while time.perf_counter() - t0 < 2.0:
+            L.rag_probe_mfma_loop(iters, 256, sink.data_ptr(), stream)
+            torch.cuda.synchronize()
+        out["clocks_during_mfma_loop"] = sampler.join()
+        out["clocks_idle"] = read_clocks()
+    out["peaks"] = {"hbm_gbs": PEAK_HBM_GBS, "bf16_tflops": PEAK_BF16_TFLOPS}
+    return out
+
+
 def copy_calibration(torch, gib=1.0):
     """A plain device copy of known size, for scaling the HBM traffic counters."""
     n = int(gib * (1 << 30))
@@ -909,6 +999,8 @@ def main():
     ap.add_argument("--prefill-only", metavar="WORKLOAD",
                     help="only run this workload's packed prefill --reps times (for counter runs)")
     ap.add_argument("--reps", type=int, default=2)
+    ap.add_argument("--ceilings", action="store_true",
+                    help="only the hardware ceiling probes (page reads, stream read, MFMA loop)")
     ap.add_argument("--no-clocks", action="store_true",
                     help="do not query amd-smi for the clocks (skipped under rocprofv3 anyway)")
     args = ap.parse_args()
@@ -923,7 +1015,7 @@ def main():
     under_profiler = any(k.startswith("ROCPROF") for k in os.environ) or \
         "rocprof" in os.environ.get("LD_PRELOAD", "")
     want_clocks = not (args.no_clocks or under_profiler or args.copy_calibration or args.awq_only
-                       or args.prefill_only)
+                       or args.prefill_only or args.ceilings)
     clocks = {"idle_before": read_clocks()} if want_clocks else None
 
     import torch
@@ -932,6 +1024,10 @@ def main():
         sys.exit(1)
     if args.copy_calibration:
         copy_calibration(torch)
+        return
+    if args.ceilings:
+        res = ceilings(torch, torch.device("cuda:0"), clocks=not under_profiler)
+        print(json.dumps({"ceilings": res}))
         return
     if args.awq_only:
         print(json.dumps({"awq_gemm_7b": bench_phase_awq(torch, torch.device("cuda:0"),

@@ -1,0 +1,46 @@
+/*
+ * ceiling_probes.h -- measurement probes for MI355X (gfx950), built into
+ * libceiling_probes.so next to librag_attn.so.  They are not part of the
+ * attention method: they measure what the hardware gives kernels shaped like
+ * the library's, the ceilings its roofline fractions are read against
+ * (bench.py --ceilings times them with HIP events).
+ *
+ * Each call enqueues one kernel on `stream` and returns 0, -1 for an invalid
+ * argument, -4 for a launch error.  `sink` is a device buffer of at least
+ * 4 * workgroups bytes that the kernel may write (it keeps the reads or the
+ * products from being optimised away).
+ */
+#ifndef RAG_CEILING_PROBES_H
+#define RAG_CEILING_PROBES_H
+
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Reads num_pages 4096-byte pages of `pool` (device), page i at byte offset
+ * 4096 * page_ids[i] (device int32 list, caller-chosen order), with 16-byte
+ * loads; each wave keeps four pages (16 KB) in flight.  stream_hint = 1 adds
+ * the non-temporal hint to the loads. */
+int rag_probe_page_read(const void *pool, const int32_t *page_ids,
+                        int64_t num_pages, int32_t workgroups,
+                        int32_t stream_hint, void *sink, hipStream_t stream);
+
+/* Reads `bytes` (a multiple of 16) of `buf` contiguously with 16-byte loads. */
+int rag_probe_stream_read(const void *buf, int64_t bytes, int32_t workgroups,
+                          void *sink, hipStream_t stream);
+
+/* `workgroups` eight-wave workgroups; every wave issues 4 * iters
+ * v_mfma_f32_32x32x16_bf16 (32768 FLOP each) into four independent
+ * accumulators, with no memory traffic. */
+int rag_probe_mfma_loop(int32_t iters, int32_t workgroups, void *sink,
+                        hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RAG_CEILING_PROBES_H */

@@ -31,6 +31,24 @@ SOURCES = ["kernels.hip", "kv_cache.hip", "awq_gemm.hip", "decode_scratch.hip", 
 HEADERS = ["common.h", "prefill_tile.h", "decode_unit.h", "launch.h", "errors.h", "awq.h"]
 
 
+PROBES = os.path.join(PKG, "libceiling_probes.so")
+
+
+def build_probes(verbose: bool = False) -> str:
+    """The hardware ceiling probes (measurement only, not the method)."""
+    os.makedirs(OBJDIR, exist_ok=True)
+    obj = os.path.join(OBJDIR, "ceiling_probes.o")
+    cmd = [HIPCC, *COMMON, *DEVICE_FLAGS, "-x", "hip", "-c",
+           os.path.join(CSRC, "ceiling_probes.hip"), "-o", obj]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    subprocess.run(cmd, check=True, stderr=None if verbose else subprocess.PIPE)
+    tmp = PROBES + ".tmp"
+    subprocess.run([HIPCC, "-shared", "-fPIC", f"--offload-arch={ARCH}", "-o", tmp, obj], check=True)
+    os.replace(tmp, PROBES)
+    return PROBES
+
+
 def build(verbose: bool = False) -> str:
     os.makedirs(OBJDIR, exist_ok=True)
     objs = []
@@ -49,6 +67,7 @@ def build(verbose: bool = False) -> str:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
     os.replace(tmp, LIBRARY)
+    build_probes(verbose)
     return LIBRARY
 
 

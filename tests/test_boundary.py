@@ -38,6 +38,27 @@ def test_header_declarations_exported():
         assert hasattr(L, n), f"{n} not exported"
 
 
+def test_ceiling_probe_library_exports_its_header():
+    """The measurement probes (bench.py --ceilings) live in their own library;
+    its header's declarations are exactly its exports, and bad arguments are
+    rejected without a launch."""
+    import ctypes
+    from paper_2412_10543_amd import build as pb
+    if not os.path.exists(pb.PROBES):
+        pytest.skip("libceiling_probes.so not built")
+    text = re.sub(r"/\*.*?\*/", "", open(os.path.join(ROOT, "include", "ceiling_probes.h")).read(),
+                  flags=re.S)
+    names = sorted(set(re.findall(r"\b(rag_[a-z0-9_]+)\s*\(", text)))
+    assert names == ["rag_probe_mfma_loop", "rag_probe_page_read", "rag_probe_stream_read"]
+    L = ctypes.CDLL(pb.PROBES)
+    for n in names:
+        assert hasattr(L, n)
+    L.rag_probe_mfma_loop.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
+                                      ctypes.c_void_p]
+    assert L.rag_probe_mfma_loop(10, 0, FAKE, None) == -1
+    assert L.rag_probe_mfma_loop(10, 4, None, None) == -1
+
+
 def test_abi_version():
     assert binding.rag_abi_version() == 1
 
