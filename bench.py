@@ -79,6 +79,15 @@ def kernel_source_hash():
     return h.hexdigest()[:16]
 
 
+def decode_kernel_name(num_decode, hkv):
+    """The decode kernel a default-policy launch of `num_decode` rows runs:
+    balanced units when rows x kv heads leave CUs idle (fewer than 256
+    pairs), one workgroup per (row, kv head, split) otherwise."""
+    if num_decode * hkv < 256:
+        return "paged_decode_balanced_kernel<128, false>"
+    return "paged_decode_kernel<128, false>"
+
+
 def stored_traffic(kernel_key):
     """HBM traffic per launch from the committed counter summary, if it was
     taken on the current kernel sources."""
@@ -268,7 +277,10 @@ def roofline(bound, achieved, peak, unit, traffic=None, kernel=None):
 
 def median(x):
     s = sorted(x)
-    return s[len(s) // 2] if s else float("nan")
+    if not s:
+        return float("nan")
+    n = len(s)
+    return s[n // 2] if n % 2 else 0.5 * (s[n // 2 - 1] + s[n // 2])
 
 
 # ---------------------------------------------------------------------------
@@ -984,6 +996,68 @@ def copy_calibration(torch, gib=1.0):
     print(json.dumps({"copy_bytes": n, "launches": 3}))
 
 
+TRAFFIC_COMMANDS = [
+    "rocprofv3 --pmc FETCH_SIZE --output-format csv -d {d}/pmc_FETCH_SIZE -o p -- "
+    "python3 -u bench.py --steps 1 --warmup 0 --no-extra --no-cpu-baseline",
+    "rocprofv3 --pmc WRITE_SIZE --output-format csv -d {d}/pmc_WRITE_SIZE -o p -- "
+    "python3 -u bench.py --steps 1 --warmup 0 --no-extra --no-cpu-baseline",
+    "rocprofv3 --pmc FETCH_SIZE --output-format csv -d {d}/cal_FETCH_SIZE -o p -- "
+    "python3 -u bench.py --copy-calibration",
+    "rocprofv3 --pmc WRITE_SIZE --output-format csv -d {d}/cal_WRITE_SIZE -o p -- "
+    "python3 -u bench.py --copy-calibration",
+]
+
+
+def traffic_summary(prof_dir, out_path):
+    """HBM traffic per launch of the attention kernels of the default command,
+    from the four counter runs of TRAFFIC_COMMANDS with {d} = `prof_dir`:
+    FETCH_SIZE and WRITE_SIZE (KiB per dispatch) of each kernel, scaled by
+    what the same counters read for the calibration copy of 1 GiB."""
+    import collections
+    import csv
+
+    def load(sub):
+        out = collections.defaultdict(list)
+        with open(os.path.join(prof_dir, sub, "p_counter_collection.csv")) as f:
+            for r in csv.DictReader(f):
+                out[r["Kernel_Name"]].append(float(r["Counter_Value"]))
+        return out
+
+    def short(name):   # "void rag::(anon)::k<128, false>(args)" -> "k<128, false>"
+        return name.split("(")[0].replace("void ", "").split("::")[-1]
+
+    cal_f, cal_w = load("cal_FETCH_SIZE"), load("cal_WRITE_SIZE")
+    copy = [k for k in cal_f if "copyBuffer" in k][0]
+    cf = sorted(cal_f[copy])[len(cal_f[copy]) // 2]       # median of the 3 copies
+    cw = sorted(cal_w[copy])[len(cal_w[copy]) // 2]
+    copy_kib = (1 << 30) / 1024
+    ff, wf = copy_kib / cf, copy_kib / cw
+    pf, pw = load("pmc_FETCH_SIZE"), load("pmc_WRITE_SIZE")
+    kern = {}
+    for name in pf:
+        key = short(name)
+        if not (key.startswith("prefill_varlen_kernel") or key.startswith("paged_decode")):
+            continue
+        f = sum(pf[name]) / len(pf[name])
+        wr = sum(pw[name]) / len(pw[name])
+        kern[key] = {"kernel": name.split("(")[0].replace("void ", ""),
+                     "dispatches": len(pf[name]),
+                     "fetch_kib_per_dispatch": round(f, 1), "write_kib_per_dispatch": round(wr, 1),
+                     "fetch_bytes_per_launch": round(f * 1024 * ff),
+                     "write_bytes_per_launch": round(wr * 1024 * wf),
+                     "bytes_per_launch": round(f * 1024 * ff + wr * 1024 * wf)}
+    t = {"source_hash": kernel_source_hash(),
+         "workload": "stuff7b (16 prompts, 102,400 tokens, Hq=32, Hkv=8, d=128; 128 decode steps)",
+         "calibration": {"copy_bytes": 1 << 30, "copy_fetch_kib": cf, "copy_write_kib": cw,
+                         "fetch_factor": round(ff, 4), "write_factor": round(wf, 4)},
+         "commands": [c.format(d=prof_dir.rstrip("/")) for c in TRAFFIC_COMMANDS]
+                     + [f"python3 bench.py --traffic-summary {prof_dir}"],
+         "kernels": kern}
+    with open(out_path, "w") as f:
+        json.dump(t, f, indent=1)
+    return t
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawTextHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -1003,7 +1077,13 @@ def main():
                     help="only the hardware ceiling probes (page reads, stream read, MFMA loop)")
     ap.add_argument("--no-clocks", action="store_true",
                     help="do not query amd-smi for the clocks (skipped under rocprofv3 anyway)")
+    ap.add_argument("--traffic-summary", metavar="PROF_DIR",
+                    help="no GPU: write profiles/traffic.json from the csv of the counter runs")
     args = ap.parse_args()
+    if args.traffic_summary:
+        t = traffic_summary(args.traffic_summary, os.path.join(PROFILES, "traffic.json"))
+        print(json.dumps(t, indent=1))
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU: this build has no multi-GPU path "
               "(sequences shard across GPUs with no exchange; see DESIGN.md). "
@@ -1068,11 +1148,12 @@ def main():
     dec_bytes_avg = sum(db) / nsteps
 
     rl_pf = roofline("mfma", tflops, PEAK_BF16_TFLOPS, "TFLOP/s",
-                     traffic=stored_traffic("prefill_varlen_kernel"),
+                     traffic=stored_traffic("prefill_varlen_kernel<128>"),
                      kernel="prefill_varlen_kernel<128>")
+    dec_kernel = decode_kernel_name(len(st["lens"]), w.hkv)
     rl_dec = roofline("hbm", dec_gbs, PEAK_HBM_GBS, "GB/s",
-                      traffic=stored_traffic("paged_kernel"),
-                      kernel="paged_decode_kernel<128> (rag_attn_decode_paged)")
+                      traffic=stored_traffic(dec_kernel),
+                      kernel=f"{dec_kernel} (rag_attn_decode_paged)")
     dominant = rl_dec if dec_total > pf_med else rl_pf
 
     res = {

@@ -110,10 +110,14 @@ int32_t resolve_splits(int32_t num_decode, int32_t hkv, int32_t max_blocks, int3
 int32_t balanced_units(int32_t num_decode, int32_t hkv, int32_t max_blocks, int32_t requested) {
   // (the kernel plans over at most 4 x 64 rows, which this bound implies)
   if (requested > 0 || num_decode <= 0 || (int64_t)num_decode * hkv >= kTargetUnits) return 0;
-  const int32_t units = std::min<int32_t>(kMaxSplits, (kTargetUnits + hkv - 1) / hkv);
+  // ... and no more units than pages / kMinPagesPerUnit (what the kernel uses)
+  const int64_t pages = (int64_t)num_decode * std::max(max_blocks, 1);
+  const int64_t units = std::min<int64_t>({kMaxSplits, (kTargetUnits + hkv - 1) / hkv,
+                                           pages / kMinPagesPerUnit});
+  if (units <= 1) return 0;
   // the kernel's page arithmetic is 32-bit
-  if ((int64_t)num_decode * std::max(max_blocks, 1) * (units + 1) >= ((int64_t)1 << 31)) return 0;
-  return units;
+  if (pages * (units + 1) >= ((int64_t)1 << 31)) return 0;
+  return (int32_t)units;
 }
 
 // Partial-result slots per decode row: the most pieces either policy cuts a

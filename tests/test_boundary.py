@@ -236,16 +236,26 @@ def test_split_policy():
     assert ns(2560, 8, 40, 16, 1) == 1
     assert binding.rag_attn_decode_workspace_size(2560, 32, 8, 128, 40, 16, 1) == 0
     for nd, hkv, mb in [(16, 8, 653), (4, 8, 2260), (320, 8, 40), (256, 8, 2048), (1, 2, 19),
-                        (1, 1, 1), (3, 4, 7)]:
+                        (1, 1, 1), (3, 4, 7), (30, 8, 600)]:
         n = ns(nd, hkv, mb)
-        assert 1 <= n <= mb
-        pps = -(-mb // n)
-        assert -(-mb // pps) == n, "every split of the longest sequence is non-empty"
+        assert 1 <= n <= 64
+        if nd * hkv < 256:
+            # balanced units: at most one per 16 pages of all rows
+            assert n <= max(1, nd * mb // 16) or n <= mb
+        else:
+            assert n <= mb
+            pps = -(-mb // n)
+            assert -(-mb // pps) == n, "every split of the longest sequence is non-empty"
         ws = binding.rag_attn_decode_workspace_size(nd, hkv * 4, hkv, 128, mb)
         if n == 1:
             assert ws == 0
         else:
             assert ws >= nd * hkv * 4 * n * 129 * 4
+    # uniform splits when a count is requested: every split of the longest row non-empty
+    for nd, hkv, mb, req in [(16, 8, 653, 3), (1, 2, 19, 5), (2, 1, 40, 64)]:
+        n = ns(nd, hkv, mb, 16, req)
+        pps = -(-mb // n)
+        assert n <= mb and -(-mb // pps) == n
     # requested counts are honoured up to one split per block
     assert ns(16, 8, 653, 16, 7) == 7
     assert ns(16, 8, 5, 16, 64) == 5

@@ -6,6 +6,7 @@ import pytest
 import torch
 
 import gpu_support as G
+from paper_2412_10543_amd import binding
 from paper_2412_10543_amd.workloads import normal_bf16, paged_pool
 
 pytestmark = pytest.mark.gpu
@@ -104,6 +105,27 @@ def test_decode_balanced_units_many_rows(orc, seed):
     G.assert_parity(o, G.oracle_paged(orc, q, pool, G.scale_for(128)), "balanced")
     o2 = G.gpu_paged(q, pool, 32, 8, 128, G.scale_for(128), num_splits=2)
     assert float((o.float() - o2.float()).abs().max()) < 1e-2
+
+
+def test_decode_split_merge_repeatable(orc):
+    """The in-kernel split merge relies on completed device-coherent stores
+    and a device-scope arrival count: 64 calls with 16 splits (and with the
+    automatic policy) must give bit-identical outputs, and the result the
+    oracle's."""
+    q, pool = G.decode_case([4000, 900, 7000, 33], 32, 8, 128, seed=77)
+    for splits in (16, 0):
+        ws = G.workspace_for(4, 32, 8, 128, pool.block_tables.shape[1], splits)
+        kl = G.to_dev_i32(pool.kv_lens)
+        outs = []
+        for _ in range(64):
+            o = torch.empty_like(q)
+            binding.rag_attn_decode_paged(q, pool.k_cache, pool.v_cache, o, pool.block_tables, kl,
+                                          G.scale_for(128), num_splits=splits, workspace=ws)
+            outs.append(o)
+        torch.cuda.synchronize()
+        for o in outs[1:]:
+            assert torch.equal(o.view(torch.int16), outs[0].view(torch.int16)), splits
+        G.assert_parity(outs[0], G.oracle_paged(orc, q, pool, G.scale_for(128)), f"splits {splits}")
 
 
 def test_decode_peaky(orc):
