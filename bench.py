@@ -900,8 +900,11 @@ def ceilings(torch, dev, reps=5, clocks=True):
     with the probes of libceiling_probes.so (HIP events around one launch,
     median of `reps`): random 4 KB page reads (decode's access pattern; two
     disjoint 512 MB page sets of an 8 GB pool alternate, so neither is found
-    in the 256 MB Infinity Cache), a contiguous 4 GB read, and a
-    dependency-free bf16 MFMA loop."""
+    in the 256 MB Infinity Cache), a contiguous 4 GB read, a
+    dependency-free bf16 MFMA loop, the prefill kernel's steady 32-key slot
+    on LDS-resident tiles, and that slot's MFMA + softmax instruction mix with
+    register operands.  Slot rates count 4 * d FLOP per query-key pair, as
+    the prefill's algorithmic FLOPs do."""
     import ctypes
 
     import numpy as np
@@ -912,6 +915,8 @@ def ceilings(torch, dev, reps=5, clocks=True):
     L.rag_probe_page_read.argtypes = [vp, vp, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, vp, vp]
     L.rag_probe_stream_read.argtypes = [vp, ctypes.c_int64, ctypes.c_int32, vp, vp]
     L.rag_probe_mfma_loop.argtypes = [ctypes.c_int32, ctypes.c_int32, vp, vp]
+    L.rag_probe_attn_slot.argtypes = [ctypes.c_int32, ctypes.c_int32, vp, vp]
+    L.rag_probe_softmax_mfma.argtypes = [ctypes.c_int32, ctypes.c_int32, vp, vp]
     stream = torch.cuda.current_stream().cuda_stream
     sink = torch.zeros(1 << 16, dtype=torch.int32, device=dev)
 
@@ -971,6 +976,13 @@ def ceilings(torch, dev, reps=5, clocks=True):
         mfma[f"wg{wg}_waves_per_simd{wg // 128}"] = round(flops / ms / 1e9, 1)
     out["mfma_bf16_loop_tflops"] = mfma
     out["mfma_bf16_loop_best_tflops"] = max(mfma.values())
+    # 32 rows x 32 keys x 4 x 128 FLOP per slot and wave, two slots per iteration
+    slot_flops = 32 * 32 * 4 * 128
+    for key, fn in (("attn_slot_lds_tflops", L.rag_probe_attn_slot),
+                    ("softmax_mfma_mix_tflops", L.rag_probe_softmax_mfma)):
+        iters = 4000
+        ms = timed(lambda fn=fn: fn(iters, 256, sink.data_ptr(), stream))
+        out[key] = round(256 * 8 * 2 * iters * slot_flops / ms / 1e9, 1)
     if clocks:
         # the shader clock while the MFMA loop runs (about 2 s of launches)
         sampler = ClockSampler(delay=1.0)
@@ -1074,7 +1086,8 @@ def main():
                     help="only run this workload's packed prefill --reps times (for counter runs)")
     ap.add_argument("--reps", type=int, default=2)
     ap.add_argument("--ceilings", action="store_true",
-                    help="only the hardware ceiling probes (page reads, stream read, MFMA loop)")
+                    help="only the hardware ceiling probes (page reads, stream read, MFMA loop, "
+                         "attention slot, softmax-MFMA mix)")
     ap.add_argument("--no-clocks", action="store_true",
                     help="do not query amd-smi for the clocks (skipped under rocprofv3 anyway)")
     ap.add_argument("--traffic-summary", metavar="PROF_DIR",

@@ -39,6 +39,21 @@ int rag_probe_stream_read(const void *buf, int64_t bytes, int32_t workgroups,
 int rag_probe_mfma_loop(int32_t iters, int32_t workgroups, void *sink,
                         hipStream_t stream);
 
+/* `workgroups` eight-wave workgroups, each with two 32 KB LDS stages holding
+ * a 64-key K/V tile (d = 128, filled once): every wave runs the prefill
+ * kernel's steady slot (32 query rows x 32 keys: QK^T and PV MFMAs, online
+ * softmax, LDS operand reads) 2 * iters times, with a workgroup barrier every
+ * two slots and no copies.  524288 FLOP per slot and wave (4 x 128 per
+ * query-key pair). */
+int rag_probe_attn_slot(int32_t iters, int32_t workgroups, void *sink,
+                        hipStream_t stream);
+
+/* The same instruction mix as rag_probe_attn_slot with K/V operands in
+ * registers (no LDS): 2 * iters slots of 16 MFMAs and the softmax vector work of
+ * 32 x 32 scores per wave. */
+int rag_probe_softmax_mfma(int32_t iters, int32_t workgroups, void *sink,
+                           hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -6,13 +6,22 @@
 //     16-byte loads -- the access pattern of paged decode;
 //   * stream read: one large contiguous buffer, 16-byte loads;
 //   * MFMA loop: v_mfma_f32_32x32x16_bf16 with independent accumulators, no
-//     memory traffic -- the practical bf16 matrix rate.
+//     memory traffic -- the practical bf16 matrix rate;
+//   * attention slot: the prefill kernel's own steady 32-key slot (pf_full_slot:
+//     QK^T and PV MFMAs, the exp2/FMA/pack/sum vector work of the online
+//     softmax, the LDS operand reads) run over and over on two LDS-resident
+//     K/V tiles with the per-tile barrier, no copies -- the rate of the inner
+//     loop itself;
+//   * softmax-MFMA mix: the same MFMA and vector instructions in the same
+//     order with the K/V operands in registers (no LDS) -- the rate the
+//     instruction mix allows on the matrix core and vector ALU alone.
 // Each workgroup writes one value derived from what it read or computed, so
 // nothing is optimised away.  Declared in include/ceiling_probes.h.
 #include <hip/hip_runtime.h>
 
 #include "ceiling_probes.h"
 #include "common.h"
+#include "prefill_tile.h"
 
 namespace rag {
 namespace {
@@ -83,6 +92,156 @@ __global__ __launch_bounds__(512, 2) void probe_mfma_kernel(int iters, float* __
   if (s == 1.2345e-30f) out[blockIdx.x] = s;
 }
 
+// Per-wave Q fragments and K/V values of the slot probes: small, so every
+// block's weights stay near 1 and the exact path runs only at the first block.
+__device__ __forceinline__ bf16x8 probe_frag(int lane, int salt) {
+  bf16x8 f;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) f[i] = (__bf16)(0.01f * (float)(((lane + 3 * i + salt) % 17) - 8));
+  return f;
+}
+
+// Eight waves (two per SIMD), two 64-key K/V stages filled once; each
+// iteration is one tile: slot 2t (K of stage 0, keys 32-63; V of stage 1,
+// keys 32-63), the workgroup barrier, slot 2t+1 (K of stage 1, keys 0-31; V
+// of stage 0, keys 0-31) -- the steady step of prefill_varlen_kernel without
+// its copies.  32 rows x 32 keys x 4 x 128 FLOP per slot and wave.
+__global__ __launch_bounds__(512, 2) void probe_attn_slot_kernel(int iters,
+                                                                 float* __restrict__ out) {
+  constexpr int D = 128;
+  using Lay = ChunkLayout<D>;
+  __shared__ __attribute__((aligned(16))) bf16_t s0[Lay::kElemsTile];
+  __shared__ __attribute__((aligned(16))) bf16_t s1[Lay::kElemsTile];
+  for (int i = threadIdx.x; i < Lay::kElemsTile; i += blockDim.x) {
+    s0[i] = __builtin_bit_cast(bf16_t, (__bf16)(0.01f * (float)((i % 23) - 11)));
+    s1[i] = __builtin_bit_cast(bf16_t, (__bf16)(0.01f * (float)((i % 19) - 9)));
+  }
+  __syncthreads();
+  const int lane = threadIdx.x & 63;
+  const Lay lay;
+  PfState<D> st;
+  pf_reset(st);
+#pragma unroll
+  for (int ks = 0; ks < D / 16; ++ks) st.qf[ks] = probe_frag(lane, ks);
+  const float c = 0.08838834764831845f * kLog2e;
+  f32x16 sE = pf_qk<D, 0>(st, lay, s0), sO = {};
+  bf16x8 pE[2] = {}, pO[2] = {};
+  float sum = pf_reref(st, sE, c, pE);
+  st.l += sum;
+  for (int it = 0; it < iters; ++it) {
+    sum = pf_full_slot<D, 1, 1>(st, lay, s0, s1, sE, sO, pE, pO, c, -st.m_used * c);
+    if (__builtin_expect(wave_any(!(sum <= kPfSumBound)), 0)) sum = pf_reref(st, sE, c, pE);
+    st.l += sum;
+    pf_barrier();
+    sum = pf_full_slot<D, 0, 0>(st, lay, s1, s0, sO, sE, pO, pE, c, -st.m_used * c);
+    if (__builtin_expect(wave_any(!(sum <= kPfSumBound)), 0)) sum = pf_reref(st, sO, c, pO);
+    st.l += sum;
+  }
+  float r = st.l;
+#pragma unroll
+  for (int dt = 0; dt < D / 32; ++dt)
+#pragma unroll
+    for (int j = 0; j < 16; ++j) r += st.oacc[dt][j];
+  if (r == 1.2345e-30f) out[blockIdx.x] = r;
+}
+
+// The slot's MFMA and vector instructions in pf_full_slot's order, K and V
+// operands from registers: per step one QK^T MFMA, the exponent arguments of
+// the next step's scores, two exp2, the bf16 packing and row sum of the step
+// before, one PV MFMA.  Two slots per iteration with the score and weight
+// registers trading roles, as in the prefill loop (no copies).
+struct ProbeRegs {
+  bf16x8 qf[8], ka[8], va[8];
+  f32x16 oacc[4];
+  float l;
+};
+
+__device__ __forceinline__ void probe_reg_slot(ProbeRegs& r, const f32x16& s_cur, f32x16& s_next,
+                                               bf16x8 (&p_cur)[2], const bf16x8 (&p_prev)[2],
+                                               float c, float nm) {
+  constexpr int kSteps = 8, kPer = 2;
+#pragma unroll
+  for (int i = 0; i < kSteps; ++i) asm volatile("" : "+v"(r.ka[i]), "+v"(r.va[i]));
+  float x[16], w[16];
+  bf16x2 pr[8];
+  float sum = 0.f;
+  auto arg = [&](int i) {
+#pragma unroll
+    for (int u = 0; u < kPer; ++u) {
+      x[i * kPer + u] = fmaf(s_cur[i * kPer + u], c, nm);
+      asm volatile("" : "+v"(x[i * kPer + u]));
+    }
+  };
+  auto expo = [&](int i) {
+#pragma unroll
+    for (int u = 0; u < kPer; ++u) {
+      w[i * kPer + u] = fast_exp2(x[i * kPer + u]);
+      asm volatile("" : "+v"(w[i * kPer + u]));
+    }
+  };
+  auto pack = [&](int i) {
+#pragma unroll
+    for (int u = 0; u < kPer; u += 2) {
+      const int e = i * kPer + u;
+      f32x2 pw = {w[e], w[e + 1]};
+      pr[e / 2] = __builtin_convertvector(pw, bf16x2);
+      asm volatile("" : "+v"(pr[e / 2]));
+      sum += w[e];
+      sum += w[e + 1];
+    }
+    asm volatile("" : "+v"(sum));
+  };
+  arg(0);
+  f32x16 acc = {};
+#pragma unroll
+  for (int i = 0; i < kSteps; ++i) {
+    __builtin_amdgcn_sched_barrier(0);
+    acc = mfma32(r.ka[i], r.qf[i], acc);
+    if (i + 1 < kSteps) arg(i + 1);
+    expo(i);
+    if (i >= 1) pack(i - 1);
+    r.oacc[i % 4] = mfma32(r.va[i], p_prev[i / 4], r.oacc[i % 4]);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  pack(kSteps - 1);
+  s_next = acc;
+#pragma unroll
+  for (int s2 = 0; s2 < 2; ++s2)
+    p_cur[s2] = __builtin_shufflevector(
+        __builtin_shufflevector(pr[4 * s2], pr[4 * s2 + 1], 0, 1, 2, 3),
+        __builtin_shufflevector(pr[4 * s2 + 2], pr[4 * s2 + 3], 0, 1, 2, 3), 0, 1, 2, 3, 4,
+        5, 6, 7);
+  r.l += sum;
+}
+
+__global__ __launch_bounds__(512, 2) void probe_softmax_mfma_kernel(int iters,
+                                                                    float* __restrict__ out) {
+  const int lane = threadIdx.x & 63;
+  ProbeRegs r;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    r.qf[i] = probe_frag(lane, i);
+    r.ka[i] = probe_frag(lane, 11 + i);
+    r.va[i] = probe_frag(lane, 29 + i);
+  }
+#pragma unroll
+  for (int dt = 0; dt < 4; ++dt) r.oacc[dt] = f32x16{};
+  r.l = 0.f;
+  f32x16 sE = {}, sO = {};
+  bf16x8 pE[2] = {}, pO[2] = {};
+  const float c = 0.08838834764831845f * kLog2e, nm = -0.5f;
+  for (int it = 0; it < iters; ++it) {
+    probe_reg_slot(r, sE, sO, pE, pO, c, nm);
+    probe_reg_slot(r, sO, sE, pO, pE, c, nm);
+  }
+  float v = r.l;
+#pragma unroll
+  for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+    for (int j = 0; j < 16; ++j) v += r.oacc[dt][j];
+  if (v == 1.2345e-30f) out[blockIdx.x] = v;
+}
+
 }  // namespace
 }  // namespace rag
 
@@ -109,6 +268,20 @@ int rag_probe_mfma_loop(int32_t iters, int32_t workgroups, void* sink, hipStream
   if (!sink || iters < 0 || workgroups <= 0) return -1;
   hipLaunchKernelGGL(rag::probe_mfma_kernel, dim3(workgroups), dim3(512), 0, stream, iters,
                      (float*)sink);
+  return hipGetLastError() == hipSuccess ? 0 : -4;
+}
+
+int rag_probe_attn_slot(int32_t iters, int32_t workgroups, void* sink, hipStream_t stream) {
+  if (!sink || iters < 0 || workgroups <= 0) return -1;
+  hipLaunchKernelGGL(rag::probe_attn_slot_kernel, dim3(workgroups), dim3(512), 0, stream, iters,
+                     (float*)sink);
+  return hipGetLastError() == hipSuccess ? 0 : -4;
+}
+
+int rag_probe_softmax_mfma(int32_t iters, int32_t workgroups, void* sink, hipStream_t stream) {
+  if (!sink || iters < 0 || workgroups <= 0) return -1;
+  hipLaunchKernelGGL(rag::probe_softmax_mfma_kernel, dim3(workgroups), dim3(512), 0, stream,
+                     iters, (float*)sink);
   return hipGetLastError() == hipSuccess ? 0 : -4;
 }
 
