@@ -574,7 +574,7 @@ def bench_phase_awq(torch, dev, reps, batches=(16, 8192), graph=True):
         for M in batches:
             x = p.x[:M]
             y = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
-            ws = torch.empty(max(binding.rag_awq_workspace_size(M, N, K), 1), dtype=torch.uint8,
+            ws = torch.zeros(max(binding.rag_awq_workspace_size(M, N, K), 1), dtype=torch.uint8,
                              device=dev)
             for _ in range(WARMUP_REPS):
                 binding.rag_awq_gemm(x, qw, sc, z, y, ws)

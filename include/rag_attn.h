@@ -461,14 +461,15 @@ rag_status rag_device_free_memory(size_t *free_bytes, size_t *total_bytes);
 rag_status rag_awq_pack_weights(const uint8_t *q, int32_t K, int32_t N,
                                 int32_t group_size, int32_t *packed);
 
-/* Bytes of workspace rag_awq_gemm needs (0 for M == 0 or invalid shapes).
- * Library-internal layout: the group sums of x [K / 128, M] (each as three
- * bf16 pieces in 16 bytes), then, when the output tiles are too few to fill
- * the GPU, fp32 partial outputs [splits, M, N] of a split over the groups
- * (added in a fixed order, so results do not depend on timing), then, for
- * M <= 64, a group-major copy of x with M padded to 16, 32 or 64 rows and,
- * with a split, one arrival counter per column block (the call zeroes them
- * itself). */
+/* Bytes of workspace rag_awq_gemm needs (0 for M == 0, invalid shapes, or
+ * a small batch that needs none).  Library-internal layout.  M > 64: the
+ * group sums of x [K / 128, M] (each as three bf16 pieces in 16 bytes), then,
+ * when the output tiles are too few to fill the GPU, fp32 partial outputs
+ * [splits, M, N] of a split over the groups.  M <= 64, when the groups are
+ * split over workgroups (long K, or too few column blocks to fill the GPU):
+ * one arrival counter per column block, then fp32 partial outputs
+ * [splits, M, N].  Partials are added in a fixed order, so results do not
+ * depend on timing. */
 size_t rag_awq_workspace_size(int32_t M, int32_t N, int32_t K,
                               int32_t group_size);
 
@@ -479,8 +480,10 @@ size_t rag_awq_workspace_size(int32_t M, int32_t N, int32_t K,
  *   zeros    device uint8 [K / 128, N], each 0..15
  *   y        device bf16 [M, N]; output, written in full
  *   workspace  device, >= rag_awq_workspace_size(M, N, K, group_size) bytes,
- *            256-byte aligned; no state is kept in it between calls.
- *            Overlapping calls must not share it.
+ *            256-byte aligned, zero-filled once before its first use: for
+ *            small batches split over the weight groups it starts with one
+ *            arrival counter per column block, which every call leaves at
+ *            zero again.  Overlapping calls must not share it.
  * Returns RAG_OK (M == 0 is a no-op; x and y may then be NULL),
  * RAG_ERR_INVALID_ARG (null pointer, a pointer not 16-byte aligned, negative
  * M, N or K not positive), RAG_ERR_UNSUPPORTED (group_size not 128, K or N not a multiple of

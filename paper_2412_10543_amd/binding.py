@@ -414,8 +414,8 @@ def rag_awq_gemm(x, qweight, scales, zeros, y, workspace, group_size: int = 128,
                  stream=None) -> None:
     """x [M, K] bf16; qweight int32 [K/128, N, 16] (rag_awq_pack_weights);
     scales bf16 [K/128, N]; zeros uint8 [K/128, N]; y [M, N] bf16 output;
-    workspace a GPU uint8 tensor of rag_awq_workspace_size bytes (no
-    initialisation needed)."""
+    workspace a GPU uint8 tensor of rag_awq_workspace_size bytes, zero-filled
+    once before its first use (every call leaves its counters zero again)."""
     _need(x, torch.bfloat16, "x", 2)
     _need(qweight, torch.int32, "qweight", 3)
     _need(scales, torch.bfloat16, "scales", 2)

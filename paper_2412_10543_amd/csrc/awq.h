@@ -23,12 +23,12 @@ struct AwqPlan {
   bool large;                   // M > 64: LDS-staged 128 x 512 tiles
   int groups, splits, groups_per_split;
   int tiles_m, tiles_n, tiles_per_xcd;
-  int m_pad;                    // small batches: rows padded to 16, 32 or 64
+  int sm_mb;                    // small batches: 16-row blocks (1, 2 or 4)
   int sm_nb;                    // small batches: 16-column blocks per workgroup
   int64_t tiles;
-  size_t sp_bytes, part_bytes;  // group-sum pieces, split partials
-  size_t xr_bytes;              // small batches: group-major copy of X
+  size_t sp_bytes, part_bytes;  // large batches: group-sum pieces; split partials
   size_t counter_bytes;         // small batches split over groups: arrival counters
+                                // (at the workspace's start)
 };
 
 AwqPlan awq_plan(int M, int N, int K);

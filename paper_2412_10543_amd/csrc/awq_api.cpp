@@ -39,7 +39,7 @@ extern "C" {
 size_t rag_awq_workspace_size(int32_t M, int32_t N, int32_t K, int32_t group_size) {
   if (check_shape("awq workspace", M, N, K, group_size) != RAG_OK || M == 0) return 0;
   const rag::AwqPlan p = rag::awq_plan(M, N, K);
-  return p.sp_bytes + p.part_bytes + p.xr_bytes + p.counter_bytes;
+  return p.sp_bytes + p.part_bytes + p.counter_bytes;
 }
 
 rag_status rag_awq_pack_weights(const uint8_t* q, int32_t K, int32_t N, int32_t group_size,

@@ -8,12 +8,14 @@
 // bf16 operands with one shift and one and-or.  For group g,
 //     sum_k X[m, k] W[k, n] = s[g, n] * (P[m, n] - (128 + z[g, n]) * S[g, m]),
 //     P = sum_k X[m, k] (128 + q[k, n]),   S[g, m] = sum of X[m, k] over g.
-// A pre-pass computes S in fp32 and stores it as three bf16 pieces
-// S1 + S2 + S3 = S (exact: 24 bits in 3 x 8).  Both kernels fold the
+// Large batches: a pre-pass computes S in fp32 and stores it as three bf16
+// pieces S1 + S2 + S3 = S (exact: 24 bits in 3 x 8), and the kernel folds the
 // zero-point term into the matrix cores as one more MFMA per group (A = the
-// pieces, B = -(128 + z), which bf16 holds exactly as bits 0xC300 | z); the
-// scale is then one fp32 FMA per output element and group (small batches) or
-// a running rescale of the accumulators (large batches, see there).
+// pieces, B = -(128 + z), which bf16 holds exactly as bits 0xC300 | z), with a
+// running rescale of the accumulators for the scale (see there).  Small
+// batches need no pre-pass: the kernel stages its slice of X in LDS and forms
+// S with the matrix cores (X times a ones operand), then applies zero point
+// and scale with two fp32 FMAs per output element and group.
 //
 // Packed weight layout (rag_awq_pack_weights): int32 [K/128][N][16].  The
 // 16 words of (group g, column n) are 64 contiguous bytes; word
@@ -24,6 +26,8 @@
 // are words 8h .. 8h+7 (step t at 8h + 4(t&1) + t/2); a 16x16x32 lane
 // (column, quarter qq) needs the octets 4t + qq of k-steps t = 0..3, words
 // 8(qq&1) + 4(qq>>1) .. +3.
+#include <cstdlib>
+
 #include "common.h"
 #include "awq.h"
 
@@ -33,39 +37,20 @@ constexpr int kAwqGroup = 128;
 constexpr int kAwqCus = 256;     // MI355X compute units
 
 // S[g, m] = sum over the group of X[m, k] (fp32), stored as bf16 pieces
-// [S1, S2, S3, 0, 0, 0, 0, 0] (16 bytes per (g, m)).  For small batches (xr
-// non-null) the same pass also writes X group-major in the order the
-// small-batch kernel's 16x16x32 A operands are read, xr[g][b][t][q][r] = the
-// 8 values X[16 b + r][128 g + 32 t + 8 q ..], rows past M as zeros: each of
-// that kernel's activation loads is then 1 KB contiguous instead of 16 rows K
-// apart (which all fall into the same cache sets).  It also zeroes the
-// arrival counters of the small-batch kernel of the same call.  16 lanes share one
-// (g, m): lane c loads the 16-byte chunk c of the group's row (consecutive
-// lanes, consecutive chunks) and the 16 partial sums are added with lane
-// shuffles in a fixed order.
+// [S1, S2, S3, 0, 0, 0, 0, 0] (16 bytes per (g, m)), for the large-batch
+// kernel.  16 lanes share one (g, m): lane c loads the 16-byte chunk c of the
+// group's row (consecutive lanes, consecutive chunks) and the 16 partial sums
+// are added with lane shuffles in a fixed order.
 __global__ __launch_bounds__(256) void awq_group_sums_kernel(const bf16_t* __restrict__ x,
-                                                             bf16_t* __restrict__ sp,
-                                                             bf16_t* __restrict__ xr,
-                                                             int* __restrict__ counters,
-                                                             int n_counters, int M, int m_pad,
+                                                             bf16_t* __restrict__ sp, int M,
                                                              int K) {
   const int groups = K / kAwqGroup;
-  const int rows = xr ? m_pad : M;
   const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (tid < n_counters) counters[tid] = 0;        // the small-batch kernel's arrivals
   const int64_t i = tid >> 4;
   const int c = threadIdx.x & 15;
-  if (i >= (int64_t)groups * rows) return;        // whole 16-lane groups
-  const int g = (int)(i / rows), m = (int)(i % rows);
-  u32x4 raw = {0, 0, 0, 0};
-  if (m < M) raw = load16(x + (size_t)m * K + (size_t)g * kAwqGroup + 8 * c);
-  if (xr) {
-    // chunk c = 4 t + q of row m
-    bf16_t* dst = xr + ((size_t)(g * (m_pad / 16) + m / 16) * 4 * 64 +
-                        (size_t)((c >> 2) * 64 + (c & 3) * 16 + (m % 16))) * 8;
-    *reinterpret_cast<u32x4*>(dst) = raw;
-  }
-  if (m >= M) return;
+  if (i >= (int64_t)groups * M) return;           // whole 16-lane groups
+  const int g = (int)(i / M), m = (int)(i % M);
+  const u32x4 raw = load16(x + (size_t)m * K + (size_t)g * kAwqGroup + 8 * c);
   const bf16x8 v = as_bf16x8(raw);
   float acc = 0.f;
 #pragma unroll
@@ -439,55 +424,80 @@ __global__ __launch_bounds__(awq_lg::kThreads) void awq_gemm_lg_kernel(
 // Small batches (M <= 64), where streaming the codes from HBM is the cost.
 // 16x16x32 MFMAs (16 rows per block: no padding rows for a decode batch of
 // 16), one workgroup of W waves per 16 NB output columns (NB blocks of 16
-// columns, which share each activation load); wave w takes the groups
-// [w R, w R + R), R = ceil(G / W), and streams them through a ring of
-// register slots: the code words (16 contiguous bytes per lane and column
-// block), activations, scales, zero points and group-sum pieces of group
-// i + depth are requested as soon as group i has taken its slot.  Per group
-// and block: the zero-point MFMA (group-sum pieces times -(128 + z), bf16
-// exact) opens the chain, 4 k-steps follow, and y += s * P in fp32.  The
-// waves' sums are added in LDS in wave order.
+// columns, which share each activation read) and split of the groups.
+//
+// X.  Each wave first copies its groups' X (16-row blocks of 16 x 128,
+// 4 KB each) into LDS with direct global -> LDS copies: each copy
+// instruction moves four whole rows of a block (4 x 256 contiguous bytes, so
+// no cache line is fetched twice), lane l of instruction i landing at
+// position p = 64 i + l, which holds the 16-byte chunk j = (p % 16) ^ r of row
+// r = p / 16.  The A operand of k-step t (lane (c, qq): row c, chunk 4 t + qq)
+// is then one 16-byte LDS read at position 16 c + ((4 t + qq) ^ c): the 16
+// lanes of a read group hit 16 different bank groups.  Rows past M read row
+// M - 1 (their outputs are not stored).
+//
+// Codes.  Wave w takes the groups [w R, w R + R), R = ceil(G / W), and
+// streams them through a ring of register slots: the code words (16
+// contiguous bytes per lane and column block), scales and zero points of
+// group i + depth are requested as soon as group i has taken its slot.
+//
+// Per group and 16-row block: P = sum_t X_t B_t over the 4 k-steps (B = the
+// codes as bf16 128 + q), S = sum_t X_t 1 (a ones operand: lane (c, qq) gets
+// the group sums of rows 4 qq .. 4 qq + 3, the rows of its outputs), and
+// y += s (P - (128 + z) S) in fp32.  The waves' sums are added in LDS in wave
+// order.  With the groups split over workgroups, fp32 partials go out with
+// device-coherent stores and the last workgroup of a column block to arrive
+// (device-scope counter) adds them in split order and resets the counter.
 // ---------------------------------------------------------------------------
+namespace awq_sm {
+constexpr int kXCap = 32;                        // 4 KB X blocks a workgroup can stage
+constexpr int kLds = kXCap * 4096;
+}  // namespace awq_sm
 
-// MB: 16-row blocks (M <= 16 MB).  NB: 16-column blocks per workgroup (4 for
-// M <= 16 when that still leaves one workgroup per CU, else 2).  kWaves: 8 when there are
-// fewer workgroups than CUs (more waves each keep enough loads in flight),
-// else 4.
 template <int MB, int NB, int kWaves>
 __global__ __launch_bounds__(kWaves * 64) void awq_gemm_sm_kernel(
-    const bf16_t* __restrict__ xr, const uint32_t* __restrict__ qw,
+    const bf16_t* __restrict__ x, const uint32_t* __restrict__ qw,
     const bf16_t* __restrict__ scales, const uint8_t* __restrict__ zeros,
-    const bf16_t* __restrict__ sp, bf16_t* __restrict__ y, float* __restrict__ part,
-    int* __restrict__ arrivals, int M, int N, int K, int splits) {
+    bf16_t* __restrict__ y, float* __restrict__ part, int* __restrict__ arrivals, int M, int N,
+    int K, int splits) {
+  using namespace awq_sm;
   constexpr int kCols = 16 * NB;
   constexpr int kThreads = kWaves * 64;
   constexpr int kDepth = 8 / (MB * NB) > 1 ? 8 / (MB * NB) : 1;   // ring slots (registers)
   constexpr int kOut = MB * NB * 4;                // accumulator values per lane
-  __shared__ float red[kWaves * kOut * 64];
+  static_assert(kWaves * kOut * 64 * 4 <= kLds, "wave sums fit the X region");
+  __shared__ __attribute__((aligned(16))) char lds[kLds];
   const int lane = threadIdx.x & 63, w = wave_id();
   const int c = lane & 15, qq = lane >> 4;
   const int n0 = kCols * blockIdx.x + c;           // columns n0 + 16 nb
   const int groups = K / kAwqGroup;
   const int spl = blockIdx.y;
   const int per_wg = (groups + splits - 1) / splits;
-  const int wg_end = min(groups, (spl + 1) * per_wg);
+  const int wg_g0 = spl * per_wg;
+  const int wg_end = min(groups, wg_g0 + per_wg);
   const int per_wave = (per_wg + kWaves - 1) / kWaves;
-  const int g0 = spl * per_wg + w * per_wave;
+  const int g0 = wg_g0 + w * per_wave;
   const int ng = max(0, min(per_wave, wg_end - g0));
   const uint32_t kMask = in_vgpr(0x000F000Fu), kMagic = in_vgpr(0x43004300u);
   const int wpos = 8 * (qq & 1) + 4 * (qq >> 1);   // this lane's 4 words
-  int rows[MB];
-#pragma unroll
-  for (int mb = 0; mb < MB; ++mb) rows[mb] = min(16 * mb + c, M - 1);
+
+  // ---- X of this wave's groups into LDS (each wave waits for its own) ----
+  for (int ii = 0; ii < ng * MB * 4; ++ii) {
+    const int blk = (g0 - wg_g0) * MB + (ii >> 2), part4 = ii & 3;   // (group, row block)
+    const int gl = blk / MB, mb = blk % MB;
+    const int p = 64 * part4 + lane;
+    const int r = p >> 4, j = (p & 15) ^ r;
+    const int row = min(16 * mb + r, M - 1);
+    dma16(x + (size_t)row * K + (size_t)(wg_g0 + gl) * kAwqGroup + 8 * j,
+          (bf16_t*)(lds + blk * 4096 + part4 * 1024));
+  }
 
   struct Slot {
     u32x4 wd[NB];
-    u32x4 xa[4][MB];
-    u32x4 az[MB];
     uint32_t sbits[NB], z[NB];
   };
-  // everything one group needs; raw values only (arithmetic on a loaded
-  // value here would wait for the load)
+  // everything one group needs from HBM; raw values only (arithmetic on a
+  // loaded value here would wait for the load)
   auto fetch = [&](int g, Slot& sl) {
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
@@ -496,13 +506,6 @@ __global__ __launch_bounds__(kWaves * 64) void awq_gemm_sm_kernel(
       sl.sbits[nb] = scales[col];
       sl.z[nb] = zeros[col];
     }
-#pragma unroll
-    for (int t = 0; t < 4; ++t)
-#pragma unroll
-      for (int mb = 0; mb < MB; ++mb)
-        sl.xa[t][mb] = load16(xr + ((((size_t)g * MB + mb) * 4 + t) * 64 + lane) * 8);
-#pragma unroll
-    for (int mb = 0; mb < MB; ++mb) sl.az[mb] = load16(sp + ((size_t)g * M + rows[mb]) * 8);
   };
 
   f32x4 yv[MB][NB];
@@ -510,10 +513,14 @@ __global__ __launch_bounds__(kWaves * 64) void awq_gemm_sm_kernel(
   for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) yv[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  Slot ring[kDepth];
   if (ng > 0) {
-    Slot ring[kDepth];
 #pragma unroll
     for (int d = 0; d < kDepth; ++d) fetch(g0 + min(d, ng - 1), ring[d]);
+  }
+  wait_vm<0>();                                    // this wave's X (and first codes) landed
+  if (ng > 0) {
+    const u32x4 ones = {0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u};
     const int g_last = g0 + ng - 1;
     for (int i0 = 0; i0 < ng; i0 += kDepth) {
 #pragma unroll
@@ -527,38 +534,53 @@ __global__ __launch_bounds__(kWaves * 64) void awq_gemm_sm_kernel(
         const Slot sl = ring[d];
         fetch(min(g + kDepth, g_last), ring[d]);
         __builtin_amdgcn_sched_barrier(0);
-        f32x4 p[MB][NB];
+        bf16x8 xa[4][MB];
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb) {
-          const uint32_t nz = 0xC300u | sl.z[nb];              // bf16 -(128 + z)
-          const u32x4 bzv = {nz | (nz << 16), nz, 0u, 0u};
+        for (int mb = 0; mb < MB; ++mb) {
+          const char* blk = lds + ((g - wg_g0) * MB + mb) * 4096;
 #pragma unroll
-          for (int mb = 0; mb < MB; ++mb) {
-            const u32x4 az = qq ? u32x4{0, 0, 0, 0} : sl.az[mb];
-            p[mb][nb] = mfma16(as_bf16x8(az), as_bf16x8(bzv), f32x4{0.f, 0.f, 0.f, 0.f});
-          }
+          for (int t = 0; t < 4; ++t)
+            xa[t][mb] = as_bf16x8(
+                *reinterpret_cast<const u32x4*>(blk + 16 * (16 * c + ((4 * t + qq) ^ c))));
+        }
+        f32x4 p[MB][NB], sx[MB];
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) {
+          sx[mb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int nb = 0; nb < NB; ++nb) p[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
         }
 #pragma unroll
-        for (int t = 0; t < 4; ++t)
+        for (int t = 0; t < 4; ++t) {
+          // one k-step at a time (converting every step's codes up front
+          // would need their registers all at once)
+          __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+          for (int mb = 0; mb < MB; ++mb) sx[mb] = mfma16(xa[t][mb], as_bf16x8(ones), sx[mb]);
 #pragma unroll
           for (int nb = 0; nb < NB; ++nb) {
             const bf16x8 b = codes_to_bf16(sl.wd[nb][t], kMask, kMagic);
 #pragma unroll
-            for (int mb = 0; mb < MB; ++mb) p[mb][nb] = mfma16(as_bf16x8(sl.xa[t][mb]), b, p[mb][nb]);
+            for (int mb = 0; mb < MB; ++mb) p[mb][nb] = mfma16(xa[t][mb], b, p[mb][nb]);
           }
+        }
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) {
           const float sc = bf16_to_f32(sl.sbits[nb]);
+          const float nz = -(float)(128 + (int)sl.z[nb]);
 #pragma unroll
           for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-            for (int j = 0; j < 4; ++j) yv[mb][nb][j] = fmaf(sc, p[mb][nb][j], yv[mb][nb][j]);
+            for (int j = 0; j < 4; ++j)
+              yv[mb][nb][j] = fmaf(sc, fmaf(nz, sx[mb][j], p[mb][nb][j]), yv[mb][nb][j]);
         }
       }
     }
   }
 
-  // ---- the waves' sums, added in wave order ----
+  // ---- the waves' sums, added in wave order (the X region is free) ----
+  __syncthreads();
+  float* red = reinterpret_cast<float*>(lds);
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
@@ -566,18 +588,21 @@ __global__ __launch_bounds__(kWaves * 64) void awq_gemm_sm_kernel(
 #pragma unroll
       for (int j = 0; j < 4; ++j) red[(w * kOut + (mb * NB + nb) * 4 + j) * 64 + lane] = yv[mb][nb][j];
   __syncthreads();
-  constexpr int kPer = kOut * 64 / kThreads;       // outputs per thread
+  constexpr int kPer = (kOut * 64 + kThreads - 1) / kThreads;   // outputs per thread
   float tot[kPer];
   int orow[kPer], ocol[kPer];
 #pragma unroll
   for (int e = 0; e < kPer; ++e) {
     const int idx = threadIdx.x + e * kThreads;     // (mb, nb, j, lane') of the tile
     const int l = idx & 63, j = (idx >> 6) & 3, nb = (idx >> 8) % NB, mb = (idx >> 8) / NB;
-    orow[e] = 16 * mb + 4 * (l >> 4) + j;
+    const bool have = idx < kOut * 64;
+    orow[e] = have ? 16 * mb + 4 * (l >> 4) + j : M;
     ocol[e] = kCols * blockIdx.x + 16 * nb + (l & 15);
     float acc = 0.f;
+    if (have) {
 #pragma unroll
-    for (int v = 0; v < kWaves; ++v) acc += red[v * kOut * 64 + idx];
+      for (int v = 0; v < kWaves; ++v) acc += red[v * kOut * 64 + idx];
+    }
     tot[e] = acc;
   }
   if (splits == 1) {
@@ -591,7 +616,7 @@ __global__ __launch_bounds__(kWaves * 64) void awq_gemm_sm_kernel(
   }
   // ---- groups split over workgroups: fp32 partials (device-coherent stores,
   // another XCD may add them), then the last workgroup of the column block to
-  // arrive adds them in split order ----
+  // arrive adds them in split order and leaves its counter at zero ----
   __shared__ int flag;
 #pragma unroll
   for (int e = 0; e < kPer; ++e)
@@ -603,13 +628,32 @@ __global__ __launch_bounds__(kWaves * 64) void awq_gemm_sm_kernel(
                                   __HIP_MEMORY_SCOPE_AGENT);
   __syncthreads();
   if (flag != splits - 1) return;
+  if (threadIdx.x == 0)
+    __hip_atomic_store(arrivals + blockIdx.x, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  // eight partials in flight at a time, added in split order
+  float acc[kPer];
+#pragma unroll
+  for (int e = 0; e < kPer; ++e) acc[e] = 0.f;
+  for (int s0 = 0; s0 < splits; s0 += 8) {
+    float v[kPer][8];
+#pragma unroll
+    for (int e = 0; e < kPer; ++e)
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int s2 = min(s0 + u, splits - 1);
+        const int row = min(orow[e], M - 1);
+        v[e][u] = load_coherent(part + ((size_t)s2 * M + row) * N + ocol[e]);
+      }
+#pragma unroll
+    for (int e = 0; e < kPer; ++e)
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        if (s0 + u < splits) acc[e] += v[e][u];
+  }
 #pragma unroll
   for (int e = 0; e < kPer; ++e) {
     if (orow[e] >= M) continue;
-    float acc = 0.f;
-    for (int s2 = 0; s2 < splits; ++s2)
-      acc += load_coherent(part + ((size_t)s2 * M + orow[e]) * N + ocol[e]);
-    const __bf16 o = (__bf16)acc;
+    const __bf16 o = (__bf16)acc[e];
     y[(size_t)orow[e] * N + ocol[e]] = __builtin_bit_cast(bf16_t, o);
   }
 }
@@ -626,15 +670,24 @@ __global__ __launch_bounds__(256) void awq_reduce_kernel(const float* __restrict
   y[i] = __builtin_bit_cast(bf16_t, v);
 }
 
+// RAG_AWQ_SM_NB / RAG_AWQ_SM_SPLITS (read at each call) fix the small-batch
+// column blocks per workgroup (2, 4 or 8, at most 8 / row blocks) and the split of the groups: a
+// testing and tuning knob (any choice computes the same sums; only split
+// counts change the fp32 addition order).
+static int env_int(const char* name) {
+  const char* e = std::getenv(name);
+  return (e != nullptr && e[0] != 0) ? std::atoi(e) : 0;
+}
+
 AwqPlan awq_plan(int M, int N, int K) {
   AwqPlan p{};
   p.groups = K / kAwqGroup;
   p.large = M > 64;
   const size_t up = 255;
-  p.sp_bytes = ((size_t)p.groups * M * 16 + up) & ~up;
   p.splits = 1;
   p.groups_per_split = p.groups;
   if (p.large) {
+    p.sp_bytes = ((size_t)p.groups * M * 16 + up) & ~up;
     p.tiles_m = (M + awq_lg::kBM - 1) / awq_lg::kBM;
     p.tiles_n = (N + awq_lg::kBN - 1) / awq_lg::kBN;
     p.tiles = (int64_t)p.tiles_m * p.tiles_n;
@@ -646,24 +699,42 @@ AwqPlan awq_plan(int M, int N, int K) {
       p.splits = (p.groups + p.groups_per_split - 1) / p.groups_per_split;
     }
     p.part_bytes = p.splits > 1 ? (((size_t)p.splits * M * N * sizeof(float) + up) & ~up) : 0;
-  } else {
-    p.tiles_m = 1;
-    p.sm_nb = M <= 16 && N / 64 >= kAwqCus ? 4 : 2;
-    p.tiles_n = N / (16 * p.sm_nb);
-    // fewer column blocks than CUs and a long K: split the groups too (at
-    // least 4 per workgroup), so that every CU streams codes (for short K the
-    // merge costs more than the idle CUs)
-    if (p.tiles_n < kAwqCus && p.groups >= 64)
-      p.splits = std::max(1, std::min((kAwqCus + p.tiles_n - 1) / p.tiles_n, p.groups / 4));
-    p.groups_per_split = (p.groups + p.splits - 1) / p.splits;
-    p.splits = (p.groups + p.groups_per_split - 1) / p.groups_per_split;
-    p.tiles = (int64_t)p.tiles_n * p.splits;
-    if (p.splits > 1) {
-      p.part_bytes = ((size_t)p.splits * M * N * sizeof(float) + up) & ~up;
-      p.counter_bytes = ((size_t)p.tiles_n * sizeof(int) + up) & ~up;
+    return p;
+  }
+  // Small batches: a workgroup stages X of at most kXCap 16-row blocks, so
+  // the groups are split at least groups * MB / kXCap ways, and no further:
+  // the merge of a split (coherent partial stores, arrival count, reloads)
+  // costs more than the CUs a smaller grid leaves idle (the 7B o_proj at 16
+  // rows: 6.5 us on 128 workgroups, 7.4 us split in two on 256).  The column
+  // blocks per workgroup are the fewest (2, 4, 8) for which the workgroups
+  // fit one per CU.
+  p.tiles_m = 1;
+  p.sm_mb = M <= 16 ? 1 : (M <= 32 ? 2 : 4);
+  const int min_splits = (p.groups * p.sm_mb + awq_sm::kXCap - 1) / awq_sm::kXCap;
+  const int nb_max = 8 / p.sm_mb;                  // MB * NB <= 8 (registers)
+  p.sm_nb = nb_max;
+  for (int nb : {2, 4, 8}) {
+    if (nb > nb_max || N % (16 * nb) != 0) continue;
+    if ((int64_t)(N / (16 * nb)) * min_splits <= kAwqCus) {
+      p.sm_nb = nb;
+      break;
     }
-    p.m_pad = M <= 16 ? 16 : (M <= 32 ? 32 : 64);
-    p.xr_bytes = (size_t)p.groups * p.m_pad * kAwqGroup * 2;
+  }
+  if (const int nb = env_int("RAG_AWQ_SM_NB");
+      (nb == 2 || nb == 4 || nb == 8) && nb <= nb_max && N % (16 * nb) == 0)
+    p.sm_nb = nb;
+  p.tiles_n = N / (16 * p.sm_nb);
+  int splits = min_splits;
+  if (const int sp = env_int("RAG_AWQ_SM_SPLITS"); sp > 0) splits = std::max(min_splits, sp);
+  splits = std::max(1, std::min(splits, p.groups));
+  p.groups_per_split = (p.groups + splits - 1) / splits;
+  p.splits = (p.groups + p.groups_per_split - 1) / p.groups_per_split;
+  p.tiles = (int64_t)p.tiles_n * p.splits;
+  if (p.splits > 1) {
+    // arrival counters first: zero-filled once by the caller, left zero by
+    // every call
+    p.counter_bytes = ((size_t)p.tiles_n * sizeof(int) + up) & ~up;
+    p.part_bytes = ((size_t)p.splits * M * N * sizeof(float) + up) & ~up;
   }
   return p;
 }
@@ -671,20 +742,16 @@ AwqPlan awq_plan(int M, int N, int K) {
 hipError_t launch_awq_gemm(const AwqArgs& a, hipStream_t stream) {
   const AwqPlan p = awq_plan(a.M, a.N, a.K);
   char* ws = static_cast<char*>(a.workspace);
-  bf16_t* sp = reinterpret_cast<bf16_t*>(ws);
-  float* part = reinterpret_cast<float*>(ws + p.sp_bytes);
-  bf16_t* xr = p.large ? nullptr : reinterpret_cast<bf16_t*>(ws + p.sp_bytes + p.part_bytes);
-  int* counters = reinterpret_cast<int*>(ws + p.sp_bytes + p.part_bytes + p.xr_bytes);
-  const int n_counters = (int)(p.counter_bytes / sizeof(int));
-  const int64_t nsum = std::max<int64_t>((int64_t)p.groups * (p.large ? a.M : p.m_pad) * 16,
-                                         n_counters);   // 16 lanes per row
-  hipLaunchKernelGGL(awq_group_sums_kernel, dim3((unsigned)((nsum + 255) / 256)), dim3(256), 0,
-                     stream, (const bf16_t*)a.x, sp, xr, counters, n_counters, a.M, p.m_pad, a.K);
   const bf16_t* x = (const bf16_t*)a.x;
   const uint32_t* qw = (const uint32_t*)a.qweight;
   const bf16_t* sc = (const bf16_t*)a.scales;
   bf16_t* y = (bf16_t*)a.y;
   if (p.large) {
+    bf16_t* sp = reinterpret_cast<bf16_t*>(ws);
+    float* part = reinterpret_cast<float*>(ws + p.sp_bytes);
+    const int64_t nsum = (int64_t)p.groups * a.M * 16;   // 16 lanes per row
+    hipLaunchKernelGGL(awq_group_sums_kernel, dim3((unsigned)((nsum + 255) / 256)), dim3(256), 0,
+                       stream, x, sp, a.M, a.K);
     const dim3 grid((unsigned)(p.tiles_per_xcd * kNumXcd), (unsigned)p.splits);
     if (p.splits > 1) {
       hipLaunchKernelGGL(awq_gemm_lg_kernel<true>, grid, dim3(awq_lg::kThreads), 0, stream, x, qw,
@@ -698,24 +765,23 @@ hipError_t launch_awq_gemm(const AwqArgs& a, hipStream_t stream) {
                          qw, sc, a.zeros, sp, y, part, a.M, a.N, a.K, p.groups_per_split,
                          p.tiles_m, p.tiles_n, p.tiles_per_xcd);
     }
-  } else {
-    const bool wide = p.tiles >= kAwqCus;
-    const dim3 grid((unsigned)p.tiles_n, (unsigned)p.splits), block(wide ? 256 : 512);
-    auto go = [&](auto kernel) {
-      hipLaunchKernelGGL(kernel, grid, block, 0, stream, xr, qw, sc, a.zeros, sp, y, part, counters,
-                         a.M, a.N, a.K, p.splits);
-    };
-    const int mb = a.M <= 16 ? 1 : (a.M <= 32 ? 2 : 4);
-    switch (mb * 100 + p.sm_nb * 10 + (wide ? 4 : 8)) {
-      case 124: go(awq_gemm_sm_kernel<1, 2, 4>); break;
-      case 128: go(awq_gemm_sm_kernel<1, 2, 8>); break;
-      case 144: go(awq_gemm_sm_kernel<1, 4, 4>); break;
-      case 148: go(awq_gemm_sm_kernel<1, 4, 8>); break;
-      case 224: go(awq_gemm_sm_kernel<2, 2, 4>); break;
-      case 228: go(awq_gemm_sm_kernel<2, 2, 8>); break;
-      case 424: go(awq_gemm_sm_kernel<4, 2, 4>); break;
-      default: go(awq_gemm_sm_kernel<4, 2, 8>); break;
-    }
+    return hipGetLastError();
+  }
+  if ((int64_t)p.groups_per_split * p.sm_mb > awq_sm::kXCap) return hipErrorInvalidValue;
+  int* counters = reinterpret_cast<int*>(ws);
+  float* part = reinterpret_cast<float*>(ws + p.counter_bytes);
+  const dim3 grid((unsigned)p.tiles_n, (unsigned)p.splits), block(512);
+  auto go = [&](auto kernel) {
+    hipLaunchKernelGGL(kernel, grid, block, 0, stream, x, qw, sc, a.zeros, y, part, counters,
+                       a.M, a.N, a.K, p.splits);
+  };
+  switch (p.sm_mb * 10 + p.sm_nb) {
+    case 12: go(awq_gemm_sm_kernel<1, 2, 8>); break;
+    case 14: go(awq_gemm_sm_kernel<1, 4, 8>); break;
+    case 18: go(awq_gemm_sm_kernel<1, 8, 8>); break;
+    case 22: go(awq_gemm_sm_kernel<2, 2, 8>); break;
+    case 24: go(awq_gemm_sm_kernel<2, 4, 8>); break;
+    default: go(awq_gemm_sm_kernel<4, 2, 8>); break;
   }
   return hipGetLastError();
 }

@@ -5,7 +5,9 @@ The tolerance is the one the hot path is specified to: bf16 inputs, fp32
 accumulation, max-abs error <= 2e-2 and mean-abs error <= 2e-3 against the
 fp64 oracle.
 """
+import contextlib
 import math
+import os
 
 import numpy as np
 import torch
@@ -62,6 +64,25 @@ def gpu_prefill(q, k, v, lens_q, lens_k, scale, causal=True, want_lse=True):
                                     scale, causal)
     torch.cuda.synchronize()
     return o, lse
+
+
+@contextlib.contextmanager
+def env(name, value):
+    """Sets a library knob read at each call (RAG_ATTN_PF_ITEMS,
+    RAG_AWQ_SM_NB, RAG_AWQ_SM_SPLITS, ...) for the calls inside the block;
+    None leaves it unset."""
+    old = os.environ.get(name)
+    if value is None:
+        os.environ.pop(name, None)
+    else:
+        os.environ[name] = str(value)
+    try:
+        yield
+    finally:
+        if old is None:
+            os.environ.pop(name, None)
+        else:
+            os.environ[name] = old
 
 
 def oracle_prefill(orc, q, k, v, lens_q, lens_k, scale, causal=True):

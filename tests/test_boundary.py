@@ -321,7 +321,7 @@ def _awq(**kw):
     (dict(N=200), binding.RAG_ERR_UNSUPPORTED),
     (dict(M=5_000_000), binding.RAG_ERR_UNSUPPORTED),
     (dict(ws=None), binding.RAG_ERR_WORKSPACE),
-    (dict(ws_bytes=100), binding.RAG_ERR_WORKSPACE),
+    (dict(ws_bytes=100, M=16, N=4096, K=14336), binding.RAG_ERR_WORKSPACE),
     (dict(ws=FAKE + 16), binding.RAG_ERR_INVALID_ARG),
     (dict(M=0, x=None, y=None, ws=None, ws_bytes=0), binding.RAG_OK),  # nothing to compute
     (dict(M=0, qw=None), binding.RAG_ERR_INVALID_ARG),
@@ -345,18 +345,23 @@ def test_awq_workspace_size():
     M, N, K = 200, 1024, 2048
     pieces = -(-(K // 128) * M * 16 // 256) * 256
     assert ws(M, N, K) > pieces and (ws(M, N, K) - pieces) % (M * N * 4) == 0
-    # small batches: group sums and the padded group-major x; with fewer
-    # column blocks than CUs also split partials and arrival counters
-    def pieces(M, K):
-        return -(-(K // 128) * M * 16 // 256) * 256
-    M, N, K = 16, 28672, 4096
-    assert ws(M, N, K) == pieces(M, K) + 16 * K * 2
-    M, N, K = 16, 4096, 4096
-    assert ws(M, N, K) == pieces(M, K) + 16 * K * 2
-    M, N, K = 16, 4096, 14336
-    assert ws(M, N, K) >= pieces(M, K) + 2 * M * N * 4 + 16 * K * 2 + (N // 32) * 4
-    M = 20
-    assert ws(M, N, K) >= pieces(M, K) + 2 * M * N * 4 + 32 * K * 2 + (N // 32) * 4
+    # small batches (M <= 64): nothing when a workgroup's X fits its LDS
+    # (qkv, o, gate_up of the 7B model at 16 rows); with the groups split over
+    # workgroups, counters for at least N / 128 column blocks
+    # (256-byte rounded) and whole fp32 [M, N] partial planes
+    assert ws(16, 6144, 4096) == 0 and ws(16, 28672, 4096) == 0
+
+    def split_parts(M, N, K):
+        b = ws(M, N, K)
+        counters = b % (M * N * 4)
+        return b // (M * N * 4), counters
+    # 112 groups of x (4 KB each per 16 rows) exceed a workgroup's 128 KB of
+    # LDS: at least 4 splits
+    s, c = split_parts(16, 4096, 14336)
+    assert s >= 4 and c >= 4 * (4096 // 128) and c % 256 == 0
+    s, c = split_parts(20, 4096, 14336)         # two row blocks: at least 7 splits
+    assert s >= 7 and c >= 4 * (4096 // 128)
+    assert ws(16, 4096, 4096) == 0              # 32 groups fit: no split
 
 
 def test_awq_pack_layout():

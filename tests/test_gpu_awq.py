@@ -30,12 +30,16 @@ def _device(p):
     return qw, p.scales.cuda(), torch.from_numpy(p.zeros).cuda()
 
 
-def _run(p, qw, sc, z):
+def _workspace(M, N, K):
+    return torch.zeros(max(binding.rag_awq_workspace_size(M, N, K), 1), dtype=torch.uint8,
+                       device="cuda")
+
+
+def _run(p, qw, sc, z, ws=None):
     M, K = p.x.shape
     N = p.codes.shape[1]
     y = torch.full((M, N), float("nan"), dtype=torch.bfloat16, device="cuda")
-    ws = torch.empty(max(binding.rag_awq_workspace_size(M, N, K), 1), dtype=torch.uint8,
-                     device="cuda")
+    ws = _workspace(M, N, K) if ws is None else ws
     binding.rag_awq_gemm(p.x, qw, sc, z, y, ws)
     torch.cuda.synchronize()
     return y
@@ -98,6 +102,34 @@ def test_awq_deterministic_and_extremes():
     a, b = _run(p, *dev), _run(p, *dev)
     assert torch.equal(a.view(torch.int16), b.view(torch.int16))
     _check(p, a)
+
+
+@pytest.mark.parametrize("M,N,K,nb,splits", [
+    (16, 4096, 14336, None, None),    # 112 groups: split at least 4 ways (X staged in LDS)
+    (16, 4096, 4096, None, 2),        # o_proj shape, split in two
+    (3, 1024, 2048, 8, 3),            # 8 column blocks, uneven split (16 groups / 3)
+    (40, 512, 4096, 2, 5),            # 3 row blocks (padded to 4), uneven split
+    (64, 256, 1024, 2, 8)])           # one group per workgroup
+def test_awq_small_batch_splits_reuse_workspace(M, N, K, nb, splits):
+    """Small batches split over the weight groups: the last workgroup of a
+    column block adds the fp32 partials and resets its arrival counter, so one
+    workspace, zero-filled once, serves every later call (three calls, fresh
+    inputs each time), and a repeat gives identical bits."""
+    with G_.env("RAG_AWQ_SM_NB", nb), G_.env("RAG_AWQ_SM_SPLITS", splits):
+        ws = _workspace(M, N, K)
+        first = None
+        for call in range(3):
+            p = awq_problem(M, N, K, seed=M + N + K + call, device="cuda")
+            dev = _device(p)
+            y = _run(p, *dev, ws=ws)
+            _check(p, y)
+            if call == 0:
+                first = (p, dev, y)
+        p, dev, y = first
+        assert torch.equal(_run(p, *dev, ws=ws).view(torch.int16), y.view(torch.int16))
+        # the counters (one per column block, at least N / 128 of them) are zero again
+        assert binding.rag_awq_workspace_size(M, N, K) > 0
+        assert int(ws[:4 * (N // 128)].count_nonzero()) == 0
 
 
 @pytest.mark.parametrize("M,N", [(130, 512), (20, 256)])
