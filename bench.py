@@ -242,19 +242,81 @@ def run_stuff_step(st, timer=None, plan=True, decode=True):
     # The decode launches go back to back between one pair of events: an
     # event pair around every launch would add the events' own cost to each
     # (about 2.5 us of 81).  The average launch duration is the pair's time
-    # over the number of launches (inter-launch gaps included).
-    pools = st.get("pools", [])
+    # over the number of launches (inter-launch gaps included).  With a
+    # captured graph (capture_decode) the launches are one graph replay, as a
+    # serving loop runs its per-token steps.
     if not decode:
         return
     if timer and st["decode_steps"]:
         timer.start("decode")
+    if st.get("graph") is not None:
+        st["graph"].replay()
+    else:
+        run_decode_launches(st)
+    if timer and st["decode_steps"]:
+        timer.stop("decode")
+
+
+def run_decode_launches(st):
+    """The workload's decode steps, one paged-decode launch each; KV pools
+    alternate between steps (no step finds the previous one's pages in the
+    256 MB Infinity Cache)."""
+    from paper_2412_10543_amd import binding
+    w = st["w"]
+    pools = st.get("pools", [])
     for t in range(st["decode_steps"]):
         pool = pools[t % len(pools)]
         binding.rag_attn_decode_paged(st["dq"][t], pool.k_cache, pool.v_cache, st["do"],
                                       pool.block_tables, st["kv_steps"][t], w.scale,
                                       workspace=st["ws"])
-    if timer and st["decode_steps"]:
-        timer.stop("decode")
+
+
+def capture_decode(torch, st):
+    """Captures the decode steps (the launches of run_decode_launches) in a
+    HIP graph and keeps the eager result of the last step to check every
+    replay against (check_decode_replay).  No memset or allocation is
+    recorded: the kernels leave the workspace's counters zero themselves."""
+    if not st["decode_steps"]:
+        return
+    run_decode_launches(st)
+    torch.cuda.synchronize()
+    st["do_eager"] = st["do"].clone()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(side):
+        with torch.cuda.graph(g, stream=side):
+            run_decode_launches(st)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    st["graph"] = g
+    check_decode_replay(torch, st)
+
+
+def check_decode_replay(torch, st):
+    """The last decode step's output after a replay equals the eager one, bit
+    for bit (run after the replay's events, outside the timed pair)."""
+    if st.get("graph") is None:
+        return
+    st["do"].zero_()
+    st["graph"].replay()
+    torch.cuda.synchronize()
+    if not torch.equal(st["do"].view(torch.int16), st["do_eager"].view(torch.int16)):
+        raise RuntimeError("decode graph replay differs from the eager launches")
+
+
+def eager_decode_ms(torch, st, reps=5):
+    """Median time of the decode steps launched one by one from the host."""
+    ts = []
+    for _ in range(reps):
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record()
+        run_decode_launches(st)
+        b.record()
+        torch.cuda.synchronize()
+        ts.append(a.elapsed_time(b))
+    return median(ts)
 
 
 def stuff_work(st):
@@ -294,9 +356,12 @@ def bench_phase_stuff(torch, w, dev, reps, cpu=None):
     for _ in range(WARMUP_REPS):
         run_stuff_step(st, None, plan=False)
     torch.cuda.synchronize()
+    eager_ms = eager_decode_ms(torch, st) if st["decode_steps"] else None
+    capture_decode(torch, st)
     timer = Timer(torch)
     for _ in range(reps):
         run_stuff_step(st, timer, plan=False)
+        check_decode_replay(torch, st)
     torch.cuda.synchronize()
     pf_ms = median(timer.ms("prefill"))
     dec_ms = timer.ms("decode")
@@ -306,10 +371,11 @@ def bench_phase_stuff(torch, w, dev, reps, cpu=None):
            "prefill_hbm_gbs": round(pb / pf_ms / 1e6, 1)}
     if dec_ms:
         per = st["decode_steps"]
-        tot = sum(dec_ms) / reps
+        tot = median(dec_ms)
         gbs = sum(db) / tot / 1e6
         out.update({"decode_steps": per, "decode_us_per_step": round(tot / per * 1e3, 2),
                     "decode_gbs": round(gbs, 1), "decode_frac_hbm": round(gbs / PEAK_HBM_GBS, 4),
+                    "decode_us_per_step_eager": round(eager_ms / per * 1e3, 2),
                     "decode_splits": st["splits"]})
     if cpu:
         if w.name == "mapred7b":
@@ -1140,12 +1206,19 @@ def main():
     for _ in range(args.warmup):
         run_stuff_step(st)
     torch.cuda.synchronize()
+    dec_eager = eager_decode_ms(torch, st) if st["decode_steps"] else None
+    capture_decode(torch, st)
 
     timer = Timer(torch)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
+        if st.get("graph") is not None:
+            st["do"].zero_()
         run_stuff_step(st, timer)
+        if st.get("graph") is not None and not torch.equal(st["do"].view(torch.int16),
+                                                           st["do_eager"].view(torch.int16)):
+            raise RuntimeError("decode graph replay differs from the eager launches")
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
 
@@ -1188,9 +1261,12 @@ def main():
                    "frac_hbm": round(dec_gbs / PEAK_HBM_GBS, 4),
                    "us_per_step": round(dec_avg * 1e3, 3),
                    "us_per_step_mean": round(sum(dec_ms) / len(dec_ms) / nsteps * 1e3, 3),
+                   "us_per_step_eager": round(dec_eager / nsteps * 1e3, 3) if dec_eager else None,
                    "algorithmic_bytes_per_launch": round(dec_bytes_avg)},
         "timing": "median over the timed steps: prefill = one event pair per launch; decode = "
-                  "one event pair around a step's launches, divided by their number",
+                  "one event pair around a replay of the step's launches captured in a HIP graph "
+                  "(every replay checked bit for bit against the eager launches), divided by their "
+                  "number; us_per_step_eager = the same launches issued one by one from the host",
         "roofline": dominant,
         "rooflines": {"prefill": rl_pf, "decode": rl_dec},
     }
