@@ -781,7 +781,17 @@ __device__ __forceinline__ void prefill_items(const PfGroup& g, const KV& kv, co
 
     f32x16 sE = {}, sO = {};
     bf16x8 pE[2] = {}, pO[2] = {};
-    if (cx.nbw > 0) sE = pf_qk<D, 0>(st, lay, cur);
+    if (cx.nbw > 0) {
+      // The first block's row maximum is the exponent reference from the
+      // start (key 0 is visible to every row): its weights then never need
+      // the exact path, which would form them twice.
+      sE = pf_qk<D, 0>(st, lay, cur);
+      if (31 > cx.mlim) pf_mask(sE, 0, cx.lim);
+      float tmax = sE[0];
+#pragma unroll
+      for (int j = 1; j < 16; ++j) tmax = fmaxf(tmax, sE[j]);
+      st.m_used = max_halves(tmax);
+    }
 
     auto rotate = [&]() {
       bf16_t* const retired = prev;
