@@ -364,10 +364,12 @@ struct PfPipeCtx {
 // A full slot in an explicit instruction order: D/16 steps, each with the
 // LDS operand reads of the step two ahead, one QK(b+1) MFMA, vector work of
 // SM(b), one PV(b-1) MFMA.  The vector work is itself pipelined over the
-// steps -- step i forms the exponent arguments of step i+1's scores, the
-// exponentials of step i's and packs and sums step i-1's -- so no vector
-// instruction waits on the one before it (a wave issues in order, and such
-// a wait would hold back its next MFMA too).  A scheduling barrier after each
+// steps -- step i takes the exponentials of step i's scores, forms the
+// exponent arguments of step i+1's and packs and sums step i-1's -- so no
+// vector instruction waits on the one before it (a wave issues in order, and
+// such a wait would hold back its next MFMA too).  (Of the orders measured,
+// exponentials first after the QK MFMA was fastest by ~0.5%; raising the
+// wave priority around the MFMA cost 4-5%.)  A scheduling barrier after each
 // step and empty asm statements on the values each step produces keep the
 // compiler from regrouping the work (left alone it clusters the MFMAs, and
 // the two units take turns).
@@ -434,8 +436,8 @@ __device__ __forceinline__ float pf_full_slot(PfState<D>& st, const ChunkLayout<
     hook(i);
     __builtin_amdgcn_sched_barrier(0);
     acc = mfma32(ka[i], st.qf[i], acc);
-    if (i + 1 < kSteps) arg(i + 1);
     expo(i);
+    if (i + 1 < kSteps) arg(i + 1);
     if (i >= 1) pack(i - 1);
     st.oacc[i % kDt] = mfma32(va[i], p_prev[i / kDt], st.oacc[i % kDt]);
     __builtin_amdgcn_sched_barrier(0);
