@@ -519,6 +519,7 @@ __global__ __launch_bounds__(kWaves * 64) void awq_gemm_sm_kernel(
     for (int d = 0; d < kDepth; ++d) fetch(g0 + min(d, ng - 1), ring[d]);
   }
   wait_vm<0>();                                    // this wave's X (and first codes) landed
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);         // no LDS read of X moves above the wait
   if (ng > 0) {
     const u32x4 ones = {0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u};
     const int g_last = g0 + ng - 1;
