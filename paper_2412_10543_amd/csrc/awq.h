@@ -25,6 +25,7 @@ struct AwqPlan {
   int tiles_m, tiles_n, tiles_per_xcd;
   int sm_mb;                    // small batches: 16-row blocks (1, 2 or 4)
   int sm_nb;                    // small batches: 16-column blocks per workgroup
+  int sm_a;                     // small batches: waves across the columns (NB / A blocks each)
   int64_t tiles;
   size_t sp_bytes, part_bytes;  // large batches: group-sum pieces; split partials
   size_t counter_bytes;         // small batches split over groups: arrival counters

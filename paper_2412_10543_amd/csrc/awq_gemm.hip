@@ -424,9 +424,13 @@ __global__ __launch_bounds__(awq_lg::kThreads) void awq_gemm_lg_kernel(
 // Small batches (M <= 64), where streaming the codes from HBM is the cost.
 // 16x16x32 MFMAs (16 rows per block: no padding rows for a decode batch of
 // 16), one workgroup of W waves per 16 NB output columns (NB blocks of 16
-// columns, which share each activation read) and split of the groups.
+// columns, which share each activation read) and split of the groups.  The
+// waves form A column ranges of NB / A blocks (at most four: the conversion
+// of the codes, about one VALU instruction per code, is what a wave's time
+// goes to) by W / A group phases: wave w takes column range w % A and the
+// groups [p R, p R + R) of phase p = w / A, R = ceil(G / (W / A)).
 //
-// X.  Each wave first copies its groups' X (16-row blocks of 16 x 128,
+// X.  The waves of a phase first copy its groups' X (16-row blocks of 16 x 128,
 // 4 KB each) into LDS with direct global -> LDS copies: each copy
 // instruction moves four whole rows of a block (4 x 256 contiguous bytes, so
 // no cache line is fetched twice), lane l of instruction i landing at
@@ -436,10 +440,10 @@ __global__ __launch_bounds__(awq_lg::kThreads) void awq_gemm_lg_kernel(
 // lanes of a read group hit 16 different bank groups.  Rows past M read row
 // M - 1 (their outputs are not stored).
 //
-// Codes.  Wave w takes the groups [w R, w R + R), R = ceil(G / W), and
-// streams them through a ring of register slots: the code words (16
-// contiguous bytes per lane and column block), scales and zero points of
-// group i + depth are requested as soon as group i has taken its slot.
+// Codes.  Each wave streams its groups through a ring of register slots: the
+// code words (16 contiguous bytes per lane and column block), scales and zero
+// points of group i + depth, requested once group i is consumed (one row
+// block) or as soon as it has taken its slot (more row blocks).
 //
 // Per group and 16-row block: P = sum_t X_t B_t over the 4 k-steps (B = the
 // codes as bf16 128 + q), S = sum_t X_t 1 (a ones operand: lane (c, qq) gets
@@ -454,35 +458,46 @@ constexpr int kXCap = 32;                        // 4 KB X blocks a workgroup ca
 constexpr int kLds = kXCap * 4096;
 }  // namespace awq_sm
 
-template <int MB, int NB, int kWaves>
+template <int MB, int NBW, int A, int kWaves>
 __global__ __launch_bounds__(kWaves * 64) void awq_gemm_sm_kernel(
     const bf16_t* __restrict__ x, const uint32_t* __restrict__ qw,
     const bf16_t* __restrict__ scales, const uint8_t* __restrict__ zeros,
     bf16_t* __restrict__ y, float* __restrict__ part, int* __restrict__ arrivals, int M, int N,
     int K, int splits) {
   using namespace awq_sm;
+  static_assert(kWaves % A == 0, "the waves split into A column ranges");
+  constexpr int NB = NBW * A;                      // 16-column blocks of the workgroup
+  constexpr int kPhases = kWaves / A;              // waves per column range
   constexpr int kCols = 16 * NB;
   constexpr int kThreads = kWaves * 64;
-  constexpr int kDepth = 8 / (MB * NB) > 1 ? 8 / (MB * NB) : 1;   // ring slots (registers)
-  constexpr int kOut = MB * NB * 4;                // accumulator values per lane
+  // Ring of register slots, 8 / (MB NBW) of them.  One row block: at least
+  // two, each refilled once its group is consumed; larger row blocks (whose
+  // groups cost more to compute than to wait for): each refilled as soon as
+  // it is taken (measured, 16 / 32 / 64 rows).
+  constexpr bool kLate = MB == 1;
+  constexpr int kDepth0 = 8 / (MB * NBW) > 1 ? 8 / (MB * NBW) : 1;
+  constexpr int kDepth = kLate && kDepth0 < 2 ? 2 : kDepth0;
+  constexpr int kOut = MB * NBW * 4;               // accumulator values per lane
   static_assert(kWaves * kOut * 64 * 4 <= kLds, "wave sums fit the X region");
   __shared__ __attribute__((aligned(16))) char lds[kLds];
   const int lane = threadIdx.x & 63, w = wave_id();
+  const int ca = w % A, ph = w / A;                // column range, group phase
   const int c = lane & 15, qq = lane >> 4;
-  const int n0 = kCols * blockIdx.x + c;           // columns n0 + 16 nb
+  const int n0 = kCols * blockIdx.x + 16 * NBW * ca + c;   // columns n0 + 16 nb
   const int groups = K / kAwqGroup;
   const int spl = blockIdx.y;
   const int per_wg = (groups + splits - 1) / splits;
   const int wg_g0 = spl * per_wg;
   const int wg_end = min(groups, wg_g0 + per_wg);
-  const int per_wave = (per_wg + kWaves - 1) / kWaves;
-  const int g0 = wg_g0 + w * per_wave;
+  const int per_wave = (per_wg + kPhases - 1) / kPhases;
+  const int g0 = wg_g0 + ph * per_wave;
   const int ng = max(0, min(per_wave, wg_end - g0));
   const uint32_t kMask = in_vgpr(0x000F000Fu), kMagic = in_vgpr(0x43004300u);
   const int wpos = 8 * (qq & 1) + 4 * (qq >> 1);   // this lane's 4 words
 
-  // ---- X of this wave's groups into LDS (each wave waits for its own) ----
-  for (int ii = 0; ii < ng * MB * 4; ++ii) {
+  // ---- X of this phase's groups into LDS, the copies dealt over the phase's
+  // A waves ----
+  for (int ii = ca; ii < ng * MB * 4; ii += A) {
     const int blk = (g0 - wg_g0) * MB + (ii >> 2), part4 = ii & 3;   // (group, row block)
     const int gl = blk / MB, mb = blk % MB;
     const int p = 64 * part4 + lane;
@@ -493,14 +508,14 @@ __global__ __launch_bounds__(kWaves * 64) void awq_gemm_sm_kernel(
   }
 
   struct Slot {
-    u32x4 wd[NB];
-    uint32_t sbits[NB], z[NB];
+    u32x4 wd[NBW];
+    uint32_t sbits[NBW], z[NBW];
   };
   // everything one group needs from HBM; raw values only (arithmetic on a
   // loaded value here would wait for the load)
   auto fetch = [&](int g, Slot& sl) {
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
+    for (int nb = 0; nb < NBW; ++nb) {
       const size_t col = (size_t)g * N + n0 + 16 * nb;
       sl.wd[nb] = *reinterpret_cast<const u32x4*>(qw + col * 16 + wpos);
       sl.sbits[nb] = scales[col];
@@ -508,33 +523,43 @@ __global__ __launch_bounds__(kWaves * 64) void awq_gemm_sm_kernel(
     }
   };
 
-  f32x4 yv[MB][NB];
+  f32x4 yv[MB][NBW];
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) yv[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int nb = 0; nb < NBW; ++nb) yv[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
   Slot ring[kDepth];
+  const int g_last = g0 + max(ng, 1) - 1;
   if (ng > 0) {
 #pragma unroll
-    for (int d = 0; d < kDepth; ++d) fetch(g0 + min(d, ng - 1), ring[d]);
+    for (int d = 0; d < kDepth; ++d) fetch(min(g0 + d, g_last), ring[d]);
   }
-  wait_vm<0>();                                    // this wave's X (and first codes) landed
+  wait_vm<0>();                                    // this wave's X copies (and first codes) landed
   __atomic_signal_fence(__ATOMIC_SEQ_CST);         // no LDS read of X moves above the wait
+  if constexpr (A > 1) __syncthreads();            // ... and those of the phase's other waves
   if (ng > 0) {
     const u32x4 ones = {0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u};
-    const int g_last = g0 + ng - 1;
+    // Each pass takes kDepth groups, one per slot.  Refilled late (kLate),
+    // there is no branch around a slot's loads, so the compiler's waits see
+    // one order of requests and wait for a slot's own loads only, and the
+    // refill lands in the slot's registers (no copies at the back edge,
+    // which would wait for the loads just issued); passes past the wave's
+    // last group recompute it and do not add it.  Refilled early, the loads
+    // are unconditional too (clamped to the last group).
     for (int i0 = 0; i0 < ng; i0 += kDepth) {
 #pragma unroll
       for (int d = 0; d < kDepth; ++d) {
         const int i = i0 + d;
-        if (i >= ng) break;
-        const int g = g0 + i;
-        // take the slot, refill it (unconditionally: a load issued on one
-        // path only makes the compiler's waits fall back to waiting for all)
+        if constexpr (!kLate) {
+          if (i >= ng) break;
+        }
+        const int g = min(g0 + i, g_last);
         __builtin_amdgcn_sched_barrier(0);
         const Slot sl = ring[d];
-        fetch(min(g + kDepth, g_last), ring[d]);
-        __builtin_amdgcn_sched_barrier(0);
+        if constexpr (!kLate) {
+          fetch(min(g + kDepth, g_last), ring[d]);
+          __builtin_amdgcn_sched_barrier(0);
+        }
         bf16x8 xa[4][MB];
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb) {
@@ -544,12 +569,12 @@ __global__ __launch_bounds__(kWaves * 64) void awq_gemm_sm_kernel(
             xa[t][mb] = as_bf16x8(
                 *reinterpret_cast<const u32x4*>(blk + 16 * (16 * c + ((4 * t + qq) ^ c))));
         }
-        f32x4 p[MB][NB], sx[MB];
+        f32x4 p[MB][NBW], sx[MB];
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb) {
           sx[mb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-          for (int nb = 0; nb < NB; ++nb) p[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+          for (int nb = 0; nb < NBW; ++nb) p[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
         }
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
@@ -559,25 +584,32 @@ __global__ __launch_bounds__(kWaves * 64) void awq_gemm_sm_kernel(
 #pragma unroll
           for (int mb = 0; mb < MB; ++mb) sx[mb] = mfma16(xa[t][mb], as_bf16x8(ones), sx[mb]);
 #pragma unroll
-          for (int nb = 0; nb < NB; ++nb) {
+          for (int nb = 0; nb < NBW; ++nb) {
             const bf16x8 b = codes_to_bf16(sl.wd[nb][t], kMask, kMagic);
 #pragma unroll
             for (int mb = 0; mb < MB; ++mb) p[mb][nb] = mfma16(xa[t][mb], b, p[mb][nb]);
           }
         }
+        if (i < ng) {
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb) {
-          const float sc = bf16_to_f32(sl.sbits[nb]);
-          const float nz = -(float)(128 + (int)sl.z[nb]);
+          for (int nb = 0; nb < NBW; ++nb) {
+            const float sc = bf16_to_f32(sl.sbits[nb]);
+            const float nz = -(float)(128 + (int)sl.z[nb]);
 #pragma unroll
-          for (int mb = 0; mb < MB; ++mb)
+            for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-            for (int j = 0; j < 4; ++j)
-              yv[mb][nb][j] = fmaf(sc, fmaf(nz, sx[mb][j], p[mb][nb][j]), yv[mb][nb][j]);
+              for (int j = 0; j < 4; ++j)
+                yv[mb][nb][j] = fmaf(sc, fmaf(nz, sx[mb][j], p[mb][nb][j]), yv[mb][nb][j]);
+          }
+        }
+        if constexpr (kLate) {
+          __builtin_amdgcn_sched_barrier(0);
+          fetch(min(g0 + i + kDepth, g_last), ring[d]);   // slot consumed: refill it
         }
       }
     }
   }
+
 
   // ---- the waves' sums, added in wave order (the X region is free) ----
   __syncthreads();
@@ -585,24 +617,28 @@ __global__ __launch_bounds__(kWaves * 64) void awq_gemm_sm_kernel(
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb)
+    for (int nb = 0; nb < NBW; ++nb)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) red[(w * kOut + (mb * NB + nb) * 4 + j) * 64 + lane] = yv[mb][nb][j];
+      for (int j = 0; j < 4; ++j) red[(w * kOut + (mb * NBW + nb) * 4 + j) * 64 + lane] = yv[mb][nb][j];
   __syncthreads();
-  constexpr int kPer = (kOut * 64 + kThreads - 1) / kThreads;   // outputs per thread
+  constexpr int kTot = MB * NB * 4;                // output values per lane position
+  constexpr int kPer = (kTot * 64 + kThreads - 1) / kThreads;   // outputs per thread
   float tot[kPer];
   int orow[kPer], ocol[kPer];
 #pragma unroll
   for (int e = 0; e < kPer; ++e) {
     const int idx = threadIdx.x + e * kThreads;     // (mb, nb, j, lane') of the tile
-    const int l = idx & 63, j = (idx >> 6) & 3, nb = (idx >> 8) % NB, mb = (idx >> 8) / NB;
-    const bool have = idx < kOut * 64;
+    const int l = idx & 63, j = (idx >> 6) & 3, nbg = (idx >> 8) % NB, mb = (idx >> 8) / NB;
+    const bool have = idx < kTot * 64;
     orow[e] = have ? 16 * mb + 4 * (l >> 4) + j : M;
-    ocol[e] = kCols * blockIdx.x + 16 * nb + (l & 15);
+    ocol[e] = kCols * blockIdx.x + 16 * nbg + (l & 15);
     float acc = 0.f;
     if (have) {
+      // the waves of column range nbg / NBW, in group order
+      const int cw = nbg / NBW, nb = nbg % NBW;
 #pragma unroll
-      for (int v = 0; v < kWaves; ++v) acc += red[v * kOut * 64 + idx];
+      for (int v = 0; v < kPhases; ++v)
+        acc += red[(((v * A + cw) * kOut) + (mb * NBW + nb) * 4 + j) * 64 + l];
     }
     tot[e] = acc;
   }
@@ -708,23 +744,29 @@ AwqPlan awq_plan(int M, int N, int K) {
   // costs more than the CUs a smaller grid leaves idle (the 7B o_proj at 16
   // rows: 6.5 us on 128 workgroups, 7.4 us split in two on 256).  The column
   // blocks per workgroup are the fewest (2, 4, 8) for which the workgroups
-  // fit one per CU.
+  // fit one per CU, else 8 (each workgroup copies X for its groups: wider
+  // column tiles read it fewer times; the 7B gate_up_proj at 64 rows,
+  // 47 us against 76 us with 2 blocks).
   p.tiles_m = 1;
   p.sm_mb = M <= 16 ? 1 : (M <= 32 ? 2 : 4);
   const int min_splits = (p.groups * p.sm_mb + awq_sm::kXCap - 1) / awq_sm::kXCap;
-  const int nb_max = 8 / p.sm_mb;                  // MB * NB <= 8 (registers)
-  p.sm_nb = nb_max;
+  p.sm_nb = 8;
   for (int nb : {2, 4, 8}) {
-    if (nb > nb_max || N % (16 * nb) != 0) continue;
+    if (N % (16 * nb) != 0) continue;
     if ((int64_t)(N / (16 * nb)) * min_splits <= kAwqCus) {
       p.sm_nb = nb;
       break;
     }
   }
-  if (const int nb = env_int("RAG_AWQ_SM_NB");
-      (nb == 2 || nb == 4 || nb == 8) && nb <= nb_max && N % (16 * nb) == 0)
+  if (const int nb = env_int("RAG_AWQ_SM_NB"); (nb == 2 || nb == 4 || nb == 8) && N % (16 * nb) == 0)
     p.sm_nb = nb;
   p.tiles_n = N / (16 * p.sm_nb);
+  // A waves share the column blocks, at most four blocks each and
+  // MB * NB / A <= 8 (registers): eight blocks at 16 rows (the 7B
+  // gate_up_proj) go to two waves of four, each taking a quarter of the
+  // groups (14.1 us against 15.3 us for eight waves over all eight blocks;
+  // two blocks per wave, 14.8 us; one, 16.2 us)
+  p.sm_a = p.sm_nb / std::min({p.sm_nb, 4, 8 / p.sm_mb});
   int splits = min_splits;
   if (const int sp = env_int("RAG_AWQ_SM_SPLITS"); sp > 0) splits = std::max(min_splits, sp);
   splits = std::max(1, std::min(splits, p.groups));
@@ -776,13 +818,17 @@ hipError_t launch_awq_gemm(const AwqArgs& a, hipStream_t stream) {
     hipLaunchKernelGGL(kernel, grid, block, 0, stream, x, qw, sc, a.zeros, y, part, counters,
                        a.M, a.N, a.K, p.splits);
   };
-  switch (p.sm_mb * 10 + p.sm_nb) {
-    case 12: go(awq_gemm_sm_kernel<1, 2, 8>); break;
-    case 14: go(awq_gemm_sm_kernel<1, 4, 8>); break;
-    case 18: go(awq_gemm_sm_kernel<1, 8, 8>); break;
-    case 22: go(awq_gemm_sm_kernel<2, 2, 8>); break;
-    case 24: go(awq_gemm_sm_kernel<2, 4, 8>); break;
-    default: go(awq_gemm_sm_kernel<4, 2, 8>); break;
+  switch (p.sm_mb * 100 + p.sm_nb * 10 + p.sm_a) {
+    case 121: go(awq_gemm_sm_kernel<1, 2, 1, 8>); break;
+    case 141: go(awq_gemm_sm_kernel<1, 4, 1, 8>); break;
+    case 182: go(awq_gemm_sm_kernel<1, 4, 2, 8>); break;
+    case 221: go(awq_gemm_sm_kernel<2, 2, 1, 8>); break;
+    case 241: go(awq_gemm_sm_kernel<2, 4, 1, 8>); break;
+    case 282: go(awq_gemm_sm_kernel<2, 4, 2, 8>); break;
+    case 421: go(awq_gemm_sm_kernel<4, 2, 1, 8>); break;
+    case 442: go(awq_gemm_sm_kernel<4, 2, 2, 8>); break;
+    case 484: go(awq_gemm_sm_kernel<4, 2, 4, 8>); break;
+    default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }
