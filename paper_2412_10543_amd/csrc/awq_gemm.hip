@@ -470,12 +470,13 @@ __global__ __launch_bounds__(kWaves * 64) void awq_gemm_sm_kernel(
   constexpr int kPhases = kWaves / A;              // waves per column range
   constexpr int kCols = 16 * NB;
   constexpr int kThreads = kWaves * 64;
-  // Ring of register slots, 8 / (MB NBW) of them.  One row block: at least
+  // Ring of register slots, 8 / (MB NBW) of them, at most four (more only
+  // repeat the last group's loads).  One row block: at least
   // two, each refilled once its group is consumed; larger row blocks (whose
   // groups cost more to compute than to wait for): each refilled as soon as
   // it is taken (measured, 16 / 32 / 64 rows).
   constexpr bool kLate = MB == 1;
-  constexpr int kDepth0 = 8 / (MB * NBW) > 1 ? 8 / (MB * NBW) : 1;
+  constexpr int kDepth0 = 8 / (MB * NBW) > 4 ? 4 : (8 / (MB * NBW) > 1 ? 8 / (MB * NBW) : 1);
   constexpr int kDepth = kLate && kDepth0 < 2 ? 2 : kDepth0;
   constexpr int kOut = MB * NBW * 4;               // accumulator values per lane
   static_assert(kWaves * kOut * 64 * 4 <= kLds, "wave sums fit the X region");
@@ -743,15 +744,16 @@ AwqPlan awq_plan(int M, int N, int K) {
   // the merge of a split (coherent partial stores, arrival count, reloads)
   // costs more than the CUs a smaller grid leaves idle (the 7B o_proj at 16
   // rows: 6.5 us on 128 workgroups, 7.4 us split in two on 256).  The column
-  // blocks per workgroup are the fewest (2, 4, 8) for which the workgroups
-  // fit one per CU, else 8 (each workgroup copies X for its groups: wider
-  // column tiles read it fewer times; the 7B gate_up_proj at 64 rows,
-  // 47 us against 76 us with 2 blocks).
+  // blocks per workgroup are the fewest (1, 2, 4, 8) for which the workgroups
+  // fit one per CU (the 7B o_proj at 16 rows: 1 block, 256 workgroups, 5.0 us
+  // against 6.0 us for 2 blocks on 128), else 8 (each workgroup copies X for
+  // its groups: wider column tiles read it fewer times; the 7B gate_up_proj
+  // at 64 rows, 47 us against 76 us with 2 blocks).
   p.tiles_m = 1;
   p.sm_mb = M <= 16 ? 1 : (M <= 32 ? 2 : 4);
   const int min_splits = (p.groups * p.sm_mb + awq_sm::kXCap - 1) / awq_sm::kXCap;
   p.sm_nb = 8;
-  for (int nb : {2, 4, 8}) {
+  for (int nb : {1, 2, 4, 8}) {
     if (N % (16 * nb) != 0) continue;
     if ((int64_t)(N / (16 * nb)) * min_splits <= kAwqCus) {
       p.sm_nb = nb;
@@ -820,6 +822,9 @@ hipError_t launch_awq_gemm(const AwqArgs& a, hipStream_t stream) {
   };
   switch (p.sm_mb * 100 + p.sm_nb * 10 + p.sm_a) {
     case 121: go(awq_gemm_sm_kernel<1, 2, 1, 8>); break;
+    case 111: go(awq_gemm_sm_kernel<1, 1, 1, 8>); break;
+    case 211: go(awq_gemm_sm_kernel<2, 1, 1, 8>); break;
+    case 411: go(awq_gemm_sm_kernel<4, 1, 1, 8>); break;
     case 141: go(awq_gemm_sm_kernel<1, 4, 1, 8>); break;
     case 182: go(awq_gemm_sm_kernel<1, 4, 2, 8>); break;
     case 221: go(awq_gemm_sm_kernel<2, 2, 1, 8>); break;

@@ -68,7 +68,7 @@ def _check(p, y, rows=None, cols=None):
 @pytest.mark.parametrize("M,N,K", [
     (1, 128, 128), (7, 256, 384), (64, 128, 256), (77, 384, 1024), (130, 512, 512),
     (16, 4096, 4096), (256, 1024, 2048), (333, 256, 14336 // 4), (1000, 640, 256),
-    (5, 256, 8192), (40, 384, 10240)])
+    (5, 256, 8192), (40, 384, 10240), (20, 512, 1024)])
 def test_awq_parity(M, N, K):
     p = awq_problem(M, N, K, seed=M * 7 + N + K, device="cuda")
     _check(p, _run(p, *_device(p)))
