@@ -75,11 +75,12 @@ def test_awq_parity(M, N, K):
 
 
 @pytest.mark.parametrize("name,K,N", AWQ_LAYERS_7B)
-@pytest.mark.parametrize("M", [16, 8192])
+@pytest.mark.parametrize("M", [16, 40, 64, 8192])
 def test_awq_7b_layers_sampled(name, K, N, M):
-    """The 7B model's linear layers at a decode batch and a chunked-prefill
-    batch, the shapes the bench times; sampled rows and columns (first, last,
-    random) against the oracle."""
+    """The 7B model's linear layers at decode batches (16 rows, the shape the
+    bench times; 40 and 64 rows: 8-block column tiles on 2 or 4 waves) and a
+    chunked-prefill batch; sampled rows and columns (first, last, random)
+    against the oracle."""
     p = awq_problem(M, N, K, seed=K + N + M, device="cuda")
     y = _run(p, *_device(p))
     r = np.random.Generator(np.random.PCG64(M + N))
