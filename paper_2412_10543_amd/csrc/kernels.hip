@@ -322,21 +322,23 @@ __device__ __forceinline__ void decode_block_balanced(const PagedKernelArgs& a, 
   auto unit_of = [&](int g) { return (int)(((uint32_t)(g + 1) * uk + ut - 1) / ut) - 1; };
   int gs = 0;                 // first global page of the row
   bool first_piece = true;
-#pragma unroll
-  for (int c = 0; c < kBalMaxChunks; ++c) {
-    for (int i = 0; i < min(kWave, S - c * kWave) && gs < hi; ++i) {
-      const int kls = __builtin_amdgcn_readlane(kl[c], i);
-      const int ps = (kls + 15) >> 4;
-      if (ps > 0 && gs + ps > lo) {
-        const int first = unit_of(gs), last = unit_of(gs + ps - 1);
-        if (!first_piece) __syncthreads();   // LDS of the previous piece fully read
-        first_piece = false;
-        decode_piece<D, NP, W, kAppend>(a, group, block_stride, c * kWave + i, kvh, kls,
-                                        max(lo, gs) - gs, min(hi, gs + ps) - gs, k - first,
-                                        last - first + 1, lds);
-      }
-      gs += ps;
+  // one call site of decode_piece (rows walked in one loop, the chunk of a
+  // row picked by value): the kernel's code stays one copy of the unit
+  for (int s = 0; s < S && gs < hi; ++s) {
+    static_assert(kBalMaxChunks == 4, "row chunk select");
+    const int c = s >> 6;
+    const int klc = c == 0 ? kl[0] : c == 1 ? kl[1] : c == 2 ? kl[2] : kl[3];
+    const int kls = __builtin_amdgcn_readlane(klc, s & 63);
+    const int ps = (kls + 15) >> 4;
+    if (ps > 0 && gs + ps > lo) {
+      const int first = unit_of(gs), last = unit_of(gs + ps - 1);
+      if (!first_piece) __syncthreads();   // LDS of the previous piece fully read
+      first_piece = false;
+      decode_piece<D, NP, W, kAppend>(a, group, block_stride, s, kvh, kls,
+                                      max(lo, gs) - gs, min(hi, gs + ps) - gs, k - first,
+                                      last - first + 1, lds);
     }
+    gs += ps;
   }
 }
 
