@@ -760,7 +760,7 @@ AwqPlan awq_plan(int M, int N, int K) {
       break;
     }
   }
-  if (const int nb = env_int("RAG_AWQ_SM_NB"); (nb == 2 || nb == 4 || nb == 8) && N % (16 * nb) == 0)
+  if (const int nb = env_int("RAG_AWQ_SM_NB"); (nb == 1 || nb == 2 || nb == 4 || nb == 8) && N % (16 * nb) == 0)
     p.sm_nb = nb;
   p.tiles_n = N / (16 * p.sm_nb);
   // A waves share the column blocks, at most four blocks each and

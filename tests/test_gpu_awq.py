@@ -109,6 +109,7 @@ def test_awq_deterministic_and_extremes():
     (16, 4096, 14336, None, None),    # 112 groups: split at least 4 ways (X staged in LDS)
     (16, 4096, 4096, None, 2),        # o_proj shape, split in two
     (3, 1024, 2048, 8, 3),            # 8 column blocks, uneven split (16 groups / 3)
+    (3, 1024, 2048, 1, 3),            # one column block per workgroup, uneven split
     (40, 512, 4096, 2, 5),            # 3 row blocks (padded to 4), uneven split
     (64, 256, 1024, 2, 8),            # one group per workgroup
     (9, 1024, 2432, 8, 2),            # 8 blocks on 2 waves x 4 phases, uneven (3, 3, 3, 1)
