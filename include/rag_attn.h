@@ -469,7 +469,11 @@ rag_status rag_awq_pack_weights(const uint8_t *q, int32_t K, int32_t N,
  * split over workgroups (long K, or too few column blocks to fill the GPU):
  * one arrival counter per column block, then fp32 partial outputs
  * [splits, M, N].  Partials are added in a fixed order, so results do not
- * depend on timing. */
+ * depend on timing.  For M <= 64 the environment variables RAG_AWQ_SM_NB
+ * (16-column blocks per workgroup: 1, 2, 4 or 8) and RAG_AWQ_SM_SPLITS (at
+ * least this many splits) override the library's choice, read at each call
+ * of this function and of rag_awq_gemm (which must then see the same
+ * values); testing knobs: they change the size and the rounding order. */
 size_t rag_awq_workspace_size(int32_t M, int32_t N, int32_t K,
                               int32_t group_size);
 
