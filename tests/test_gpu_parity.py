@@ -107,6 +107,20 @@ def test_decode_balanced_units_many_rows(orc, seed):
     assert float((o.float() - o2.float()).abs().max()) < 1e-2
 
 
+@pytest.mark.parametrize("n_rows,hq,hkv", [(100, 16, 2), (200, 8, 1), (255, 4, 1)])
+def test_decode_balanced_units_rows_past_64(orc, n_rows, hq, hkv):
+    """Balanced units (fewer (row, kv head) pairs than CUs) with more than 64
+    rows: each unit reads the lengths in chunks of 64 rows (up to four) and
+    walks all of them; lengths from 1 to 800 with a few long rows."""
+    rng = np.random.Generator(np.random.PCG64(n_rows + hq))
+    lens = [int(x) for x in rng.integers(1, 800, size=n_rows)]
+    for i in (0, n_rows // 2, n_rows - 1):
+        lens[i] = 4000 + i
+    q, pool = G.decode_case(lens, hq, hkv, 128, seed=n_rows * 3 + hkv)
+    o = G.gpu_paged(q, pool, hq, hkv, 128, G.scale_for(128), num_splits=0)
+    G.assert_parity(o, G.oracle_paged(orc, q, pool, G.scale_for(128)), "balanced, rows past 64")
+
+
 def test_decode_split_merge_repeatable(orc):
     """The in-kernel split merge relies on completed device-coherent stores
     and a device-scope arrival count: 64 calls with 16 splits (and with the
