@@ -428,7 +428,8 @@ __global__ __launch_bounds__(awq_lg::kThreads) void awq_gemm_lg_kernel(
 // waves form A column ranges of NB / A blocks (at most four: the conversion
 // of the codes, about one VALU instruction per code, is what a wave's time
 // goes to) by W / A group phases: wave w takes column range w % A and the
-// groups [p R, p R + R) of phase p = w / A, R = ceil(G / (W / A)).
+// groups [p R, p R + R) of the workgroup's G of phase p = w / A,
+// R = ceil(G / (W / A)).
 //
 // X.  The waves of a phase first copy its groups' X (16-row blocks of 16 x 128,
 // 4 KB each) into LDS with direct global -> LDS copies: each copy
@@ -448,8 +449,9 @@ __global__ __launch_bounds__(awq_lg::kThreads) void awq_gemm_lg_kernel(
 // Per group and 16-row block: P = sum_t X_t B_t over the 4 k-steps (B = the
 // codes as bf16 128 + q), S = sum_t X_t 1 (a ones operand: lane (c, qq) gets
 // the group sums of rows 4 qq .. 4 qq + 3, the rows of its outputs), and
-// y += s (P - (128 + z) S) in fp32.  The waves' sums are added in LDS in wave
-// order.  With the groups split over workgroups, fp32 partials go out with
+// y += s (P - (128 + z) S) in fp32.  The sums of a column range's waves are
+// added in LDS in phase (group) order.  With the groups split over
+// workgroups, fp32 partials go out with
 // device-coherent stores and the last workgroup of a column block to arrive
 // (device-scope counter) adds them in split order and resets the counter.
 // ---------------------------------------------------------------------------
