@@ -968,9 +968,10 @@ def ceilings(torch, dev, reps=5, clocks=True):
     disjoint 512 MB page sets of an 8 GB pool alternate, so neither is found
     in the 256 MB Infinity Cache), a contiguous 4 GB read, a
     dependency-free bf16 MFMA loop, the prefill kernel's steady 32-key slot
-    on LDS-resident tiles, and that slot's MFMA + softmax instruction mix with
-    register operands.  Slot rates count 4 * d FLOP per query-key pair, as
-    the prefill's algorithmic FLOPs do."""
+    on LDS-resident tiles, that slot's MFMA + softmax instruction mix with
+    register operands, and the slot's work split between specialised wave
+    pairs.  Slot rates count 4 * d FLOP per query-key pair, as the prefill's
+    algorithmic FLOPs do."""
     import ctypes
 
     import numpy as np
@@ -983,6 +984,7 @@ def ceilings(torch, dev, reps=5, clocks=True):
     L.rag_probe_mfma_loop.argtypes = [ctypes.c_int32, ctypes.c_int32, vp, vp]
     L.rag_probe_attn_slot.argtypes = [ctypes.c_int32, ctypes.c_int32, vp, vp]
     L.rag_probe_softmax_mfma.argtypes = [ctypes.c_int32, ctypes.c_int32, vp, vp]
+    L.rag_probe_attn_pair.argtypes = [ctypes.c_int32, ctypes.c_int32, vp, vp]
     stream = torch.cuda.current_stream().cuda_stream
     sink = torch.zeros(1 << 16, dtype=torch.int32, device=dev)
 
@@ -1049,6 +1051,11 @@ def ceilings(torch, dev, reps=5, clocks=True):
         iters = 4000
         ms = timed(lambda fn=fn: fn(iters, 256, sink.data_ptr(), stream))
         out[key] = round(256 * 8 * 2 * iters * slot_flops / ms / 1e9, 1)
+    # the same work split between the two waves of a SIMD: per 32-key block
+    # and pair, 64 rows x 32 keys x 4 x 128 FLOP
+    blocks = 8000
+    ms = timed(lambda: L.rag_probe_attn_pair(blocks, 256, sink.data_ptr(), stream))
+    out["attn_pair_lds_tflops"] = round(256 * 4 * blocks * 2 * slot_flops / ms / 1e9, 1)
     if clocks:
         # the shader clock while the MFMA loop runs (about 2 s of launches)
         sampler = ClockSampler(delay=1.0)

@@ -48,6 +48,15 @@ int rag_probe_mfma_loop(int32_t iters, int32_t workgroups, void *sink,
 int rag_probe_attn_slot(int32_t iters, int32_t workgroups, void *sink,
                         hipStream_t stream);
 
+/* `workgroups` eight-wave workgroups on the same two LDS tiles, the slot's
+ * work split between the two waves of each SIMD: wave w < 4 computes QK^T
+ * and the exponentials for 64 query rows (one K read per step for both 32-row
+ * blocks) and passes the bf16 weights through LDS to wave w + 4, which runs
+ * PV for the 64 rows; a workgroup barrier per 32-key block, iters blocks.
+ * 1048576 FLOP per block and wave pair. */
+int rag_probe_attn_pair(int32_t iters, int32_t workgroups, void *sink,
+                        hipStream_t stream);
+
 /* The same instruction mix as rag_probe_attn_slot with K/V operands in
  * registers (no LDS): 2 * iters slots of 16 MFMAs and the softmax vector work of
  * 32 x 32 scores per wave. */

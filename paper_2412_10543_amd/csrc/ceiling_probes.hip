@@ -14,7 +14,10 @@
 //     loop itself;
 //   * softmax-MFMA mix: the same MFMA and vector instructions in the same
 //     order with the K/V operands in registers (no LDS) -- the rate the
-//     instruction mix allows on the matrix core and vector ALU alone.
+//     instruction mix allows on the matrix core and vector ALU alone;
+//   * specialised pairs: the same work split between the two waves of a SIMD
+//     (one computes scores and weights for 64 rows, the other PV), the
+//     weights passed through LDS -- an alternative layout, for comparison.
 // Each workgroup writes one value derived from what it read or computed, so
 // nothing is optimised away.  Declared in include/ceiling_probes.h.
 #include <hip/hip_runtime.h>
@@ -143,6 +146,92 @@ __global__ __launch_bounds__(512, 2) void probe_attn_slot_kernel(int iters,
 #pragma unroll
     for (int j = 0; j < 16; ++j) r += st.oacc[dt][j];
   if (r == 1.2345e-30f) out[blockIdx.x] = r;
+}
+
+// A different split of the same slot work (the layout the prefill does not
+// use, measured for comparison): the two waves of a SIMD specialise.  Wave w
+// < 4 (the producer of pair w) computes QK^T for 64 query rows -- two 32-row
+// blocks sharing each K operand read -- and their exponentials, and hands the
+// bf16 weights to wave w + 4 through LDS (double-buffered); wave w + 4 (the
+// consumer) runs PV for the 64 rows, each V^T operand read serving both
+// blocks.  A workgroup barrier per 32-key block.  Per iteration and pair:
+// 64 rows x 32 keys x 4 x 128 FLOP, 24 KB of LDS traffic (32 KB for two
+// waves of the prefill's own slot).
+__global__ __launch_bounds__(512, 2) void probe_attn_pair_kernel(int iters,
+                                                                 float* __restrict__ out) {
+  constexpr int D = 128;
+  using Lay = ChunkLayout<D>;
+  __shared__ __attribute__((aligned(16))) bf16_t s0[Lay::kElemsTile];
+  __shared__ __attribute__((aligned(16))) bf16_t s1[Lay::kElemsTile];
+  __shared__ __attribute__((aligned(16))) u32x4 xb[2][4][64 * 4];   // [buffer][pair][lane, part]
+  for (int i = threadIdx.x; i < Lay::kElemsTile; i += blockDim.x) {
+    s0[i] = __builtin_bit_cast(bf16_t, (__bf16)(0.01f * (float)((i % 23) - 11)));
+    s1[i] = __builtin_bit_cast(bf16_t, (__bf16)(0.01f * (float)((i % 19) - 9)));
+  }
+  for (int i = threadIdx.x; i < 2 * 4 * 64 * 4; i += blockDim.x)
+    (&xb[0][0][0])[i] = u32x4{0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u};
+  __syncthreads();
+  const int lane = threadIdx.x & 63, w = wave_id(), pair = w & 3;
+  const Lay lay;
+  const float c = 0.08838834764831845f * kLog2e;
+  float res = 0.f;
+  if (w < 4) {
+    bf16x8 qf[2][8];
+#pragma unroll
+    for (int r = 0; r < 2; ++r)
+#pragma unroll
+      for (int ks = 0; ks < 8; ++ks) qf[r][ks] = probe_frag(lane, ks + 8 * r);
+    const float nm = -0.5f;
+    for (int it = 0; it < iters; ++it) {
+      const bf16_t* kst = (it & 1) ? s1 : s0;
+      const int H = (it >> 1) & 1;
+      f32x16 s[2] = {};
+#pragma unroll
+      for (int ks = 0; ks < 8; ++ks) {
+        const bf16x8 ka = *reinterpret_cast<const bf16x8*>(kst + lay.k_off(H, ks));
+        s[0] = mfma32(ka, qf[0][ks], s[0]);
+        s[1] = mfma32(ka, qf[1][ks], s[1]);
+      }
+      u32x4* dst = &xb[it & 1][pair][lane * 4];
+#pragma unroll
+      for (int r = 0; r < 2; ++r) {
+        bf16x8 p[2];
+        res += pf_weights(s[r], c, nm, p);
+        dst[2 * r] = __builtin_bit_cast(u32x4, p[0]);
+        dst[2 * r + 1] = __builtin_bit_cast(u32x4, p[1]);
+      }
+      pf_barrier();
+    }
+  } else {
+    f32x16 o[2][4] = {};
+    for (int it = 0; it < iters; ++it) {
+      const bf16_t* vst = ((it & 1) ? s0 : s1) + kPfBN * D;
+      const int H = (it >> 1) & 1;
+      const u32x4* src = &xb[(it + 1) & 1][pair][lane * 4];   // the previous block's weights
+      bf16x8 pp[2][2];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) pp[q >> 1][q & 1] = __builtin_bit_cast(bf16x8, src[q]);
+#pragma unroll
+      for (int s2 = 0; s2 < 2; ++s2) {
+        const int rw = 32 * H + 16 * s2;
+#pragma unroll
+        for (int dt = 0; dt < D / 32; ++dt) {
+          const bf16x8 a = join_bf16x8(lds_read_tr4(vst + lay.v_off(rw, dt)),
+                                       lds_read_tr4(vst + lay.v_off(rw + 8, dt)));
+          o[0][dt] = mfma32(a, pp[0][s2], o[0][dt]);
+          o[1][dt] = mfma32(a, pp[1][s2], o[1][dt]);
+        }
+      }
+      pf_barrier();
+    }
+#pragma unroll
+    for (int r = 0; r < 2; ++r)
+#pragma unroll
+      for (int dt = 0; dt < D / 32; ++dt)
+#pragma unroll
+        for (int j = 0; j < 16; ++j) res += o[r][dt][j];
+  }
+  if (res == 1.2345e-30f) out[blockIdx.x] = res;
 }
 
 // The slot's MFMA and vector instructions in pf_full_slot's order, K and V
@@ -274,6 +363,13 @@ int rag_probe_mfma_loop(int32_t iters, int32_t workgroups, void* sink, hipStream
 int rag_probe_attn_slot(int32_t iters, int32_t workgroups, void* sink, hipStream_t stream) {
   if (!sink || iters < 0 || workgroups <= 0) return -1;
   hipLaunchKernelGGL(rag::probe_attn_slot_kernel, dim3(workgroups), dim3(512), 0, stream, iters,
+                     (float*)sink);
+  return hipGetLastError() == hipSuccess ? 0 : -4;
+}
+
+int rag_probe_attn_pair(int32_t iters, int32_t workgroups, void* sink, hipStream_t stream) {
+  if (!sink || iters < 0 || workgroups <= 0) return -1;
+  hipLaunchKernelGGL(rag::probe_attn_pair_kernel, dim3(workgroups), dim3(512), 0, stream, iters,
                      (float*)sink);
   return hipGetLastError() == hipSuccess ? 0 : -4;
 }
