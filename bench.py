@@ -1171,8 +1171,8 @@ def main():
         print(json.dumps(t, indent=1))
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py measures one GPU: this build has no multi-GPU path "
-              "(sequences shard across GPUs with no exchange; see DESIGN.md). "
+        print("bench.py measures one GPU: the library has no multi-GPU path "
+              "(sequences would shard across GPUs with no exchange between them). "
               "Run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
 
