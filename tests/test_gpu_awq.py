@@ -178,3 +178,17 @@ def test_awq_empty_batch():
     y = torch.empty((0, 256), dtype=torch.bfloat16, device="cuda")
     binding.rag_awq_gemm(p.x, qw, sc, z, y, None)
     torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("seed", [3, 4])
+def test_awq_random_shapes(seed):
+    """Seeded random shapes on both kernels: M 1-300, N and K multiples of
+    128 up to 2048 and 5120 (small batches split or not, large batches with and
+    without the group split)."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    for case in range(12):
+        M = int(rng.integers(1, 301))
+        N = 128 * int(rng.integers(1, 17))
+        K = 128 * int(rng.integers(1, 41))
+        p = awq_problem(M, N, K, seed=seed * 1000 + case, device="cuda")
+        _check(p, _run(p, *_device(p)))
