@@ -4,7 +4,8 @@ decode + chunked-prefill launch with split-KV merges, and the int4 GEMM split
 over the weight groups.  Every replay, with eager launches of other inputs and
 synchronisations in between, gives the eager result bit for bit; the split
 counters in the workspaces stay usable by eager calls after the replays; the
-outputs match the fp64 oracle."""
+outputs match the fp64 oracle.  The same three calls enqueued on three streams
+at once (each with its own workspace) give the results computed alone."""
 import numpy as np
 import pytest
 import torch
@@ -142,3 +143,54 @@ def test_awq_split_graph_replays():
     x = p.x.float().cpu().numpy().astype(np.float64)
     ref = oracle.awq_gemm(x, p.codes, p.zeros, p.scales.float().numpy().astype(np.float64), 128)
     G.assert_parity(y.float().cpu().numpy().astype(np.float64), ref, "awq after replays")
+
+
+def test_concurrent_streams_match_sequential():
+    """A prefill, a split-KV decode (own workspace) and a split int4 GEMM (own
+    workspace) enqueued on three streams so that they may run at the same
+    time, four rounds: every result equals the one computed alone."""
+    hq, hkv, d = 32, 8, 128
+    sc = G.scale_for(d)
+    lq = [576, 300, 1000]
+    q, k, v = G.prefill_inputs(lq, lq, hq, hkv, d, seed=1540)
+    cu = G.to_dev_i32(G.cu_from_lens(lq))
+    kv = [3000, 17, 900, 4000]
+    pool = paged_pool(kv, hkv, d, 1541, device="cuda")
+    kl = G.to_dev_i32(pool.kv_lens)
+    dq = normal_bf16((len(kv), hq, d), 1542, "cuda")
+    ws_d = G.workspace_for(len(kv), hq, hkv, d, pool.block_tables.shape[1], 4)
+    M, N, K = 16, 1024, 14336
+    p = awq_problem(M, N, K, seed=1543, device="cuda")
+    qw = torch.from_numpy(binding.rag_awq_pack_weights(p.codes)).cuda()
+    asc, az = p.scales.cuda(), torch.from_numpy(p.zeros).cuda()
+    ws_a = torch.zeros(binding.rag_awq_workspace_size(M, N, K), dtype=torch.uint8, device="cuda")
+
+    def prefill(o, stream):
+        binding.rag_attn_prefill_varlen(q, k, v, o, None, cu, cu, max(lq), max(lq), sc, True,
+                                        stream=stream)
+
+    def decode(o, stream):
+        binding.rag_attn_decode_paged(dq, pool.k_cache, pool.v_cache, o, pool.block_tables, kl,
+                                      sc, num_splits=4, workspace=ws_d, stream=stream)
+
+    def gemm(y, stream):
+        binding.rag_awq_gemm(p.x, qw, asc, az, y, ws_a, stream=stream)
+
+    alone = [torch.empty_like(q), torch.empty_like(dq),
+             torch.empty((M, N), dtype=torch.bfloat16, device="cuda")]
+    for fn, out in zip((prefill, decode, gemm), alone):
+        fn(out, None)
+        torch.cuda.synchronize()
+    streams = [torch.cuda.Stream() for _ in range(3)]
+    for s in streams:
+        s.wait_stream(torch.cuda.current_stream())
+    for r in range(4):
+        print(f"concurrent round {r}", flush=True)
+        outs = [torch.empty_like(a) for a in alone]
+        torch.cuda.synchronize()
+        for fn, out, s in zip((prefill, decode, gemm), outs, streams):
+            with torch.cuda.stream(s):
+                fn(out, s.cuda_stream)
+        torch.cuda.synchronize()
+        for a, b in zip(alone, outs):
+            assert _same(a, b), f"round {r}"
