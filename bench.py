@@ -657,7 +657,7 @@ def bench_phase_fused_kv(torch, dev, reps):
     return out
 
 
-def bench_phase_awq(torch, dev, reps, batches=(16, 8192), graph=True):
+def bench_phase_awq(torch, dev, reps, batches=(16, 8192), graph=True, dense=True):
     """Group-quantized int4-weight GEMMs of the 7B model's linear layers
     (qkv, o, gate_up, down) at a decode batch of 16 rows (HBM-bound: the packed
     weights dominate) and a chunked-prefill batch of 8192 rows (MFMA-bound).
@@ -667,7 +667,12 @@ def bench_phase_awq(torch, dev, reps, batches=(16, 8192), graph=True):
     `us` is one call timed with HIP events around it, host launch included; at
     16 rows that is mostly the launch path, so `us_gpu` times the same calls
     captured in a HIP graph (10 per replay; every replay's output is checked
-    bit for bit against the eager result) and the rates use `us_gpu`."""
+    bit for bit against the eager result) and the rates use `us_gpu`.
+
+    For context, `dense_bf16_library_us` times torch's bf16 matmul (the
+    vendor GEMM library) of x with a dense bf16 weight of the same shape,
+    i.e. the same product without the quantisation (ten back-to-back calls
+    between two events); `vs_dense_library` is that time over `us_gpu`."""
     from paper_2412_10543_amd import binding
     from paper_2412_10543_amd.workloads import AWQ_LAYERS_7B, awq_problem
     out = {}
@@ -716,6 +721,23 @@ def bench_phase_awq(torch, dev, reps, batches=(16, 8192), graph=True):
                     gms.append(timer.ms("r")[0] / 10)
                 ms_gpu = median(gms)
                 del cg
+            ms_dense = None
+            if dense:
+                wd = torch.empty((K, N), dtype=torch.bfloat16, device=dev).normal_(0, K ** -0.5)
+                for _ in range(WARMUP_REPS):
+                    yd = x @ wd
+                torch.cuda.synchronize()
+                dms = []
+                for _ in range(5):
+                    timer = Timer(torch)
+                    timer.start("d")
+                    for _ in range(10):
+                        yd = x @ wd
+                    timer.stop("d")
+                    torch.cuda.synchronize()
+                    dms.append(timer.ms("d")[0] / 10)
+                ms_dense = median(dms)
+                del wd, yd
             nbytes = 2.0 * M * K + K * N / 2 + (K // 128) * N * 3 + 2.0 * M * N
             tflops = 2.0 * M * N * K / ms_gpu / 1e9
             gbs = nbytes / ms_gpu / 1e6
@@ -723,7 +745,11 @@ def bench_phase_awq(torch, dev, reps, batches=(16, 8192), graph=True):
                                    "us_gpu": round(ms_gpu * 1e3, 2),
                                    "tflops": round(tflops, 1), "gbs": round(gbs, 1),
                                    "frac_mfma": round(tflops / PEAK_BF16_TFLOPS, 4),
-                                   "frac_hbm": round(gbs / PEAK_HBM_GBS, 4)}
+                                   "frac_hbm": round(gbs / PEAK_HBM_GBS, 4),
+                                   "dense_bf16_library_us":
+                                       None if ms_dense is None else round(ms_dense * 1e3, 2),
+                                   "vs_dense_library":
+                                       None if ms_dense is None else round(ms_dense / ms_gpu, 3)}
             del x, y, ws
         del p, qw, sc, z
     torch.cuda.empty_cache()
@@ -1235,7 +1261,8 @@ def main():
         return
     if args.awq_only:
         print(json.dumps({"awq_gemm_7b": bench_phase_awq(torch, torch.device("cuda:0"),
-                                                         max(args.extra_reps, 10), graph=False)}))
+                                                         max(args.extra_reps, 10), graph=False,
+                                                         dense=False)}))
         return
     from paper_2412_10543_amd import binding
     from paper_2412_10543_amd.workloads import long70b, mapred7b, stuff7b
@@ -1325,7 +1352,8 @@ def main():
         phases["mixed"] = bench_phase_mixed(torch, dev, args.extra_reps, cpu=cpu)
         phases["kv_write"] = bench_phase_kv_write(torch, dev, max(args.extra_reps, 10))
         phases["fused_kv"] = bench_phase_fused_kv(torch, dev, max(args.extra_reps, 10))
-        phases["awq_gemm_7b"] = bench_phase_awq(torch, dev, max(args.extra_reps, 10))
+        phases["awq_gemm_7b"] = bench_phase_awq(torch, dev, max(args.extra_reps, 10),
+                                                dense=not under_profiler)
         phases["query_stream"] = bench_phase_stream(torch)
         phases["query_stream_tight"] = bench_phase_stream(torch, n=32, rate=2000.0, budget_gb=1)
         res["phases"] = phases
