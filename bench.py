@@ -756,6 +756,61 @@ def bench_phase_awq(torch, dev, reps, batches=(16, 8192), graph=True, dense=True
     return out
 
 
+def bench_phase_library_attention(torch, dev, reps=5):
+    """For context: torch's own fused attention (scaled_dot_product_attention
+    restricted to its flash backend, the framework's library kernel; no other
+    backend is allowed to run) on the prompts of stuff7b, mapred7b and
+    long70b, causal, bf16.  Prompts of different lengths are one call each;
+    equal lengths (the mappers) one batched call.  K and V are expanded to
+    the q heads (repeat_interleave) for the call; the FLOP count is the same
+    as the prefill phases'.  Not part of the product path."""
+    import torch.nn.functional as F
+    from torch.nn.attention import SDPBackend, sdpa_kernel
+
+    from paper_2412_10543_amd import binding, workloads
+    from paper_2412_10543_amd.workloads import normal_bf16
+    out = {}
+    for name in ("stuff7b", "mapred7b", "long70b"):
+        w = getattr(workloads, name)()
+        cu, _ = binding.rag_plan_prompts(w.method, w.query_lens, w.num_chunks, w.chunk_len,
+                                         w.intermediate_length, w.answer_len)
+        lens = [b - a for a, b in zip(cu[:-1], cu[1:])]
+        g = w.hq // w.hkv
+        groups = [(len(lens), lens[0])] if len(set(lens)) == 1 else [(1, n) for n in lens]
+        calls = []
+        for i, (batch, n) in enumerate(groups):
+            q = normal_bf16((batch, w.hq, n, w.d), w.seed + 10 * i, dev)
+            k = normal_bf16((batch, w.hkv, n, w.d), w.seed + 10 * i + 1, dev)
+            v = normal_bf16((batch, w.hkv, n, w.d), w.seed + 10 * i + 2, dev)
+            calls.append((q, k.repeat_interleave(g, dim=1).contiguous(),
+                          v.repeat_interleave(g, dim=1).contiguous()))
+            del k, v
+
+        def run():
+            with sdpa_kernel([SDPBackend.FLASH_ATTENTION]):
+                for q, k, v in calls:
+                    F.scaled_dot_product_attention(q, k, v, is_causal=True)
+        try:
+            run()
+            torch.cuda.synchronize()
+        except RuntimeError as e:
+            out[name] = {"error": str(e)[:200]}
+            continue
+        timer = Timer(torch)
+        for _ in range(reps):
+            timer.start("a")
+            run()
+            timer.stop("a")
+        torch.cuda.synchronize()
+        ms = median(timer.ms("a"))
+        out[name] = {"ms": round(ms, 4),
+                     "tflops": round(prefill_flops(lens, lens, w.hq, w.d) / ms / 1e9, 1),
+                     "calls": len(calls)}
+        del calls
+    torch.cuda.empty_cache()
+    return out
+
+
 def bench_phase_stream(torch, n=32, rate=100.0, budget_gb=16):
     """A synthetic query stream (Poisson arrivals, random profiles) through the
     configuration planner and the kernels: 7B-class shape (Hq 32, Hkv 8, d 128,
@@ -1354,6 +1409,15 @@ def main():
         phases["fused_kv"] = bench_phase_fused_kv(torch, dev, max(args.extra_reps, 10))
         phases["awq_gemm_7b"] = bench_phase_awq(torch, dev, max(args.extra_reps, 10),
                                                 dense=not under_profiler)
+        if not under_profiler:
+            lib_attn = bench_phase_library_attention(torch, dev)
+            ours = {"stuff7b": res["prefill"]["ms"],
+                    "mapred7b": phases["mapred7b"]["prefill_ms"],
+                    "long70b": phases["long70b"]["prefill_ms"]}
+            for name, r in lib_attn.items():
+                if "ms" in r:
+                    r["ours_speedup"] = round(r["ms"] / ours[name], 2)
+            phases["torch_sdpa_flash"] = lib_attn
         phases["query_stream"] = bench_phase_stream(torch)
         phases["query_stream_tight"] = bench_phase_stream(torch, n=32, rate=2000.0, budget_gb=1)
         res["phases"] = phases
