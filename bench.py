@@ -1083,10 +1083,11 @@ def prefill_only(torch, name, dev, reps):
 def ceilings(torch, dev, reps=5, clocks=True):
     """Hardware ceilings the roofline fractions are read against, measured
     with the probes of libceiling_probes.so (HIP events around one launch,
-    median of `reps`): random 4 KB page reads (decode's access pattern; two
-    disjoint 512 MB page sets of an 8 GB pool alternate, so neither is found
-    in the 256 MB Infinity Cache), a contiguous 4 GB read, a
-    dependency-free bf16 MFMA loop, the prefill kernel's steady 32-key slot
+    median of `reps`): random 4 KB page reads (two disjoint 512 MB page sets
+    of an 8 GB pool alternate, so neither is found in the 256 MB Infinity
+    Cache), K and V pages loaded as the paged decode kernel loads them (and
+    as whole rows), a contiguous 4 GB read -- the reads under the default and
+    the non-temporal load policy -- a dependency-free bf16 MFMA loop, the prefill kernel's steady 32-key slot
     on LDS-resident tiles, that slot's MFMA + softmax instruction mix with
     register operands, and the slot's work split between specialised wave
     pairs.  Slot rates count 4 * d FLOP per query-key pair, as the prefill's
@@ -1099,7 +1100,10 @@ def ceilings(torch, dev, reps=5, clocks=True):
     L = ctypes.CDLL(pb.PROBES)
     vp = ctypes.c_void_p
     L.rag_probe_page_read.argtypes = [vp, vp, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, vp, vp]
-    L.rag_probe_stream_read.argtypes = [vp, ctypes.c_int64, ctypes.c_int32, vp, vp]
+    L.rag_probe_stream_read.argtypes = [vp, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, vp,
+                                        vp]
+    L.rag_probe_kv_page_read.argtypes = [vp, vp, vp, ctypes.c_int64, ctypes.c_int32,
+                                         ctypes.c_int32, vp, vp]
     L.rag_probe_mfma_loop.argtypes = [ctypes.c_int32, ctypes.c_int32, vp, vp]
     L.rag_probe_attn_slot.argtypes = [ctypes.c_int32, ctypes.c_int32, vp, vp]
     L.rag_probe_softmax_mfma.argtypes = [ctypes.c_int32, ctypes.c_int32, vp, vp]
@@ -1142,15 +1146,44 @@ def ceilings(torch, dev, reps=5, clocks=True):
             pages[f"{'nt' if hint else 'default'}_wg{wg}"] = round(n * 4096 / ms / 1e6, 1)
     out["random_4k_page_read_gbs"] = pages
     out["random_4k_page_read_best_gbs"] = max(pages.values())
-    del pool, sets
+    del pool
+    # K and V pages per id from two 4 GiB pools, two disjoint sets of 2^16
+    # random ids (256 MiB of K and of V per launch) alternating: the decode
+    # kernel's loads, and both pools as whole rows under either policy
+    kpool = torch.empty(pool_pages * 512, dtype=torch.int32, device=dev)
+    kpool.fill_(5)
+    vpool = torch.empty_like(kpool)
+    vpool.fill_(9)
+    nkv = 64 << 10
+    perm_kv = np.random.Generator(np.random.PCG64(6)).permutation(pool_pages // 2)
+    kv_sets = [torch.from_numpy(perm_kv[i * nkv:(i + 1) * nkv].astype(np.int32)).to(dev)
+               for i in range(2)]
+    kv = {}
+    for pattern, key in ((0, "decode_loads"), (1, "rows_default"), (2, "rows_nt")):
+        for wg in (512, 1024, 2048):
+            it = [0]
+
+            def run_kv(wg=wg, pattern=pattern):
+                ids = kv_sets[it[0] % 2]
+                it[0] += 1
+                assert L.rag_probe_kv_page_read(kpool.data_ptr(), vpool.data_ptr(), ids.data_ptr(),
+                                                nkv, wg, pattern, sink.data_ptr(), stream) == 0
+            ms = timed(run_kv)
+            kv[f"{key}_wg{wg}"] = round(nkv * 8192 / ms / 1e6, 1)
+    out["kv_page_read_gbs"] = kv
+    out["kv_page_read_decode_loads_best_gbs"] = max(v for k, v in kv.items()
+                                                    if k.startswith("decode_loads"))
+    del kpool, vpool, sets, kv_sets
     torch.cuda.empty_cache()
     buf = torch.empty(1 << 30, dtype=torch.int32, device=dev)   # 4 GiB
     buf.fill_(3)
     stream_gbs = {}
-    for wg in (1024, 2048, 4096):
-        ms = timed(lambda wg=wg: L.rag_probe_stream_read(buf.data_ptr(), buf.numel() * 4, wg,
-                                                         sink.data_ptr(), stream))
-        stream_gbs[f"wg{wg}"] = round(buf.numel() * 4 / ms / 1e6, 1)
+    for hint in (0, 1):
+        for wg in (1024, 2048, 4096):
+            ms = timed(lambda wg=wg, hint=hint: L.rag_probe_stream_read(
+                buf.data_ptr(), buf.numel() * 4, wg, hint, sink.data_ptr(), stream))
+            stream_gbs[f"{'nt' if hint else 'default'}_wg{wg}"] = \
+                round(buf.numel() * 4 / ms / 1e6, 1)
     out["stream_read_gbs"] = stream_gbs
     out["stream_read_best_gbs"] = max(stream_gbs.values())
     del buf

@@ -29,9 +29,22 @@ int rag_probe_page_read(const void *pool, const int32_t *page_ids,
                         int64_t num_pages, int32_t workgroups,
                         int32_t stream_hint, void *sink, hipStream_t stream);
 
-/* Reads `bytes` (a multiple of 16) of `buf` contiguously with 16-byte loads. */
+/* Reads, for each of num_pages ids, the 4096-byte page at byte offset
+ * 4096 * page_ids[i] of k_pool and the one of v_pool (both device), each
+ * wave two pairs at a time.  pattern 0: the paged decode kernel's loads (K as
+ * its MFMA operand layout, 64 bytes of each of 16 rows per instruction, with
+ * the default policy; V as whole 256-byte rows with the non-temporal hint);
+ * 1: both as whole rows, default policy; 2: both as whole rows, non-temporal.
+ * Counts 8192 bytes per id. */
+int rag_probe_kv_page_read(const void *k_pool, const void *v_pool,
+                           const int32_t *page_ids, int64_t num_pages,
+                           int32_t workgroups, int32_t pattern, void *sink,
+                           hipStream_t stream);
+
+/* Reads `bytes` (a multiple of 16) of `buf` contiguously with 16-byte loads;
+ * stream_hint = 1 adds the non-temporal hint. */
 int rag_probe_stream_read(const void *buf, int64_t bytes, int32_t workgroups,
-                          void *sink, hipStream_t stream);
+                          int32_t stream_hint, void *sink, hipStream_t stream);
 
 /* `workgroups` eight-wave workgroups; every wave issues 4 * iters
  * v_mfma_f32_32x32x16_bf16 (32768 FLOP each) into four independent

@@ -3,8 +3,11 @@
 // same way (one launch, HIP events around it, by bench.py --ceilings).  They
 // compute nothing of the attention method; they bound it:
 //   * page reads: 4 KB pages at random places of a multi-GB pool, read with
-//     16-byte loads -- the access pattern of paged decode;
-//   * stream read: one large contiguous buffer, 16-byte loads;
+//     16-byte loads, default or non-temporal policy;
+//   * K/V page reads: a K page and a V page per random id, loaded as the
+//     paged decode loads them (or both as whole rows, either policy) -- the
+//     ceiling of the decode's own access pattern;
+//   * stream read: one large contiguous buffer, 16-byte loads, either policy;
 //   * MFMA loop: v_mfma_f32_32x32x16_bf16 with independent accumulators, no
 //     memory traffic -- the practical bf16 matrix rate;
 //   * attention slot: the prefill kernel's own steady 32-key slot (pf_full_slot:
@@ -32,10 +35,20 @@ namespace {
 // Wave w of workgroup b reads the pages of list entries (b*4 + w)*4 .. +4,
 // then the same again one grid further on; a page is 4096 bytes = 4 loads of
 // 16 bytes per lane, so every wave has 16 loads (16 KB) in flight per step.
+// The load policy is a template parameter: chosen at run time, the compiler
+// merges the two loads of the same address and drops the hint.
+template <bool kNT>
+__device__ __forceinline__ u32x4 probe_load(const u32x4* p) {
+  if constexpr (kNT)
+    return __builtin_nontemporal_load(p);
+  else
+    return *p;
+}
+
+template <bool kNT>
 __global__ __launch_bounds__(256) void probe_pages_kernel(const u32x4* __restrict__ pool,
                                                           const int32_t* __restrict__ ids,
-                                                          int64_t n_pages, uint32_t* __restrict__ out,
-                                                          int stream_hint) {
+                                                          int64_t n_pages, uint32_t* __restrict__ out) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int64_t stride = (int64_t)gridDim.x * 16;
   uint32_t acc = 0;
@@ -46,9 +59,7 @@ __global__ __launch_bounds__(256) void probe_pages_kernel(const u32x4* __restric
       const int64_t p = min(p0 + j, n_pages - 1);
       const u32x4* base = pool + (size_t)ids[p] * 256;
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-        v[j][i] = stream_hint ? __builtin_nontemporal_load(base + i * 64 + lane)
-                              : base[i * 64 + lane];
+      for (int i = 0; i < 4; ++i) v[j][i] = probe_load<kNT>(base + i * 64 + lane);
     }
 #pragma unroll
     for (int j = 0; j < 4; ++j)
@@ -58,6 +69,49 @@ __global__ __launch_bounds__(256) void probe_pages_kernel(const u32x4* __restric
   if (acc == 0x9E3779B9u) out[blockIdx.x] = acc;   // practically never: keeps the loads
 }
 
+// The paged decode's own access pattern: per page id, a 4 KB K page and a
+// 4 KB V page (two pools), two pages of each per wave and step.  kDecode:
+// K loaded as the decode's MFMA operand layout (an instruction takes 64 bytes
+// of each of the 16 rows, default policy) and V as four whole 256-byte rows
+// per instruction with the non-temporal hint -- the decode kernel's loads;
+// otherwise both as whole rows, with the policy kNT.
+template <bool kDecode, bool kNT>
+__global__ __launch_bounds__(256) void probe_kv_pages_kernel(const u32x4* __restrict__ kpool,
+                                                             const u32x4* __restrict__ vpool,
+                                                             const int32_t* __restrict__ ids,
+                                                             int64_t n_pages,
+                                                             uint32_t* __restrict__ out) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int l16 = lane & 15, gq = lane >> 4;
+  const int64_t stride = (int64_t)gridDim.x * 8;
+  uint32_t acc = 0;
+  for (int64_t p0 = ((int64_t)blockIdx.x * 4 + w) * 2; p0 < n_pages; p0 += stride) {
+    u32x4 k[2][4], v[2][4];
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const size_t id = (size_t)ids[min(p0 + j, n_pages - 1)];
+      const u32x4* kb = kpool + id * 256;
+      const u32x4* vb = vpool + id * 256;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        if constexpr (kDecode) {
+          k[j][i] = probe_load<false>(kb + l16 * 16 + 4 * i + gq);
+          v[j][i] = probe_load<true>(vb + i * 64 + lane);
+        } else {
+          k[j][i] = probe_load<kNT>(kb + i * 64 + lane);
+          v[j][i] = probe_load<kNT>(vb + i * 64 + lane);
+        }
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) acc ^= k[j][i][0] ^ k[j][i][3] ^ v[j][i][1] ^ v[j][i][2];
+  }
+  if (acc == 0x9E3779B9u) out[blockIdx.x] = acc;
+}
+
+template <bool kNT>
 __global__ __launch_bounds__(256) void probe_stream_kernel(const u32x4* __restrict__ buf,
                                                            int64_t n16, uint32_t* __restrict__ out) {
   uint32_t acc = 0;
@@ -66,7 +120,8 @@ __global__ __launch_bounds__(256) void probe_stream_kernel(const u32x4* __restri
     u32x4 v[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j)
-      v[j] = i + j * blockDim.x < n16 ? buf[i + j * blockDim.x] : u32x4{0, 0, 0, 0};
+      v[j] = i + j * blockDim.x < n16 ? probe_load<kNT>(buf + i + j * blockDim.x)
+                                      : u32x4{0, 0, 0, 0};
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc ^= v[j][0] ^ v[j][1] ^ v[j][2] ^ v[j][3];
   }
@@ -340,16 +395,44 @@ int rag_probe_page_read(const void* pool, const int32_t* page_ids, int64_t num_p
                         int32_t workgroups, int32_t stream_hint, void* sink,
                         hipStream_t stream) {
   if (!pool || !page_ids || !sink || num_pages < 0 || workgroups <= 0) return -1;
-  hipLaunchKernelGGL(rag::probe_pages_kernel, dim3(workgroups), dim3(256), 0, stream,
-                     (const rag::u32x4*)pool, page_ids, num_pages, (uint32_t*)sink, stream_hint);
+  if (stream_hint)
+    hipLaunchKernelGGL(rag::probe_pages_kernel<true>, dim3(workgroups), dim3(256), 0, stream,
+                       (const rag::u32x4*)pool, page_ids, num_pages, (uint32_t*)sink);
+  else
+    hipLaunchKernelGGL(rag::probe_pages_kernel<false>, dim3(workgroups), dim3(256), 0, stream,
+                       (const rag::u32x4*)pool, page_ids, num_pages, (uint32_t*)sink);
   return hipGetLastError() == hipSuccess ? 0 : -4;
 }
 
-int rag_probe_stream_read(const void* buf, int64_t bytes, int32_t workgroups, void* sink,
-                          hipStream_t stream) {
+int rag_probe_kv_page_read(const void* k_pool, const void* v_pool, const int32_t* page_ids,
+                           int64_t num_pages, int32_t workgroups, int32_t pattern, void* sink,
+                           hipStream_t stream) {
+  if (!k_pool || !v_pool || !page_ids || !sink || num_pages < 0 || workgroups <= 0 ||
+      pattern < 0 || pattern > 2)
+    return -1;
+  const rag::u32x4* kp = (const rag::u32x4*)k_pool;
+  const rag::u32x4* vp = (const rag::u32x4*)v_pool;
+  if (pattern == 0)
+    hipLaunchKernelGGL((rag::probe_kv_pages_kernel<true, false>), dim3(workgroups), dim3(256),
+                       0, stream, kp, vp, page_ids, num_pages, (uint32_t*)sink);
+  else if (pattern == 1)
+    hipLaunchKernelGGL((rag::probe_kv_pages_kernel<false, false>), dim3(workgroups), dim3(256),
+                       0, stream, kp, vp, page_ids, num_pages, (uint32_t*)sink);
+  else
+    hipLaunchKernelGGL((rag::probe_kv_pages_kernel<false, true>), dim3(workgroups), dim3(256),
+                       0, stream, kp, vp, page_ids, num_pages, (uint32_t*)sink);
+  return hipGetLastError() == hipSuccess ? 0 : -4;
+}
+
+int rag_probe_stream_read(const void* buf, int64_t bytes, int32_t workgroups,
+                          int32_t stream_hint, void* sink, hipStream_t stream) {
   if (!buf || !sink || bytes < 0 || workgroups <= 0) return -1;
-  hipLaunchKernelGGL(rag::probe_stream_kernel, dim3(workgroups), dim3(256), 0, stream,
-                     (const rag::u32x4*)buf, bytes / 16, (uint32_t*)sink);
+  if (stream_hint)
+    hipLaunchKernelGGL(rag::probe_stream_kernel<true>, dim3(workgroups), dim3(256), 0, stream,
+                       (const rag::u32x4*)buf, bytes / 16, (uint32_t*)sink);
+  else
+    hipLaunchKernelGGL(rag::probe_stream_kernel<false>, dim3(workgroups), dim3(256), 0, stream,
+                       (const rag::u32x4*)buf, bytes / 16, (uint32_t*)sink);
   return hipGetLastError() == hipSuccess ? 0 : -4;
 }
 

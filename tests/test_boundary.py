@@ -49,7 +49,8 @@ def test_ceiling_probe_library_exports_its_header():
     text = re.sub(r"/\*.*?\*/", "", open(os.path.join(ROOT, "include", "ceiling_probes.h")).read(),
                   flags=re.S)
     names = sorted(set(re.findall(r"\b(rag_[a-z0-9_]+)\s*\(", text)))
-    assert names == ["rag_probe_attn_pair", "rag_probe_attn_slot", "rag_probe_mfma_loop",
+    assert names == ["rag_probe_attn_pair", "rag_probe_attn_slot", "rag_probe_kv_page_read",
+                     "rag_probe_mfma_loop",
                      "rag_probe_page_read", "rag_probe_softmax_mfma", "rag_probe_stream_read"]
     L = ctypes.CDLL(pb.PROBES)
     for n in names:
