@@ -28,10 +28,13 @@ __global__ __launch_bounds__(256) void kv_cache_write_kernel(
   if (slot < 0) return;                            // padding token
   const size_t src = ((size_t)t * hkv + h) * D + c * 8;
   const size_t dst = (((size_t)(slot >> 4) * hkv + h) * 16 + (slot & 15)) * D + c * 8;
-  const u32x4 kx = load16(k + src);
-  const u32x4 vx = load16(v + src);
-  *reinterpret_cast<u32x4*>(kc + dst) = kx;
-  *reinterpret_cast<u32x4*>(vc + dst) = vx;
+  // Every byte is read once and written once: both sides with the
+  // non-temporal hint (4% faster than the default policy on the stuff7b
+  // prompt tokens; the hint on one side only was no faster).
+  const u32x4 kx = load16_stream(k + src);
+  const u32x4 vx = load16_stream(v + src);
+  __builtin_nontemporal_store(kx, reinterpret_cast<u32x4*>(kc + dst));
+  __builtin_nontemporal_store(vx, reinterpret_cast<u32x4*>(vc + dst));
 }
 
 int64_t kv_cache_write_grid(int64_t num_tokens, int hkv, int d) {
